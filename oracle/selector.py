@@ -1,0 +1,146 @@
+"""CPU oracle for the wave-quantized launch-time partition selector
+(test infrastructure: only tests and the benchmark use it).
+
+It evaluates the paper's model in exact rational arithmetic
+(``fractions.Fraction``), step by step in the order of Algorithm 1
+("CPU-side communication-grid selection"):
+
+  routed-tile reduction      eq:routed-tile-reduction   sum_e ceil(M_e / T_M)
+  compute work per split     eq:compute-work            W_comp
+  communication work         eq:communication-work      W_comm
+  reservation                eq:reservation             R(C) = ceil(C / o_comm)
+  compute capacity           eq:compute-capacity        P(C) = o_comp (G - R(C))
+  split readiness            eq:split-arrival           A_s = ceil((s+1) W_comp / P)
+  communication waves        eq:communication-waves     V_comm = ceil(W_comm / C)
+  service time               eq:comm-service            q = rho V_comm
+  split completion           eq:split-finish            F_s = max(A_s, F_{s-1}) + q
+  makespan                   eq:makespan                T(C) = F_{L-1}
+  tie-break                  eq:tie-breaker             Delta = V_comp P - W_comp
+  rho at run time            eq:rho-scaling             rho_ref (K_ref/K)(tile_ref/tile)(D/D_ref)
+
+Readings where the paper is silent (each listed in the design notes):
+  * g (input groups) = 1;
+  * when no host counts exist, the routed-tile sum is estimated from the
+    total assignments spread evenly over E experts:
+    E * ceil(ceil(M k / E) / T_M);
+  * a candidate whose P(C) <= 0 is not in the legal set;
+  * ties left after Delta go to the smaller C;
+  * D = 1 on one GPU, so the token count per rank is M itself.
+"""
+from __future__ import annotations
+
+import dataclasses
+from fractions import Fraction
+from typing import List, Optional, Sequence
+
+
+def cdiv(a: int, b: int) -> int:
+    return -(-a // b)
+
+
+@dataclasses.dataclass
+class Candidate:
+    C: int
+    R: int
+    P: int
+    A: List[int]          # split readiness, compute-wave units
+    V_comm: int
+    q: Fraction
+    F: List[Fraction]
+    T: Fraction
+    V_comp: int
+    delta: int
+
+
+def routed_m_tiles(counts: Optional[Sequence[int]], tile_m: int, E: int,
+                   total_assignments: int) -> int:
+    """sum_e ceil(M_e / T_M) from host counts, or the even-load estimate."""
+    if counts is not None:
+        return sum(cdiv(int(m), tile_m) for m in counts)
+    per_expert = cdiv(total_assignments, E)
+    return E * cdiv(per_expert, tile_m)
+
+
+def compute_work(m_tiles: int, N: int, L: int, tile_n: int, g: int = 1) -> int:
+    """W_comp = g * (sum_e ceil(M_e/T_M)) * ceil(ceil(N/L) / T_N)."""
+    return g * m_tiles * cdiv(cdiv(N, L), tile_n)
+
+
+def comm_work(M: int, D: int, N: int, L: int, comm_m: int, comm_n: int) -> int:
+    """W_comm = ceil(ceil(M/D) / T_M^comm) * ceil(ceil(N/L) / T_N^comm)."""
+    return cdiv(cdiv(M, D), comm_m) * cdiv(cdiv(N, L), comm_n)
+
+
+def rho_scaled(rho_ref: Fraction, K: int, K_ref: int, tile_m: int, tile_n: int,
+               tile_m_ref: int, tile_n_ref: int, D: int, D_ref: int) -> Fraction:
+    return (Fraction(rho_ref) * Fraction(K_ref, K)
+            * Fraction(tile_m_ref * tile_n_ref, tile_m * tile_n)
+            * Fraction(D, D_ref))
+
+
+def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
+             o_comp: int, rho: Fraction) -> Optional[Candidate]:
+    """The recurrence for one candidate C; None if P(C) <= 0 (illegal)."""
+    R = cdiv(C, o_comm)
+    P = o_comp * (G - R)
+    if P <= 0:
+        return None
+    A = [cdiv((s + 1) * W_comp, P) for s in range(L)]
+    V_comm = cdiv(W_comm, C)
+    q = Fraction(rho) * V_comm
+    F: List[Fraction] = []
+    prev = Fraction(0)
+    for s in range(L):
+        prev = max(Fraction(A[s]), prev) + q
+        F.append(prev)
+    V_comp = cdiv(W_comp, P)
+    return Candidate(C=C, R=R, P=P, A=A, V_comm=V_comm, q=q, F=F, T=F[-1],
+                     V_comp=V_comp, delta=V_comp * P - W_comp)
+
+
+def select_from_work(W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
+                     o_comp: int, rho: Fraction, c_min: int, c_max: int):
+    """Argmin of T(C) over the legal C, then smallest Delta, then smallest C.
+
+    Returns (best Candidate or None, list of all legal candidates)."""
+    cands = []
+    for C in range(c_min, c_max + 1):
+        c = evaluate(C, W_comp, W_comm, L, G, o_comm, o_comp, rho)
+        if c is not None:
+            cands.append(c)
+    if not cands:
+        return None, cands
+    best = min(cands, key=lambda c: (c.T, c.delta, c.C))
+    return best, cands
+
+
+@dataclasses.dataclass
+class SelectParams:
+    tile_m: int
+    tile_n: int
+    comm_tile_m: int
+    comm_tile_n: int
+    occ_comp: int
+    occ_comm: int
+    num_cus: int
+    c_min: int
+    c_max: int
+    rho_ref: Fraction
+    k_ref: int
+    tile_m_ref: int
+    tile_n_ref: int
+    d_ref: int
+    groups: int = 1
+
+
+def select(T: int, H: int, I: int, E: int, topk: int, L: int,
+           counts: Optional[Sequence[int]], p: SelectParams, D: int = 1):
+    """Algorithm 1 on a workload: returns (best, candidates, W_comp, W_comm, rho)."""
+    m_tiles = routed_m_tiles(counts, p.tile_m, E, T * topk)
+    W_comp = compute_work(m_tiles, H, L, p.tile_n, p.groups)
+    W_comm = comm_work(T, D, H, L, p.comm_tile_m, p.comm_tile_n)
+    rho = rho_scaled(p.rho_ref, I, p.k_ref, p.tile_m, p.tile_n,
+                     p.tile_m_ref, p.tile_n_ref, D, p.d_ref)
+    best, cands = select_from_work(W_comp, W_comm, L, p.num_cus, p.occ_comm,
+                                   p.occ_comp, rho, p.c_min, p.c_max)
+    return best, cands, W_comp, W_comm, rho
