@@ -1,0 +1,196 @@
+/*
+ * moe_gemm2.h - C ABI of the MI355X MoE down-projection + combine stage and
+ * its launch-time partition selector.
+ *
+ * The operation (paper: Background, "Distributed MoE Execution", third step;
+ * Method, "System Integration and Correctness"):
+ *
+ *   Y[r, :]   = x_perm[r, :] @ W2[e(r)]      e(r): expert_offsets[e] <= r < expert_offsets[e+1]
+ *   out[t, :] = sum over rows r with token_ids[r] == t of gate_w[r] * Y[r, :]
+ *
+ * computed by one persistent kernel whose workgroups take one of two roles:
+ * compute workgroups run the grouped GEMM tile by tile and publish each
+ * finished tile with a readiness flag and a per-split counter; consumer
+ * workgroups wait until a split is published and then gather each token's
+ * rows, weight them by the gates and write the token's output once.  The
+ * number of consumer workgroups C is the paper's decision variable; the
+ * selector below evaluates its wave-quantized makespan model (Method,
+ * "Wave-Quantized Pipeline Model" and Algorithm 1) to choose it.
+ *
+ * Conventions for every function:
+ *   - all functions are extern "C"; none throws, aborts or prints;
+ *   - a negative return value is a moe_status_t error; 0 or a documented
+ *     non-negative value is success;
+ *   - device pointers are plain HIP device addresses; the caller allocates
+ *     and owns every buffer, including the workspace; the library allocates
+ *     no device memory;
+ *   - "stream" is a hipStream_t passed as void* (NULL = the null stream);
+ *     calls that take one only enqueue work on it and return without
+ *     synchronising, except moe_gemm2_status;
+ *   - tensors are dense and row-major.
+ */
+#ifndef MOE_GEMM2_H
+#define MOE_GEMM2_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = -1,        /* null pointer, bad dimension or bad parameter */
+  MOE_ERR_ALIGNMENT = -2,          /* a pointer is not aligned as documented */
+  MOE_ERR_WORKSPACE = -3,          /* workspace missing or smaller than moe_gemm2_workspace_size */
+  MOE_ERR_NO_LEGAL_PARTITION = -4, /* no C in [c_min, c_max] leaves P(C) > 0 */
+  MOE_ERR_HIP = -5,                /* a HIP runtime call failed (no device, launch error, ...) */
+  MOE_ERR_TIMEOUT = -6,            /* a consumer's bounded wait expired (reported by moe_gemm2_status) */
+  MOE_ERR_UNSUPPORTED = -7,        /* shape outside what the kernel handles (see moe_gemm2_combine) */
+  MOE_ERR_BAD_ROUTING = -8         /* device saw a token id outside [0,T), a token with more than
+                                      topk rows, or offsets that are not a non-decreasing prefix
+                                      of [0, rows] (reported by moe_gemm2_status) */
+} moe_status_t;
+
+/* One invocation's workload (paper: Table "Workload and tile notation").
+ *   T      tokens before top-k expansion (M; one GPU, so D = 1 and M/D = T)
+ *   H      hidden size = GEMM2 output width (N)
+ *   I      local expert intermediate size = GEMM2 reduction length (K)
+ *   E      local experts
+ *   topk   maximum routed rows per token (k)
+ *   splits pipeline splits along H (L), >= 1
+ *   ranks  participating ranks (D) for the service-rate scaling; 1 on one GPU
+ *   rows   permuted rows = expert_offsets[E]; 0 means T * topk
+ *   host_expert_counts  optional host array [E] of routed rows per expert
+ *          (M_e); NULL makes the selector use the even-load estimate. */
+typedef struct {
+  int32_t T, H, I, E, topk, splits, ranks;
+  int64_t rows;
+  const int32_t* host_expert_counts;
+} moe_workload_t;
+
+/* Kernel and GPU residency facts the selector needs (paper: Table "Resource
+ * notation"; Method, "Launch-Time Analytical Selection"), plus the
+ * service-time ratio rho_ref measured once at a reference configuration
+ * (eq:rho-reference) and that configuration (eq:rho-config). */
+typedef struct {
+  int32_t tile_m, tile_n;            /* compute tile T_M^comp x T_N^comp */
+  int32_t comm_tile_m, comm_tile_n;  /* consumer task tile T_M^comm x T_N^comm */
+  int32_t occ_comp, occ_comm;        /* resident workgroups per CU of each role */
+  int32_t num_cus;                   /* G */
+  int32_t c_min, c_max;              /* legal candidates, eq:c-domain */
+  int32_t groups;                    /* g, input groups (1) */
+  int64_t rho_ref_num, rho_ref_den;  /* rho_ref as a positive rational */
+  int32_t k_ref, tile_m_ref, tile_n_ref, d_ref;
+} moe_select_params_t;
+
+/* The chosen partition.  T(C) = T_num / T_den in compute-wave units; W_comp
+ * and W_comm are the per-split work counts (eq:compute-work,
+ * eq:communication-work); delta_comp is eq:tie-breaker. */
+typedef struct {
+  int32_t C, R, P, delta_comp;
+  int64_t T_num, T_den;
+  int64_t W_comp, W_comm;
+} moe_partition_t;
+
+/* Algorithm 1: for C = c_min..c_max compute R(C) = ceil(C/o_comm)
+ * (eq:reservation), P(C) = o_comp (G - R(C)) (eq:compute-capacity), the split
+ * readiness times A_s (eq:split-arrival), V_comm (eq:communication-waves),
+ * q = rho V_comm (eq:comm-service) with rho from eq:rho-scaling, and the
+ * completion recurrence F_s (eq:split-finish); return the C with the least
+ * T(C) = F_{L-1} (eq:makespan), ties to the least Delta_comp
+ * (eq:tie-breaker), then to the least C.  Candidates with P(C) <= 0 are
+ * illegal.  Arithmetic is exact (rational rho, integer time).
+ * Pure host code: no HIP call, no allocation, thread-safe.
+ * Returns C* >= 1 and fills *out when out != NULL; MOE_ERR_INVALID_ARG for a
+ * null wl/p, non-positive dimensions or parameters, a negative host count or
+ * arithmetic overflow; MOE_ERR_NO_LEGAL_PARTITION when no candidate is legal. */
+int moe_select_partition(const moe_workload_t* wl, const moe_select_params_t* p,
+                         moe_partition_t* out);
+
+/* The whole T(C) table of the same model: T_num_out[i] is the numerator of
+ * T(c_min + i) over the common denominator *T_den_out, or -1 where P <= 0.
+ * n must be >= c_max - c_min + 1.  Returns the number of entries written, or
+ * a negative status as moe_select_partition does. */
+int moe_select_evaluate(const moe_workload_t* wl, const moe_select_params_t* p,
+                        int64_t* T_num_out, int32_t n, int64_t* T_den_out);
+
+/* Parameters for the fused kernel on a HIP device: its tile shapes, its
+ * occupancy from hipOccupancyMaxActiveBlocksPerMultiprocessor, the device's
+ * CU count and the MI355X calibration of rho_ref.  Device facts are cached
+ * on first use (Method, "System Integration and Correctness").  Returns 0 or
+ * MOE_ERR_HIP / MOE_ERR_INVALID_ARG. */
+int moe_gemm2_default_params(int device, moe_select_params_t* out);
+
+/* Bytes of workspace moe_gemm2_combine needs for this workload (flags,
+ * counters, the token->rows inverse map and the bf16 staging of Y).
+ * Returns 0 for an invalid workload. */
+size_t moe_gemm2_workspace_size(const moe_workload_t* wl);
+
+/* Zero a workspace (required once after allocating it, before its first
+ * use).  Enqueued on stream.  Returns 0 or MOE_ERR_HIP / MOE_ERR_INVALID_ARG. */
+int moe_gemm2_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
+
+/* The stage.
+ *   x_perm          device bf16 [rows, I], rows grouped by expert (16-byte aligned)
+ *   w2              device bf16 [E, I, H], H contiguous (16-byte aligned)
+ *   expert_offsets  device int32 [E+1]: 0 = offsets[0] <= ... <= offsets[E] = rows
+ *   token_ids       device int32 [rows]: token of each permuted row, in [0, T);
+ *                   a token may own at most topk rows (fewer is allowed: dropped slots)
+ *   gate_w          device fp32 [rows]: gate weight of each permuted row
+ *   out             device fp32 [T, H] (16-byte aligned): fully overwritten
+ *                   (tokens without rows get zeros); never read
+ *   wl              dimensions (+ optional host counts for the selector)
+ *   num_consumers   >= 1: that many consumer workgroups (an explicit choice
+ *                   wins, Method "System Integration and Correctness");
+ *                   0: no dedicated consumers, every workgroup computes its
+ *                   tiles and then takes consumer tasks;
+ *                   -1: chosen by moe_select_partition with
+ *                   moe_gemm2_default_params, unless the environment sets
+ *                   MOE_GEMM2_SELECTOR=0, which restores a fixed C = 8
+ *   workspace       device memory of at least moe_gemm2_workspace_size(wl)
+ *                   bytes, 256-byte aligned, zeroed once by
+ *                   moe_gemm2_workspace_init; calls that may overlap in
+ *                   time need distinct workspaces
+ *   stream          hipStream_t the kernel is enqueued on
+ * Supported shapes: H % (8 * splits) == 0, I % 8 == 0, 1 <= E <= 1024,
+ * 1 <= topk <= 64, splits <= 16 (else MOE_ERR_UNSUPPORTED).
+ * Values inside device arrays are checked by the kernel, which skips bad
+ * entries and records MOE_ERR_BAD_ROUTING for moe_gemm2_status.
+ * Returns the number of consumer workgroups launched (>= 0) or a negative
+ * status (host-side validation and launch errors only). */
+int moe_gemm2_combine(const void* x_perm, const void* w2, const int32_t* expert_offsets,
+                      const int32_t* token_ids, const float* gate_w, float* out,
+                      const moe_workload_t* wl, int32_t num_consumers,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Same as moe_gemm2_combine, and also records timestamps (the device's
+ * constant 100 MHz clock) into trace (device, 8-byte aligned, at least
+ * moe_gemm2_trace_size(wl) bytes): per compute tile its start and publish
+ * time, per consumer task its wait start, wait end and finish time.  The
+ * arithmetic and the result are identical to the untraced call. */
+int moe_gemm2_combine_traced(const void* x_perm, const void* w2, const int32_t* expert_offsets,
+                             const int32_t* token_ids, const float* gate_w, float* out,
+                             const moe_workload_t* wl, int32_t num_consumers,
+                             void* workspace, size_t workspace_bytes, void* stream,
+                             uint64_t* trace, size_t trace_bytes);
+
+/* Bytes the trace buffer needs for this workload (0 for an invalid one). */
+size_t moe_gemm2_trace_size(const moe_workload_t* wl);
+
+/* Synchronises stream, then reports the device-side status of the last
+ * launches that used this workspace: 0, MOE_ERR_TIMEOUT or
+ * MOE_ERR_BAD_ROUTING (or MOE_ERR_HIP).  clear != 0 resets it. */
+int moe_gemm2_status(void* workspace, void* stream, int clear);
+
+/* Static description of an error code. */
+const char* moe_strerror(int status);
+
+/* ABI version of this header (major * 100 + minor). */
+int moe_gemm2_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_GEMM2_H */

@@ -1,0 +1,187 @@
+// Launch-time partition selector: the wave-quantized makespan model of the
+// paper's Method section, evaluated exactly on the host.
+//
+// Time is kept as an integer count of 1/rho_den compute waves, where
+// rho = rho_num / rho_den is the reduced service-time ratio of eq:rho-scaling,
+// so T(C) compares exactly and ties (eq:tie-breaker) are real ties.
+//
+//   W_comp = g * (sum_e ceil(M_e/T_M)) * ceil(ceil(N/L)/T_N)       eq:compute-work
+//   W_comm = ceil(ceil(M/D)/T_M^comm) * ceil(ceil(N/L)/T_N^comm)    eq:communication-work
+//   R(C)   = ceil(C/o_comm)                                         eq:reservation
+//   P(C)   = o_comp (G - R(C))                                      eq:compute-capacity
+//   A_s    = ceil((s+1) W_comp / P(C))                              eq:split-arrival
+//   q      = rho ceil(W_comm / C)                                   eq:comm-service
+//   F_s    = max(A_s, F_{s-1}) + q,  T(C) = F_{L-1}                 eq:split-finish, eq:makespan
+//   Delta  = ceil(W_comp/P) P - W_comp                              eq:tie-breaker
+#include <cstdint>
+#include <cstdlib>
+
+#include "moe_gemm2.h"
+
+namespace {
+
+typedef __int128 i128;
+
+const i128 kI64Max = (i128)INT64_MAX;
+
+inline int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+struct Model {
+  int64_t W_comp = 0, W_comm = 0;
+  int64_t rho_num = 0, rho_den = 1;
+  int L = 1;
+};
+
+// Builds the per-split work counts and the scaled rho; returns a status.
+int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m) {
+  if (!wl || !p) return MOE_ERR_INVALID_ARG;
+  if (wl->T < 0 || wl->H <= 0 || wl->I <= 0 || wl->E <= 0 || wl->topk <= 0 ||
+      wl->splits <= 0 || wl->ranks <= 0 || wl->rows < 0)
+    return MOE_ERR_INVALID_ARG;
+  if (p->tile_m <= 0 || p->tile_n <= 0 || p->comm_tile_m <= 0 || p->comm_tile_n <= 0 ||
+      p->occ_comp <= 0 || p->occ_comm <= 0 || p->num_cus <= 0 || p->c_min < 1 ||
+      p->c_max < p->c_min || p->groups <= 0 || p->rho_ref_num <= 0 || p->rho_ref_den <= 0 ||
+      p->k_ref <= 0 || p->tile_m_ref <= 0 || p->tile_n_ref <= 0 || p->d_ref <= 0)
+    return MOE_ERR_INVALID_ARG;
+
+  // eq:routed-tile-reduction, or the even-load estimate when the counts only
+  // live on the device (Method, "System Integration and Correctness").
+  int64_t m_tiles = 0;
+  if (wl->host_expert_counts) {
+    for (int e = 0; e < wl->E; ++e) {
+      int64_t me = wl->host_expert_counts[e];
+      if (me < 0) return MOE_ERR_INVALID_ARG;
+      m_tiles += cdiv64(me, p->tile_m);
+    }
+  } else {
+    int64_t total = wl->rows > 0 ? wl->rows : (int64_t)wl->T * wl->topk;
+    m_tiles = (int64_t)wl->E * cdiv64(cdiv64(total, wl->E), p->tile_m);
+  }
+  const int64_t n_split = cdiv64(wl->H, wl->splits);
+  m->W_comp = (int64_t)p->groups * m_tiles * cdiv64(n_split, p->tile_n);
+  m->W_comm = cdiv64(cdiv64(wl->T, wl->ranks), p->comm_tile_m) * cdiv64(n_split, p->comm_tile_n);
+  m->L = wl->splits;
+
+  // eq:rho-scaling: rho = rho_ref (K_ref/K) (T_M,ref T_N,ref)/(T_M T_N) (D/D_ref)
+  i128 num = (i128)p->rho_ref_num * p->k_ref * p->tile_m_ref * p->tile_n_ref * wl->ranks;
+  i128 den = (i128)p->rho_ref_den * wl->I * p->tile_m * p->tile_n * p->d_ref;
+  // reduce in 128 bits, then require both to fit in 63 bits
+  i128 a = num, b = den;
+  while (b != 0) {
+    i128 t = a % b;
+    a = b;
+    b = t;
+  }
+  num /= a;
+  den /= a;
+  if (num > kI64Max || den > kI64Max) return MOE_ERR_INVALID_ARG;
+  m->rho_num = (int64_t)num;
+  m->rho_den = (int64_t)den;
+  return MOE_OK;
+}
+
+// One candidate; returns false if P(C) <= 0.  Status MOE_ERR_INVALID_ARG on
+// overflow of the scaled integer time.
+bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int64_t* T_out,
+                    int64_t* delta_out, int32_t* R_out, int32_t* P_out, int* status) {
+  const int64_t R = cdiv64(C, p->occ_comm);
+  const int64_t P = (int64_t)p->occ_comp * ((int64_t)p->num_cus - R);
+  if (P <= 0) return false;
+  const i128 q = (i128)m.rho_num * cdiv64(m.W_comm, C);
+  i128 F = 0;
+  for (int s = 0; s < m.L; ++s) {
+    const i128 A = (i128)cdiv64((int64_t)(s + 1) * m.W_comp, P) * m.rho_den;
+    F = (A > F ? A : F) + q;
+    if (F > kI64Max) {
+      *status = MOE_ERR_INVALID_ARG;
+      return false;
+    }
+  }
+  const int64_t V_comp = cdiv64(m.W_comp, P);
+  *T_out = (int64_t)F;
+  *delta_out = V_comp * P - m.W_comp;
+  *R_out = (int32_t)R;
+  *P_out = (int32_t)P;
+  return true;
+}
+
+}  // namespace
+
+extern "C" int moe_select_partition(const moe_workload_t* wl, const moe_select_params_t* p,
+                                    moe_partition_t* out) {
+  Model m;
+  int st = build_model(wl, p, &m);
+  if (st != MOE_OK) return st;
+  bool found = false;
+  int64_t bestT = 0, bestD = 0;
+  int32_t bestC = 0, bestR = 0, bestP = 0;
+  for (int32_t C = p->c_min; C <= p->c_max; ++C) {
+    int64_t T, D;
+    int32_t R, P;
+    st = MOE_OK;
+    if (!eval_candidate(m, p, C, &T, &D, &R, &P, &st)) {
+      if (st != MOE_OK) return st;
+      continue;
+    }
+    // lexicographic (T, Delta, C); C ascends, so strict improvement only
+    if (!found || T < bestT || (T == bestT && D < bestD)) {
+      found = true;
+      bestT = T;
+      bestD = D;
+      bestC = C;
+      bestR = R;
+      bestP = P;
+    }
+  }
+  if (!found) return MOE_ERR_NO_LEGAL_PARTITION;
+  if (out) {
+    out->C = bestC;
+    out->R = bestR;
+    out->P = bestP;
+    out->delta_comp = (int32_t)bestD;
+    out->T_num = bestT;
+    out->T_den = m.rho_den;
+    out->W_comp = m.W_comp;
+    out->W_comm = m.W_comm;
+  }
+  return bestC;
+}
+
+extern "C" int moe_select_evaluate(const moe_workload_t* wl, const moe_select_params_t* p,
+                                   int64_t* T_num_out, int32_t n, int64_t* T_den_out) {
+  Model m;
+  int st = build_model(wl, p, &m);
+  if (st != MOE_OK) return st;
+  const int32_t count = p->c_max - p->c_min + 1;
+  if (!T_num_out || n < count) return MOE_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < count; ++i) {
+    int64_t T, D;
+    int32_t R, P;
+    st = MOE_OK;
+    if (eval_candidate(m, p, p->c_min + i, &T, &D, &R, &P, &st)) {
+      T_num_out[i] = T;
+    } else {
+      if (st != MOE_OK) return st;
+      T_num_out[i] = -1;
+    }
+  }
+  if (T_den_out) *T_den_out = m.rho_den;
+  return count;
+}
+
+extern "C" const char* moe_strerror(int status) {
+  switch (status) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_INVALID_ARG: return "invalid argument";
+    case MOE_ERR_ALIGNMENT: return "misaligned pointer";
+    case MOE_ERR_WORKSPACE: return "workspace missing or too small";
+    case MOE_ERR_NO_LEGAL_PARTITION: return "no legal partition: every candidate leaves P(C) <= 0";
+    case MOE_ERR_HIP: return "HIP runtime error";
+    case MOE_ERR_TIMEOUT: return "a consumer wait timed out";
+    case MOE_ERR_UNSUPPORTED: return "unsupported shape";
+    case MOE_ERR_BAD_ROUTING: return "bad routing data on the device";
+    default: return status >= 0 ? "ok" : "unknown error";
+  }
+}
+
+extern "C" int moe_gemm2_abi_version(void) { return 100; }

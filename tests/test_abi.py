@@ -1,0 +1,193 @@
+"""The C ABI on the CPU: exports, the selector (bit-exact against the Python
+oracle) and host-side validation.  Nothing here launches GPU work."""
+import os
+import random
+import re
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import selector as osel
+from paper_2609_07536_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "moe_gemm2.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    L = B.lib()
+    declared = _declared_functions()
+    assert len(declared) >= 11
+    for name in declared:
+        assert hasattr(L, name), name
+    assert set(declared) == set(B.EXPORTED)
+    assert L.moe_gemm2_abi_version() == 100
+
+
+def _params(**kw):
+    p = B.SelectParams(tile_m=256, tile_n=256, comm_tile_m=128, comm_tile_n=1024,
+                       occ_comp=1, occ_comm=1, num_cus=256, c_min=1, c_max=64, groups=1,
+                       rho_ref_num=4, rho_ref_den=3, k_ref=704, tile_m_ref=256,
+                       tile_n_ref=256, d_ref=1)
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+def _oracle_params(p):
+    return osel.SelectParams(
+        tile_m=p.tile_m, tile_n=p.tile_n, comm_tile_m=p.comm_tile_m,
+        comm_tile_n=p.comm_tile_n, occ_comp=p.occ_comp, occ_comm=p.occ_comm,
+        num_cus=p.num_cus, c_min=p.c_min, c_max=p.c_max,
+        rho_ref=Fraction(p.rho_ref_num, p.rho_ref_den), k_ref=p.k_ref,
+        tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups)
+
+
+def test_hand_example_through_the_abi():
+    """G=10, o_comm=1, o_comp=2, W_comp=30, W_comm=6, L=2, rho=3/2 (C* = 5)."""
+    # one expert with 30 rows, 1-row tiles, 2 columns in 2 splits of 1 column,
+    # 30 tokens in comm tiles of 5 tokens: W_comp = 30, W_comm = 6
+    p = _params(tile_m=1, tile_n=1, comm_tile_m=5, comm_tile_n=1, occ_comp=2,
+                occ_comm=1, num_cus=10, c_max=6, rho_ref_num=3, rho_ref_den=2,
+                k_ref=8, tile_m_ref=1, tile_n_ref=1)
+    wl, keep = B.make_workload(T=30, H=2, I=8, E=1, topk=1, splits=2, counts=[30])
+    r, part = B.select_partition(wl, p)
+    assert r == 5 and part.C == 5 and part.P == 10 and part.R == 5
+    assert part.W_comp == 30 and part.W_comm == 6
+    assert Fraction(part.T_num, part.T_den) == 9 and part.delta_comp == 0
+    n, table, den = B.select_evaluate(wl, p)
+    want = [20, 11, 9, 9, 9, Fraction(19, 2)]
+    assert [Fraction(t, den) for t in table] == want
+    p.c_max = 4
+    r, part = B.select_partition(wl, p)
+    assert r == 4
+
+
+def _random_case(rnd):
+    E = rnd.randint(1, 64)
+    topk = rnd.randint(1, min(E, 8))
+    T = rnd.randint(0, 40000)
+    L = rnd.randint(1, 4)
+    H = 8 * L * rnd.randint(1, 512)
+    I = 8 * rnd.randint(1, 200)
+    counts = None
+    if rnd.random() < 0.8:
+        w = np.array([rnd.random() ** 3 for _ in range(E)])
+        c = np.floor(w / w.sum() * T * topk).astype(np.int64)
+        c[0] += T * topk - c.sum()
+        counts = [int(v) for v in c]
+    p = _params(tile_m=rnd.choice([64, 128, 256]), tile_n=rnd.choice([64, 128, 256]),
+                comm_tile_m=rnd.choice([64, 128]), comm_tile_n=rnd.choice([512, 1024]),
+                occ_comp=rnd.randint(1, 3), occ_comm=rnd.randint(1, 3),
+                num_cus=rnd.choice([8, 64, 108, 256, 304]), c_min=1,
+                c_max=rnd.randint(1, 80), rho_ref_num=rnd.randint(1, 100000),
+                rho_ref_den=rnd.randint(1, 10000), k_ref=rnd.choice([352, 704, 1408]),
+                tile_m_ref=rnd.choice([128, 256]), tile_n_ref=rnd.choice([128, 256]),
+                d_ref=rnd.choice([1, 4]))
+    D = rnd.choice([1, 1, 2, 4])
+    return T, H, I, E, topk, L, counts, p, D
+
+
+def test_selector_bit_exact_against_oracle():
+    rnd = random.Random(2024)
+    n_checked = 0
+    for _ in range(3000):
+        T, H, I, E, topk, L, counts, p, D = _random_case(rnd)
+        wl, keep = B.make_workload(T, H, I, E, topk, L, counts, ranks=D)
+        r, part = B.select_partition(wl, p)
+        best, cands, W_comp, W_comm, rho = osel.select(T, H, I, E, topk, L, counts,
+                                                        _oracle_params(p), D=D)
+        if best is None:
+            assert r == B.MOE_ERR_NO_LEGAL_PARTITION
+            continue
+        assert r == best.C
+        assert (part.C, part.R, part.P, part.delta_comp) == (best.C, best.R, best.P, best.delta)
+        assert (part.W_comp, part.W_comm) == (W_comp, W_comm)
+        assert part.T_den == rho.denominator
+        assert Fraction(part.T_num, part.T_den) == best.T
+        # whole table
+        n, table, den = B.select_evaluate(wl, p)
+        assert n == p.c_max - p.c_min + 1
+        byC = {c.C: c.T for c in cands}
+        for i, tnum in enumerate(table):
+            C = p.c_min + i
+            if C in byC:
+                assert Fraction(tnum, den) == byC[C]
+            else:
+                assert tnum == -1
+        n_checked += 1
+    assert n_checked > 2000
+
+
+def test_selector_argument_errors():
+    p = _params()
+    wl, keep = B.make_workload(T=100, H=2048, I=704, E=4, topk=2, splits=2,
+                               counts=[50, 50, 50, 50])
+    assert B.select_partition(wl, p)[0] >= 1
+    for field, bad in [("c_min", 0), ("occ_comp", 0), ("num_cus", 0), ("rho_ref_den", 0),
+                       ("rho_ref_num", -3), ("tile_m", 0)]:
+        q = _params(**{field: bad})
+        assert B.select_partition(wl, q)[0] == B.MOE_ERR_INVALID_ARG, field
+    q = _params(c_min=10, c_max=5)
+    assert B.select_partition(wl, q)[0] == B.MOE_ERR_INVALID_ARG
+    bad_wl, k2 = B.make_workload(T=100, H=2048, I=704, E=4, topk=2, splits=2,
+                                 counts=[50, -1, 50, 50])
+    assert B.select_partition(bad_wl, p)[0] == B.MOE_ERR_INVALID_ARG
+    # P(C) <= 0 for every candidate
+    q = _params(num_cus=4, c_min=4, c_max=10)
+    assert B.select_partition(wl, q)[0] == B.MOE_ERR_NO_LEGAL_PARTITION
+    L = B.lib()
+    assert L.moe_select_partition(None, None, None) == B.MOE_ERR_INVALID_ARG
+    assert L.moe_strerror(-4).decode().startswith("no legal partition")
+
+
+def test_combine_host_validation_without_gpu():
+    """Every check below fails before any HIP call, so it runs on the CPU."""
+    import ctypes
+    L = B.lib()
+    vp = ctypes.c_void_p
+    A = 0x100000                       # a 256-aligned fake address, never touched
+    wl, keep = B.make_workload(T=256, H=1024, I=512, E=8, topk=2, splits=1)
+    need = B.workspace_size(wl)
+    assert need > 256 * 2 * 1024 * 2
+
+    def call(x=A, w=A, off=A, tid=A, g=A, out=A, wlp=wl, C=-1, ws=A, wsb=need):
+        return L.moe_gemm2_combine(vp(x), vp(w), vp(off), vp(tid), vp(g), vp(out),
+                                   ctypes.byref(wlp) if wlp is not None else None, C,
+                                   vp(ws), ctypes.c_size_t(wsb), vp(0))
+
+    assert call(wlp=None) == B.MOE_ERR_INVALID_ARG
+    assert call(x=0) == B.MOE_ERR_INVALID_ARG
+    assert call(out=0) == B.MOE_ERR_INVALID_ARG
+    assert call(x=A + 8) == B.MOE_ERR_ALIGNMENT
+    assert call(out=A + 4) == B.MOE_ERR_ALIGNMENT
+    assert call(tid=A + 2) == B.MOE_ERR_ALIGNMENT
+    assert call(ws=A + 128) == B.MOE_ERR_ALIGNMENT
+    assert call(ws=0) == B.MOE_ERR_WORKSPACE
+    assert call(wsb=need - 1) == B.MOE_ERR_WORKSPACE
+    assert call(C=-2) == B.MOE_ERR_INVALID_ARG
+    for kw in [dict(H=1020), dict(I=500), dict(E=2000), dict(topk=65), dict(H=1024, splits=3)]:
+        args = dict(T=256, H=1024, I=512, E=8, topk=2, splits=1)
+        args.update(kw)
+        w2, k2 = B.make_workload(**args)
+        assert call(wlp=w2) == B.MOE_ERR_UNSUPPORTED, kw
+        assert B.workspace_size(w2) == 0
+    w3, k3 = B.make_workload(T=256, H=1024, I=512, E=8, topk=2, splits=1,
+                             counts=[64] * 7 + [63])         # sums to 511 != 512
+    assert call(wlp=w3) == B.MOE_ERR_INVALID_ARG
+    assert L.moe_gemm2_workspace_init(None, 0, None) == B.MOE_ERR_INVALID_ARG
+    assert L.moe_gemm2_status(None, None, 0) == B.MOE_ERR_INVALID_ARG
+
+
+def test_workspace_size_grows_with_rows():
+    a, _ = B.make_workload(T=1024, H=2048, I=704, E=32, topk=6, splits=2)
+    b, _ = B.make_workload(T=2048, H=2048, I=704, E=32, topk=6, splits=2)
+    sa, sb = B.workspace_size(a), B.workspace_size(b)
+    assert sa >= 1024 * 6 * 2048 * 2 and sb >= 2048 * 6 * 2048 * 2 and sb > sa
+    assert B.trace_size(a) > 0
