@@ -167,9 +167,13 @@ int moe_gemm2_combine(const void* x_perm, const void* w2, const int32_t* expert_
 
 /* Same as moe_gemm2_combine, and also records timestamps (the device's
  * constant 100 MHz clock) into trace (device, 8-byte aligned, at least
- * moe_gemm2_trace_size(wl) bytes): per compute tile its start and publish
- * time, per consumer task its wait start, wait end and finish time.  The
- * arithmetic and the result are identical to the untraced call. */
+ * moe_gemm2_trace_size(wl) bytes).  Layout, uint64 words: for each compute
+ * tile g of the global sequence, words 4g..4g+3 = start, end of the
+ * reduction loop, end of the Y stores, publish; then, from word
+ * 4 * max_tiles (max_tiles = splits * ceil(H/splits/256) *
+ * (ceil(rows/256) + E)), for each consumer task j, words 4j..4j+3 = wait
+ * start, wait end, finish, workgroup id.  The arithmetic and the result are
+ * identical to the untraced call. */
 int moe_gemm2_combine_traced(const void* x_perm, const void* w2, const int32_t* expert_offsets,
                              const int32_t* token_ids, const float* gate_w, float* out,
                              const moe_workload_t* wl, int32_t num_consumers,

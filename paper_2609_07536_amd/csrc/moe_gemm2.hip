@@ -42,6 +42,7 @@ constexpr int kCommTN = 1024;           // consumer task: columns (at most)
 constexpr int kMaxE = 1024;
 constexpr int kMaxSplits = 16;
 constexpr int kMaxTopk = 64;
+constexpr int kMaxGrid = 4096;
 
 constexpr uint32_t kStBadRouting = 1u;
 constexpr uint32_t kStTimeout = 2u;
@@ -59,11 +60,10 @@ struct KArgs {
   const float* gate_w;        // [rows]
   float* out;                 // [T, H]
   uint16_t* Y;                // [rows, H] bf16 staging
-  uint32_t* tile_flags;       // [max_tiles]
-  u64* split_cnt;             // [kMaxSplits]
-  u64* tok_cnt;               // [T]
+  uint32_t* tile_flags;       // [max_tiles]: epoch once tile g is published
+  uint32_t* wg_flags;         // [kMaxGrid]: epoch once workgroup b added its inverse-map rows
+  u64* tok_cnt;               // [T]: epoch-tagged count of each token's rows
   int32_t* inv;               // [T, topk]
-  u64* inv_done;              // [1]
   uint32_t* status;           // [1]
   u64* trace;                 // optional
   long long rows;             // capacity of x / Y / token_ids / gate_w
@@ -124,21 +124,34 @@ __device__ __forceinline__ uint32_t epoch_count(u64 v, uint32_t epoch) {
 
 __device__ __forceinline__ u64 now_100mhz() { return __builtin_amdgcn_s_memrealtime(); }
 
-// Thread 0 polls *p until it equals want (bounded); the whole workgroup
-// then acquires.  Returns false (and records a timeout) if the bound expired.
-__device__ bool wait_equal(Smem& sm, u64* p, u64 want, const KArgs& a) {
-  if (threadIdx.x == 0) {
-    long long it = 0;
+// Wave 0 polls flags[0..n) until every flag equals the epoch (bounded),
+// advancing past the leading run of set flags; then the whole workgroup
+// acquires.  Returns false (and records a timeout) if the bound expired.
+__device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& a) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    long long i = 0, spins = 0;
     int ok = 1;
-    while (ld_relaxed(p) != want) {
-      if (++it > a.spin_limit) {
+    while (i < n) {
+      const long long idx = i + lane;
+      const uint32_t v = idx < n ? __hip_atomic_load(&flags[idx], __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT)
+                                 : a.epoch;
+      const u64 ready = __ballot(v == a.epoch);
+      if (ready == ~0ull) {
+        i += 64;
+        continue;
+      }
+      i += __builtin_ctzll(~ready);   // leading set flags stay set
+      if (++spins > a.spin_limit) {
         ok = 0;
-        __hip_atomic_fetch_or(a.status, kStTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (lane == 0)
+          __hip_atomic_fetch_or(a.status, kStTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
       }
-      __builtin_amdgcn_s_sleep(2);
+      __builtin_amdgcn_s_sleep(8);
     }
-    sm.flag = ok;
+    if (lane == 0) sm.flag = ok;
   }
   __syncthreads();
   const bool ok = sm.flag != 0;
@@ -207,7 +220,8 @@ __device__ void build_inverse(const KArgs& a, long long rows_dev) {
   __syncthreads();
   if (threadIdx.x == 0) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    epoch_inc(a.inv_done, a.epoch);
+    __hip_atomic_store(&a.wg_flags[blockIdx.x], a.epoch, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -303,7 +317,7 @@ __device__ __forceinline__ void mma_step(const Smem& sm, int buf, f32x4 (&acc)[8
 }
 
 __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_valid, int n0,
-                             int cols_valid) {
+                             int cols_valid, u64* t_mid) {
   const uint16_t* xg = a.x + (size_t)r0 * a.I;
   const uint16_t* wg = a.w2 + (size_t)e * a.I * a.H + n0;
   const int nk = (a.I + kBK - 1) / kBK;
@@ -326,6 +340,7 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
     if (more) stage_store(sm, cur ^ 1, ra, rb);
     __syncthreads();
   }
+  t_mid[0] = now_100mhz();
 
   // epilogue: bf16 rows of Y, 16 bytes per lane per n-block pair
   const int lane = threadIdx.x & 63;
@@ -348,87 +363,158 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
         v[i] = (__bf16)acc[2 * c][mb][i];
         v[4 + i] = (__bf16)acc[2 * c + 1][mb][i];
       }
-      *(bf16x8*)(yrow + n) = v;
+      __builtin_nontemporal_store(v, (bf16x8*)(yrow + n));
     }
   }
+  t_mid[1] = now_100mhz();
 }
 
 // ---- consumer role: one task --------------------------------------------------
 __device__ __forceinline__ float bf16lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
-// out[t, col0 : col0+ncols] for the tokens [t0, t0+ntok): wave w takes
-// tokens t0 + w, t0 + w + 4, ...; lane l takes 8 columns per 512.
+// The rows of token t sorted ascending, spread over the wave: lane j < n
+// holds the j-th row (rs) and its gate bits (gs).  Rows of a token are
+// distinct, so a lane's rank among the n rows is its sorted position.
+__device__ __forceinline__ int token_rows(const KArgs& a, int t, int* rs, int* gs) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t]), a.epoch);
+  const int n = (int)(have < (uint32_t)a.topk ? have : (uint32_t)a.topk);
+  int r = 0;
+  float g = 0.f;
+  if (lane < n) {
+    r = a.inv[(long long)t * a.topk + lane];
+    g = a.gate_w[r];
+  }
+  int rank = lane;
+  if (lane < n) {
+    rank = 0;
+    for (int i = 0; i < n; ++i) rank += __builtin_amdgcn_readlane(r, i) < r ? 1 : 0;
+  }
+  *rs = __builtin_amdgcn_ds_permute(rank << 2, r);
+  *gs = __builtin_amdgcn_ds_permute(rank << 2, __float_as_int(g));
+  return n;
+}
+
+__device__ __forceinline__ void fma8(float (&acc)[8], float g, const u32x4& v) {
+  acc[0] = fmaf(g, bf16lo(v[0]), acc[0]);
+  acc[1] = fmaf(g, bf16hi(v[0]), acc[1]);
+  acc[2] = fmaf(g, bf16lo(v[1]), acc[2]);
+  acc[3] = fmaf(g, bf16hi(v[1]), acc[3]);
+  acc[4] = fmaf(g, bf16lo(v[2]), acc[4]);
+  acc[5] = fmaf(g, bf16hi(v[2]), acc[5]);
+  acc[6] = fmaf(g, bf16lo(v[3]), acc[6]);
+  acc[7] = fmaf(g, bf16hi(v[3]), acc[7]);
+}
+
+// Rows j0 .. j0+U-1 of two tokens at two column chunks: all loads first
+// (a padding row j >= n re-reads row n-1 and gets weight 0), then the FMAs
+// in ascending row order.  n >= 1 for both tokens; every row read is one
+// this launch has written, so its values are finite and weight 0 adds 0.
+template <int U>
+__device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&rs)[2],
+                                            const int (&gs)[2], const int (&n)[2],
+                                            const int (&col)[2], float (&acc)[2][2][8]) {
+  u32x4 v[2][U][2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u < n[p] ? j0 + u : n[p] - 1;
+      const uint16_t* yr = a.Y + (size_t)__builtin_amdgcn_readlane(rs[p], j) * a.H;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) v[p][u][h] = __builtin_nontemporal_load((const u32x4*)(yr + col[h]));
+    }
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u;
+      const float gj = j < n[p] ? __int_as_float(__builtin_amdgcn_readlane(gs[p], j)) : 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) fma8(acc[p][h], gj, v[p][u][h]);
+    }
+}
+
+// out[t, col0 : col0+ncols] for the tokens [t0, t0+ntok): wave w takes the
+// token pairs w, w+4, ...; lane l owns columns 8l..8l+7 and 512+8l..512+8l+7.
 __device__ void consume_task(const KArgs& a, int t0, int ntok, int col0, int ncols) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  for (int tt = wave; tt < ntok; tt += kThreads / 64) {
-    const int t = t0 + tt;
-    const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t]), a.epoch);
-    const int n = (int)(have < (uint32_t)a.topk ? have : (uint32_t)a.topk);
-    // the token's rows, sorted ascending by rank (rows are distinct)
-    int r = 0;
-    float g = 0.f;
-    if (lane < n) {
-      r = a.inv[(long long)t * a.topk + lane];
-      g = a.gate_w[r];
-    }
-    int rank = lane;
-    if (lane < n) {
-      rank = 0;
-      for (int i = 0; i < n; ++i) {
-        const int ri = __builtin_amdgcn_readlane(r, i);
-        rank += ri < r ? 1 : 0;
-      }
-    }
-    const int rs = __builtin_amdgcn_ds_permute(rank << 2, r);
-    const int gs = __builtin_amdgcn_ds_permute(rank << 2, __float_as_int(g));
-    for (int c = 8 * lane; c < ncols; c += 512) {
-      const int col = col0 + c;
-      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      for (int j0 = 0; j0 < n; j0 += 8) {
-        u32x4 v[8];
-        float gj[8];
+  const int nwaves = blockDim.x >> 6;
+  int col[2];
+  bool cok[2];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int j = j0 + u < n ? j0 + u : j0;   // padding lanes reload row j0 ...
-          const int rj = __builtin_amdgcn_readlane(rs, j);
-          gj[u] = j0 + u < n ? __int_as_float(__builtin_amdgcn_readlane(gs, j)) : 0.f;  // ... with weight 0
-          v[u] = *(const u32x4*)(a.Y + (size_t)rj * a.H + col);
-        }
+  for (int h = 0; h < 2; ++h) {
+    const int c = 512 * h + 8 * lane;
+    cok[h] = c < ncols;
+    col[h] = col0 + (cok[h] ? c : 0);   // in-range address; the store is skipped
+  }
+  for (int pp = 2 * wave; pp < ntok; pp += 2 * nwaves) {
+    int rs[2], gs[2], n[2], t[2];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          if (j0 + u >= n) break;
-          acc[0] = fmaf(gj[u], bf16lo(v[u][0]), acc[0]);
-          acc[1] = fmaf(gj[u], bf16hi(v[u][0]), acc[1]);
-          acc[2] = fmaf(gj[u], bf16lo(v[u][1]), acc[2]);
-          acc[3] = fmaf(gj[u], bf16hi(v[u][1]), acc[3]);
-          acc[4] = fmaf(gj[u], bf16lo(v[u][2]), acc[4]);
-          acc[5] = fmaf(gj[u], bf16hi(v[u][2]), acc[5]);
-          acc[6] = fmaf(gj[u], bf16lo(v[u][3]), acc[6]);
-          acc[7] = fmaf(gj[u], bf16hi(v[u][3]), acc[7]);
-        }
+    for (int p = 0; p < 2; ++p) {
+      t[p] = t0 + pp + p;
+      n[p] = 0;
+      rs[p] = 0;
+      gs[p] = 0;
+      if (pp + p < ntok) n[p] = token_rows(a, t[p], &rs[p], &gs[p]);
+    }
+    float acc[2][2][8];
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[p][h][i] = 0.f;
+    // A token without rows borrows the other token's row list for its
+    // loads, with all weights zero, so both tokens share one load stream.
+    const int nl[2] = {n[0] > 0 ? n[0] : n[1], n[1] > 0 ? n[1] : n[0]};
+    const int rl[2] = {n[0] > 0 ? rs[0] : rs[1], n[1] > 0 ? rs[1] : rs[0]};
+    const int gl[2] = {n[0] > 0 ? gs[0] : 0, n[1] > 0 ? gs[1] : 0};
+    const int nmax = nl[0] > nl[1] ? nl[0] : nl[1];
+    for (int j0 = 0; j0 < nmax; j0 += 8) {
+      const int left = nmax - j0;
+      if (left <= 2)
+        gather_step<2>(a, j0, rl, gl, nl, col, acc);
+      else if (left <= 4)
+        gather_step<4>(a, j0, rl, gl, nl, col, acc);
+      else if (left <= 6)
+        gather_step<6>(a, j0, rl, gl, nl, col, acc);
+      else
+        gather_step<8>(a, j0, rl, gl, nl, col, acc);
+    }
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      if (pp + p >= ntok) continue;
+      float* o = a.out + (size_t)t[p] * a.H;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (!cok[h]) continue;
+        const f32x4 lo = {acc[p][h][0], acc[p][h][1], acc[p][h][2], acc[p][h][3]};
+        const f32x4 hi = {acc[p][h][4], acc[p][h][5], acc[p][h][6], acc[p][h][7]};
+        __builtin_nontemporal_store(lo, (f32x4*)(o + col[h]));
+        __builtin_nontemporal_store(hi, (f32x4*)(o + col[h] + 4));
       }
-      float* o = a.out + (size_t)t * a.H + col;
-      *(f32x4*)o = f32x4{acc[0], acc[1], acc[2], acc[3]};
-      *(f32x4*)(o + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
     }
   }
 }
 
 __device__ void consumer_loop(Smem& sm, const KArgs& a, int cid, int ncons, long long W_comp) {
-  if (!wait_equal(sm, a.inv_done, ((u64)a.epoch << 32) | (u64)gridDim.x, a)) return;
+  if (!wait_flags(sm, a.wg_flags, gridDim.x, a)) return;
   const int total = a.L * a.tasks_per_split;
-  u64* trace_tasks = a.trace ? a.trace + 2 * a.max_tiles : nullptr;
+  u64* trace_tasks = a.trace ? a.trace + 4 * a.max_tiles : nullptr;
+  int ready = -1;  // splits [0, ready] are known to be published
   for (int task = cid; task < total; task += ncons) {
     const int s = task / a.tasks_per_split;
     const int rem = task - s * a.tasks_per_split;
     const int tb = rem / a.cb_per_split;
     const int cb = rem - tb * a.cb_per_split;
     const u64 t_wait = now_100mhz();
-    if (W_comp > 0 &&
-        !wait_equal(sm, &a.split_cnt[s], ((u64)a.epoch << 32) | (u64)W_comp, a))
-      return;
+    if (s > ready) {
+      if (W_comp > 0 && !wait_flags(sm, a.tile_flags + (long long)s * W_comp, W_comp, a)) return;
+      ready = s;
+    }
     const u64 t_go = now_100mhz();
     const int t0 = tb * kCommTM;
     const int ntok = min(kCommTM, a.T - t0);
@@ -496,17 +582,19 @@ moe_gemm2_fused(KArgs a) {
     const int n0 = s * a.nsplit + nt * kBN;
     const int cols_valid = min(kBN, (s + 1) * a.nsplit - n0);
     const u64 t_start = now_100mhz();
-    compute_tile(sm, a, e, r0, rows_valid, n0, cols_valid);
+    u64 t_mid[2];
+    compute_tile(sm, a, e, r0, rows_valid, n0, cols_valid, t_mid);
     // publish: every wave's Y stores reach agent scope before the flag
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
     if (threadIdx.x == 0) {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
       __hip_atomic_store(&a.tile_flags[g], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      epoch_inc(&a.split_cnt[s], a.epoch);
       if (a.trace) {
-        a.trace[2 * g + 0] = t_start;
-        a.trace[2 * g + 1] = now_100mhz();
+        a.trace[4 * g + 0] = t_start;
+        a.trace[4 * g + 1] = t_mid[0];
+        a.trace[4 * g + 2] = t_mid[1];
+        a.trace[4 * g + 3] = now_100mhz();
       }
     }
   }
@@ -522,7 +610,7 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
 // ---- host side -----------------------------------------------------------------
 
 struct Layout {
-  size_t status, split_cnt, inv_done, flags, tok_cnt, inv, Y, total;
+  size_t status, wg_flags, flags, tok_cnt, inv, Y, total;
   long long rows, max_tiles;
   int nsplit, ntps, comm_tn, cb_per_split, tasks_per_split;
 };
@@ -554,10 +642,8 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   size_t off = 0;
   L->status = off;
   off += 256;
-  L->split_cnt = off;
-  off += 256;
-  L->inv_done = off;
-  off += 256;
+  L->wg_flags = off;
+  off += (size_t)kMaxGrid * 4;
   L->flags = off;
   off = round_up(off + (size_t)L->max_tiles * 4, 256);
   L->tok_cnt = off;
@@ -699,6 +785,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
     if (P <= 0) return MOE_ERR_NO_LEGAL_PARTITION;
   }
   if (wl->T == 0) return C;  // nothing to write
+  if (C + P > kMaxGrid) return MOE_ERR_UNSUPPORTED;
 
   char* ws = static_cast<char*>(workspace);
   KArgs a;
@@ -710,10 +797,9 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.out = out;
   a.Y = reinterpret_cast<uint16_t*>(ws + L.Y);
   a.tile_flags = reinterpret_cast<uint32_t*>(ws + L.flags);
-  a.split_cnt = reinterpret_cast<u64*>(ws + L.split_cnt);
+  a.wg_flags = reinterpret_cast<uint32_t*>(ws + L.wg_flags);
   a.tok_cnt = reinterpret_cast<u64*>(ws + L.tok_cnt);
   a.inv = reinterpret_cast<int32_t*>(ws + L.inv);
-  a.inv_done = reinterpret_cast<u64*>(ws + L.inv_done);
   a.status = reinterpret_cast<uint32_t*>(ws + L.status);
   a.trace = reinterpret_cast<u64*>(trace);
   a.rows = L.rows;
@@ -757,7 +843,7 @@ extern "C" size_t moe_gemm2_workspace_size(const moe_workload_t* wl) {
 extern "C" size_t moe_gemm2_trace_size(const moe_workload_t* wl) {
   Layout L;
   if (!make_layout(wl, &L)) return 0;
-  return (size_t)(2 * L.max_tiles + 4LL * wl->splits * L.tasks_per_split) * 8;
+  return (size_t)(4 * L.max_tiles + 4LL * wl->splits * L.tasks_per_split) * 8;
 }
 
 extern "C" int moe_gemm2_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
