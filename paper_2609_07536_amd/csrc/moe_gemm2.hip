@@ -33,10 +33,12 @@
 
 namespace {
 
-constexpr int kThreads = 256;           // 4 waves of 64
+constexpr int kThreads = 256;           // 4 waves of 64, one per SIMD
 constexpr int kBM = 256;                // compute tile rows (routed rows)
 constexpr int kBN = 256;                // compute tile columns (hidden)
-constexpr int kBK = 64;                 // reduction step staged in LDS
+constexpr int kBK = 64;                 // reduction step of one LDS stage
+constexpr int kStages = 2;              // LDS ring depth
+constexpr int kResidentPerCu = 1;       // one workgroup (four waves, 512 registers each) per CU
 constexpr int kCommTM = 128;            // consumer task: tokens
 constexpr int kCommTN = 1024;           // consumer task: columns (at most)
 constexpr int kMaxE = 1024;
@@ -49,6 +51,9 @@ constexpr uint32_t kStTimeout = 2u;
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned long long u64;
 
@@ -81,24 +86,14 @@ struct KArgs {
 };
 
 struct Smem {
-  uint16_t a[2][kBM * kBK];   // x tile: row m, 8 chunks of 8 k (swizzled)
-  uint16_t b[2][kBN * kBK];   // W2^T tile: row n, 8 chunks of 8 k (swizzled)
+  uint16_t a[kStages][kBM * kBK];  // x tile: row m = 8 chunks of 8 k (swizzled)
+  uint16_t b[kStages][kBK * kBN];  // W2 tile: row k = 32 chunks of 8 n (swizzled)
   int start[kMaxE];           // sanitized first row of each expert
   int count[kMaxE];           // sanitized row count of each expert
   int tile_prefix[kMaxE + 1]; // exclusive prefix of ceil(count/kBM)
   int scan[kThreads];
   int flag;
 };
-
-// ---- LDS swizzles ----------------------------------------------------------
-// A row holds 64 bf16 = 8 chunks of 16 bytes; the chunk index is XORed with
-// a row function so that 8 consecutive lanes of every access pattern hit 8
-// distinct chunks.  x tile: MFMA reads walk 8 consecutive rows.  W2^T tile:
-// MFMA reads walk rows {8q + i + 4h}, staging writes walk rows {8l + c}.
-__device__ __forceinline__ int swz_a(int m) { return (m ^ (m >> 3)) & 7; }
-__device__ __forceinline__ int swz_b(int n) {
-  return ((n ^ (n >> 3)) & 3) | ((((n >> 3) ^ (n >> 5)) & 1) << 2);
-}
 
 // ---- memory-model helpers ----------------------------------------------------
 __device__ __forceinline__ u64 ld_relaxed(u64* p) {
@@ -227,143 +222,242 @@ __device__ void build_inverse(const KArgs& a, long long rows_dev) {
 
 // ---- compute role: one 256x256 tile ------------------------------------------
 // The MFMA computes D = Y^T for the tile: its A operand is W2^T (rows n) and
-// its B operand is x (columns m), both holding 8 consecutive k per lane.  A
-// wave owns 128 n x 128 m as 8 x 8 blocks of v_mfma_f32_16x16x32_bf16.
-// Inside a pair of n-blocks (2c, 2c+1) the MFMA row rho of block 2c+h maps
-// to n = 32c + 8(rho/4) + 4h + rho%4, so a lane's 4+4 accumulators of the
-// pair are 8 consecutive columns of one row of Y: one 16-byte store.
-__device__ __forceinline__ void stage_load(const KArgs& a, const uint16_t* xg, const uint16_t* wg,
-                                           int rows_valid, int cols_valid, int kt, u32x4 (&ra)[8],
-                                           u32x4 (&rb)[8]) {
-  const int tid = threadIdx.x;
+// its B operand is x (columns m), 8 consecutive k per lane.  Four waves (one
+// per SIMD) each own 128 n x 128 m as 4 x 4 blocks of
+// v_mfma_f32_32x32x16_bf16.
+//
+// Operands reach LDS by direct global->LDS loads (no registers) through a
+// ring of kStages stages of kBK reduction steps:
+//  * x stage: 256 rows of 128 bytes (8 chunks of 8 k, one cache line); chunk
+//    c of row m sits at chunk c ^ (m & 7);
+//  * W2 stage: 64 rows (k) of 512 bytes (32 chunks of 8 n); chunk c of row
+//    k sits at chunk c ^ 2(k & 3).
+// x fragments are plain 16-byte LDS reads.  W2 is stored as in memory (n
+// contiguous) and read with ds_read_b64_tr_b16: in each group of 16 lanes,
+// lane i receives element i%4 of the 8-byte reads of lanes 4p + i/4
+// (p = 0..3), so pointing lane j at row k0 + j/4, columns c(j%4)..+3 hands
+// lane i the 4 consecutive k of column c(i/4) + i%4.
+// MFMA row rho = 8q + 4h + r (q < 4, h < 2, r < 4) of an n-block is mapped
+// to column 16(q/2) + 8h + 4(q%2) + r, so a lane's accumulators 8c..8c+7
+// are 8 consecutive columns of one row of Y (one 16-byte store).
+constexpr int kWN = 128;             // wave tile: n
+constexpr int kWM = 128;             // wave tile: m
+constexpr int kNB = kWN / 32;
+constexpr int kMB = kWM / 32;
+constexpr int kStageElems = kBM * kBK;   // == kBK * kBN
+static_assert(kThreads == 256 && (kBN / kWN) * (kBM / kWM) == kThreads / 64, "wave grid");
+static_assert(kBM * kBK == kBK * kBN, "stage sizes");
+
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// One 16-byte-per-lane global -> LDS load: lane L's 16 bytes land at
+// lds_base + 16 L.  Issued as asm so the compiler does not serialise later
+// LDS reads behind it; completion is tracked with explicit vmcnt waits.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds_base), "v"(g)
+               : "memory", "m0");
+}
+
+// Waits until at most n of this wave's vector memory operations are
+// outstanding (n in {0, 8, 16}) and all its LDS operations are done.
+__device__ __forceinline__ void wait_vm(int n) {
+  // s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
+  if (n >= 16)
+    __builtin_amdgcn_s_waitcnt((16 & 15) | (7 << 4) | (0 << 8) | ((16 >> 4) << 14));
+  else if (n >= 8)
+    __builtin_amdgcn_s_waitcnt(8 | (7 << 4) | (0 << 8));
+  else
+    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));
+}
+
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+struct TileCtx {
+  const uint16_t* xg[8];   // this lane's x row for its 8 loads (k offset 0)
+  const uint16_t* wgp[8];  // this lane's W2 element for its 8 loads (k offset 0)
+  int xk[8];               // k offset of the chunk each x load fetches
+  int wk[8];               // k row (within a stage) each W2 load fetches
+  uint32_t lds_a, lds_b;   // LDS addresses of stage 0
+};
+
+// Issue the 16 loads (8 of x, 8 of W2) of this wave for reduction stage kt
+// into ring slot kt % kStages.  Chunks with k >= I are zero-filled by LDS
+// writes instead.
+__device__ __forceinline__ void issue_stage(const KArgs& a, const TileCtx& t, int kt, int wave) {
+  const int slot = kt % kStages;
   const int k0 = kt * kBK;
-  const int kx = k0 + 8 * (tid & 7);
-  const bool kx_ok = kx < a.I;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int m = (tid >> 3) + 32 * j;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (kx_ok && m < rows_valid) v = *(const u32x4*)(xg + (size_t)m * a.I + kx);
-    ra[j] = v;
-  }
-  const int kb = k0 + 8 * (tid >> 5);
-  const int nn = 8 * (tid & 31);
-  const bool n_ok = nn < cols_valid;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (n_ok && kb + j < a.I) v = *(const u32x4*)(wg + (size_t)(kb + j) * a.H + nn);
-    rb[j] = v;
-  }
-}
-
-__device__ __forceinline__ void stage_store(Smem& sm, int buf, const u32x4 (&ra)[8],
-                                            const u32x4 (&rb)[8]) {
-  const int tid = threadIdx.x;
-  uint16_t* As = sm.a[buf];
-  uint16_t* Bs = sm.b[buf];
-  const int kc = tid & 7;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int m = (tid >> 3) + 32 * j;
-    *(u32x4*)(As + m * kBK + ((kc ^ swz_a(m)) << 3)) = ra[j];
-  }
-  // rb[j] = W2[k = kb + j][n = nn .. nn+7]; write row n = nn + c of W2^T
-  // holding k = kb .. kb+7: an 8x8 transpose of 16-bit values.
-  const int kcb = tid >> 5;
-  const int nn = 8 * (tid & 31);
-#pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    const int d = c >> 1;
-    const uint32_t sel = (c & 1) ? 0x07060302u : 0x05040100u;
-    u32x4 v;
-    v[0] = __builtin_amdgcn_perm(rb[1][d], rb[0][d], sel);
-    v[1] = __builtin_amdgcn_perm(rb[3][d], rb[2][d], sel);
-    v[2] = __builtin_amdgcn_perm(rb[5][d], rb[4][d], sel);
-    v[3] = __builtin_amdgcn_perm(rb[7][d], rb[6][d], sel);
-    const int n = nn + c;
-    *(u32x4*)(Bs + n * kBK + ((kcb ^ swz_b(n)) << 3)) = v;
-  }
-}
-
-__device__ __forceinline__ void mma_step(const Smem& sm, int buf, f32x4 (&acc)[8][8]) {
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int wn0 = (wave & 1) * 128;
-  const int wm0 = (wave >> 1) * 128;
-  const int lr = lane & 15, lq = lane >> 4;
-  const uint16_t* As = sm.a[buf];
-  const uint16_t* Bs = sm.b[buf];
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
-    const int kc = ks * 4 + lq;
-    bf16x8 af[8], bm[8];
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb) {
-      const int n = wn0 + 32 * (nb >> 1) + 8 * (lr >> 2) + 4 * (nb & 1) + (lr & 3);
-      af[nb] = *(const bf16x8*)(Bs + n * kBK + ((kc ^ swz_b(n)) << 3));
+  for (int q = 0; q < 8; ++q) {
+    const uint32_t dst = t.lds_a + (uint32_t)(slot * kStageElems + (8 * wave + q) * 512) * 2;
+    const int k = k0 + t.xk[q];
+    if (k < a.I) {
+      dma16(t.xg[q] + k, dst);
+    } else {
+      *(__attribute__((address_space(3))) u32x4*)(uintptr_t)(dst + 16 * lane) = u32x4{0u, 0u, 0u, 0u};
     }
+  }
 #pragma unroll
-    for (int mb = 0; mb < 8; ++mb) {
-      const int m = wm0 + 16 * mb + lr;
-      bm[mb] = *(const bf16x8*)(As + m * kBK + ((kc ^ swz_a(m)) << 3));
+  for (int q = 0; q < 8; ++q) {
+    const uint32_t dst = t.lds_b + (uint32_t)(slot * kStageElems + (8 * wave + q) * 512) * 2;
+    const int k = k0 + t.wk[q];
+    if (k < a.I) {
+      dma16(t.wgp[q] + (size_t)k * a.H, dst);
+    } else {
+      *(__attribute__((address_space(3))) u32x4*)(uintptr_t)(dst + 16 * lane) = u32x4{0u, 0u, 0u, 0u};
     }
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb)
-#pragma unroll
-      for (int mb = 0; mb < 8; ++mb)
-        acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[nb], bm[mb], acc[nb][mb], 0, 0, 0);
   }
 }
 
 __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_valid, int n0,
                              int cols_valid, u64* t_mid) {
-  const uint16_t* xg = a.x + (size_t)r0 * a.I;
-  const uint16_t* wg = a.w2 + (size_t)e * a.I * a.H + n0;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nk = (a.I + kBK - 1) / kBK;
 
-  f32x4 acc[8][8];
+  TileCtx t;
+  t.lds_a = lds_addr(&sm.a[0][0]);
+  t.lds_b = lds_addr(&sm.b[0][0]);
+  {
+    const uint16_t* w2e = a.w2 + (size_t)e * a.I * a.H + n0;
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  u32x4 ra[8], rb[8];
-  stage_load(a, xg, wg, rows_valid, cols_valid, 0, ra, rb);
-  stage_store(sm, 0, ra, rb);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) stage_load(a, xg, wg, rows_valid, cols_valid, kt + 1, ra, rb);
-    mma_step(sm, cur, acc);
-    if (more) stage_store(sm, cur ^ 1, ra, rb);
-    __syncthreads();
+    for (int q = 0; q < 8; ++q) {
+      const int i = 8 * wave + q;            // 1 KB block of the stage
+      // x: rows 8i + L/8, physical chunk L%8
+      const int row = 8 * i + (lane >> 3);
+      const int lc = (lane & 7) ^ (row & 7);
+      const int grow = row < rows_valid ? row : rows_valid - 1;   // rows past the expert: unused
+      t.xg[q] = a.x + (size_t)(r0 + grow) * a.I;
+      t.xk[q] = 8 * lc;
+      // W2: rows 2i + L/32, physical chunk L%32
+      const int krow = 2 * i + (lane >> 5);
+      const int wc = (lane & 31) ^ (2 * (krow & 3));
+      const int n = 8 * wc < cols_valid ? 8 * wc : 0;               // columns past the tile: unused
+      t.wgp[q] = w2e + n;
+      t.wk[q] = krow;
+    }
   }
+
+  // per-lane LDS element offsets of the MFMA fragments (stage 0, step 0)
+  const int wn0 = (wave & 1) * kWN;
+  const int wm0 = (wave >> 1) * kWM;
+  int offA[kNB];
+  {
+    const int j = lane & 15;
+    const int krow = 8 * (lane >> 5) + (j >> 2);
+    const int u = j & 3;
+    const int rg = (lane >> 4) & 1;
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) {
+      const int col = wn0 + 32 * nb + 16 * rg + 8 * (u & 1) + 4 * (u >> 1);
+      offA[nb] = krow * kBN + (((col >> 3) ^ (2 * (krow & 3))) << 3) + (col & 7);
+    }
+  }
+  int offB[kBK / 16];
+  {
+    const int m = wm0 + (lane & 31);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      const int c = 2 * ks + (lane >> 5);
+      offB[ks] = m * kBK + ((c ^ (m & 7)) << 3);
+    }
+  }
+
+  f32x16 acc[kNB][kMB];
+#pragma unroll
+  for (int i = 0; i < kNB; ++i)
+#pragma unroll
+    for (int j = 0; j < kMB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  // prologue: stages 0 .. kStages-2 in flight
+#pragma unroll
+  for (int s = 0; s < kStages - 1; ++s)
+    if (s < nk) issue_stage(a, t, s, wave);
+
+  for (int kt = 0; kt < nk; ++kt) {
+    // stage kt landed for this wave (later stages may still fly) ...
+    const int ahead = min(kStages - 2, nk - 1 - kt);
+    wait_vm(16 * ahead);
+    // ... and for every wave; every wave is also done reading slot (kt-1)
+    block_barrier();
+    if (kt + kStages - 1 < nk) issue_stage(a, t, kt + kStages - 1, wave);
+
+    const int slot = kt % kStages;
+    const __attribute__((address_space(3))) uint16_t* As =
+        (const __attribute__((address_space(3))) uint16_t*)(uintptr_t)(t.lds_a + slot * kStageElems * 2);
+    const __attribute__((address_space(3))) uint16_t* Bs =
+        (const __attribute__((address_space(3))) uint16_t*)(uintptr_t)(t.lds_b + slot * kStageElems * 2);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      bf16x8 af[kNB], bm[kMB];
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) {
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_i16x4*)(Bs + offA[nb] + ks * 16 * kBN));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_i16x4*)(Bs + offA[nb] + ks * 16 * kBN + 4 * kBN));
+        const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        af[nb] = __builtin_bit_cast(bf16x8, v);
+      }
+#pragma unroll
+      for (int mb = 0; mb < kMB; ++mb)
+        bm[mb] = *(const __attribute__((address_space(3))) bf16x8*)(As + offB[ks] + mb * 32 * kBK);
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < kMB; ++mb)
+          acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[nb], bm[mb], acc[nb][mb], 0, 0, 0);
+    }
+  }
+  // every wave is done with the ring before the next tile's prologue
+  block_barrier();
   t_mid[0] = now_100mhz();
 
-  // epilogue: bf16 rows of Y, 16 bytes per lane per n-block pair
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int wn0 = (wave & 1) * 128;
-  const int wm0 = (wave >> 1) * 128;
-  const int lr = lane & 15, lq = lane >> 4;
+  // epilogue: the wave's 128 x 128 block goes through LDS (the ring is free
+  // now) as bf16 rows of 256 bytes (16-byte chunk j of row r at chunk
+  // j ^ (r & 7)), then leaves as full 128-byte lines: each store writes 4
+  // rows x 256 bytes.
+  const int h = lane >> 5;
+  __attribute__((address_space(3))) uint16_t* ep =
+      (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(t.lds_a) + wave * (kWM * kWN);
 #pragma unroll
-  for (int mb = 0; mb < 8; ++mb) {
-    const int m = wm0 + 16 * mb + lr;
-    if (m >= rows_valid) continue;
-    uint16_t* yrow = a.Y + (size_t)(r0 + m) * a.H + n0;
+  for (int mb = 0; mb < kMB; ++mb) {
+    const int row = 32 * mb + (lane & 31);
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int n = wn0 + 32 * c + 8 * lq;
-      if (n >= cols_valid) continue;
-      bf16x8 v;
+    for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        v[i] = (__bf16)acc[2 * c][mb][i];
-        v[4 + i] = (__bf16)acc[2 * c + 1][mb][i];
+      for (int c = 0; c < 2; ++c) {
+        bf16x8 v;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = (__bf16)acc[nb][mb][8 * c + i];
+        const int chunk = 4 * nb + 2 * c + h;
+        *(__attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((chunk ^ (row & 7)) << 3)) = v;
       }
-      __builtin_nontemporal_store(v, (bf16x8*)(yrow + n));
+  }
+  {
+    const int j = lane & 15;
+    const int n = wn0 + 8 * j;
+    const bool n_ok = n < cols_valid;
+#pragma unroll 4
+    for (int it = 0; it < kWM / 4; ++it) {
+      const int row = 4 * it + (lane >> 4);
+      const int m = wm0 + row;
+      const bf16x8 v =
+          *(const __attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((j ^ (row & 7)) << 3));
+      if (n_ok && m < rows_valid)
+        __builtin_nontemporal_store(v, (bf16x8*)(a.Y + (size_t)(r0 + m) * a.H + n0 + n));
     }
   }
   t_mid[1] = now_100mhz();
@@ -677,8 +771,21 @@ int device_info(int dev, DevInfo* out) {
     int occ = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
         &occ, reinterpret_cast<const void*>(moe_gemm2_fused), kThreads, 0);
+    hipFuncAttributes fa;
+    const hipError_t e2 = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(moe_gemm2_fused));
     if (cur != dev) (void)hipSetDevice(cur);
-    if (e != hipSuccess || occ <= 0) return MOE_ERR_HIP;
+    if (e != hipSuccess || e2 != hipSuccess || occ <= 0) return MOE_ERR_HIP;
+    // Every workgroup of the persistent grid must be resident at once (the
+    // consumers wait on tiles of other workgroups), so the residency used
+    // for the grid must never exceed what fits.  The occupancy query has
+    // over-reported on this target for kernels that use the unified
+    // register file, so it is capped by the LDS bound and by the one
+    // workgroup per CU the kernel is compiled for (one wave per SIMD).
+    const size_t lds = fa.sharedSizeBytes > 0 ? fa.sharedSizeBytes : sizeof(Smem);
+    const int occ_lds = (int)(prop.maxSharedMemoryPerMultiProcessor / lds);
+    occ = occ < occ_lds ? occ : occ_lds;
+    occ = occ < kResidentPerCu ? occ : kResidentPerCu;
+    if (occ <= 0) return MOE_ERR_UNSUPPORTED;
     g_dev[dev].cus = prop.multiProcessorCount;
     g_dev[dev].occ = occ;
     g_dev[dev].ready = true;
