@@ -1,13 +1,21 @@
 """Benchmark of the fused MoE GEMM2 + combine stage on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload dsv2lite] [--consumers C]
-                    [--sweep] [--no-cpu]
+                    [--no-sweep] [--no-cpu] [--calibrate] [--copy-probe MIB]
 
 One step is one call of moe_gemm2_combine (grouped down-projection GEMM plus
 the gate-weighted combine, with the launch-time partition selector) on the
 DeepSeek-V2-Lite-like one-GPU share (T=16384 tokens, H=2048, I=704, 32 local
 experts, top-6, two splits; hottest expert 4x the mean load, the rest Zipf
 s=1.2), inputs synthetic and resident in HBM.  Prints one JSON line.
+
+Also measured, in the same run:
+  * a trace of one launch (per-tile and per-task timestamps) giving the
+    GEMM-portion TFLOP/s and the combine GB/s;
+  * the selector sweep: 12 workloads (T in 4096..32768 x uniform / Zipf 0.8 /
+    Zipf 1.2 on the same shapes), every consumer count C = 0..64 timed, and
+    the selector's pick compared with the best (regret);
+  * the CPU oracle on the same workload (the CPU baseline).
 """
 from __future__ import annotations
 
@@ -30,6 +38,7 @@ PEAK_HBM_GBS = 8000.0
 KERNEL_NAME = "moe_gemm2_fused"
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_07536_amd", "csrc", "moe_gemm2.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_moe_gemm2_fused_dsv2lite.json")
+TICK_S = 1e-8  # the device timestamp runs at 100 MHz
 
 
 def kernel_sha() -> str:
@@ -62,6 +71,150 @@ def traffic_entry(workload_name):
     return t.get("hbm_bytes_per_launch")
 
 
+class DevWorkload:
+    """A workload resident on the GPU, with its workspace."""
+
+    def __init__(self, w, B, torch, synth_tensors=False, seed=0):
+        self.w, self.B, self.torch = w, B, torch
+        dev = "cuda"
+        if synth_tensors:
+            # timing-only inputs: same shapes and routing, values drawn on the GPU
+            g = torch.Generator(device=dev)
+            g.manual_seed(seed)
+            self.x = torch.randn((w.Mtot, w.I), generator=g, device=dev).to(torch.bfloat16)
+            self.w2 = (torch.randn((w.E, w.I, w.H), generator=g, device=dev)
+                       * (1.0 / np.sqrt(w.I))).to(torch.bfloat16)
+        else:
+            self.x = torch.from_numpy(w.x_perm.view(np.int16)).to(dev).view(torch.bfloat16)
+            self.w2 = torch.from_numpy(w.w2.view(np.int16)).to(dev).view(torch.bfloat16)
+        self.off = torch.from_numpy(w.expert_offsets).to(dev)
+        self.tid = torch.from_numpy(w.token_ids).to(dev)
+        self.g = torch.from_numpy(w.gate_w).to(dev)
+        self.out = torch.empty((w.T, w.H), dtype=torch.float32, device=dev)
+        self.wl, self._keep = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, w.counts)
+        self.ws = B.Workspace(B.workspace_size(self.wl))
+
+    def run(self, C=-1, trace=None):
+        w = self.w
+        return self.B.combine(self.x, self.w2, self.off, self.tid, self.g, T=w.T, splits=w.L,
+                              topk=w.topk, counts=w.counts, num_consumers=C, out=self.out,
+                              workspace=self.ws, trace=trace)[1]
+
+    def trace(self, C):
+        """One traced launch: (C used, tiles [n,4], tasks [m,4]) timestamps."""
+        torch, B = self.torch, self.B
+        buf = torch.zeros(B.trace_size(self.wl) // 8, dtype=torch.int64, device="cuda")
+        used = self.run(C, trace=buf)
+        torch.cuda.synchronize()
+        tr = buf.cpu().numpy().astype(np.int64)
+        part = B.select_partition(self.wl, B.default_params(0))[1]
+        n_tiles = int(part.W_comp) * self.w.L
+        ntasks = int(part.W_comm) * self.w.L
+        tiles = tr[: 4 * n_tiles].reshape(-1, 4)
+        tasks = tr[len(tr) - 4 * ntasks:].reshape(-1, 4) if ntasks else np.zeros((0, 4), np.int64)
+        return used, tiles, tasks
+
+
+def breakdown(dw, C):
+    w = dw.w
+    flops, gemm_bytes, combine_bytes, _ = algorithmic(w)
+    used, tiles, tasks = dw.trace(C)
+    gemm_span = (tiles[:, 3].max() - tiles[:, 0].min()) * TICK_S
+    gp = {"span_us": gemm_span * 1e6, "tflops": flops / gemm_span / 1e12,
+          "pct_peak": 100 * flops / gemm_span / 1e12 / PEAK_BF16_TFLOPS,
+          "mean_tile_us": float((tiles[:, 3] - tiles[:, 0]).mean() * TICK_S * 1e6),
+          "mean_reduction_loop_us": float((tiles[:, 1] - tiles[:, 0]).mean() * TICK_S * 1e6),
+          "mean_store_publish_us": float((tiles[:, 3] - tiles[:, 1]).mean() * TICK_S * 1e6)}
+    comb = None
+    if len(tasks) and tasks[:, 2].max() > 0:
+        busy = tasks[:, 2] - tasks[:, 1]
+        cspan = (tasks[:, 2].max() - tasks[:, 1].min()) * TICK_S
+        comb = {"span_us": cspan * 1e6, "gbps": combine_bytes / cspan / 1e9,
+                "mean_task_us": float(busy.mean() * TICK_S * 1e6),
+                "tail_after_gemm_us": float((tasks[:, 2].max() - tiles[:, 3].max()) * TICK_S * 1e6)}
+    return used, gp, comb
+
+
+def calibrate(dw, C_ref=32, reps=5):
+    """rho_ref: one consumer-task wave over one compute-tile wave, measured at
+    a fixed consumer count (the paper's calibration procedure)."""
+    task_t, tile_t = [], []
+    for _ in range(reps):
+        _, tiles, tasks = dw.trace(C_ref)
+        tile_t.append((tiles[:, 3] - tiles[:, 0]).mean())
+        task_t.append((tasks[:, 2] - tasks[:, 1]).mean())
+    tile_us = float(np.median(tile_t)) * TICK_S * 1e6
+    task_us = float(np.median(task_t)) * TICK_S * 1e6
+    return {"C_ref": C_ref, "compute_wave_us": round(tile_us, 3),
+            "consumer_wave_us": round(task_us, 3), "rho_ref": round(task_us / tile_us, 4)}
+
+
+def time_launches(dw, Cs, samples, torch):
+    """Median event time per C, samples interleaved forward/backward (ABBA)."""
+    stream = torch.cuda.current_stream()
+    times = {C: [] for C in Cs}
+    for C in Cs:               # warm-up of every partition
+        dw.run(C)
+    torch.cuda.synchronize()
+    for s in range(samples):
+        order = list(Cs) if s % 2 == 0 else list(reversed(Cs))
+        evs = []
+        for C in order:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            dw.run(C)
+            b.record(stream)
+            evs.append((C, a, b))
+        torch.cuda.synchronize()
+        for C, a, b in evs:
+            times[C].append(a.elapsed_time(b))
+    return {C: float(np.median(v)) for C, v in times.items()}
+
+
+def run_sweep(B, torch, samples, c_max=64):
+    """Time every C in 0..c_max on the 12 sweep workloads; compare the
+    selector's pick with the fastest (regret = (t_pick - t_best) / t_best).
+    The library's candidate set is 0..64 (C = 0: role switch); the paper's
+    legal set is 1..C_max, reported separately."""
+    from workloads import sweep_workload, sweep_workloads
+    params = B.default_params(0)
+    params_paper = B.default_params(0)
+    params_paper.c_min = 1
+    rows = []
+    for name, _ in sweep_workloads():
+        w = sweep_workload(name, with_tensors=False)
+        log(f"sweep {name}: rows={w.Mtot} r_expert={w.r_expert:.2f}")
+        dw = DevWorkload(w, B, torch, synth_tensors=True)
+        Cs = list(range(0, c_max + 1))
+        med = time_launches(dw, Cs, samples, torch)
+        best_all = min(Cs, key=lambda c: med[c])
+        best_dom = min(Cs[1:], key=lambda c: med[c])
+        pick = B.select_partition(dw.wl, params)[0]
+        pick_p = B.select_partition(dw.wl, params_paper)[0]
+        rows.append({
+            "workload": name, "T": w.T, "r_expert": round(w.r_expert, 3),
+            "best_C": best_all, "best_us": round(med[best_all] * 1e3, 1),
+            "pick_C": pick, "pick_us": round(med[pick] * 1e3, 1),
+            "regret": round((med[pick] - med[best_all]) / med[best_all], 4),
+            "best_C_1_64": best_dom, "best_us_1_64": round(med[best_dom] * 1e3, 1),
+            "pick_C_paper_set": pick_p, "pick_us_paper_set": round(med[pick_p] * 1e3, 1),
+            "regret_paper_set_vs_best_1_64": round((med[pick_p] - med[best_dom]) / med[best_dom], 4),
+            "us_by_C": {str(c): round(med[c] * 1e3, 1) for c in Cs},
+        })
+        del dw
+        torch.cuda.empty_cache()
+
+    def agg(key):
+        v = [r[key] for r in rows]
+        return {"mean": round(float(np.mean(v)), 4), "max": round(float(np.max(v)), 4)}
+
+    return {"workloads": len(rows), "samples_per_C": samples, "C_range": [0, c_max],
+            "rho_ref": [params.rho_ref_num, params.rho_ref_den],
+            "regret": agg("regret"),
+            "regret_paper_set_vs_best_1_64": agg("regret_paper_set_vs_best_1_64"),
+            "per_workload": rows}
+
+
 def cpu_baseline(w, budget_s=12.0):
     """The oracle as it stands, timed on the host cores on this workload."""
     import threadpoolctl
@@ -79,7 +232,7 @@ def cpu_baseline(w, budget_s=12.0):
             break
     per = el / n
     flops = 2 * w.Mtot * w.I * w.H
-    return {"value": flops / per / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+    return {"value": round(flops / per / 1e12, 4), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"whole {w.name} workload (numpy fp32 per-expert matmul + per-token "
                       f"weighted sum), {n} run(s), {per * 1e3:.1f} ms each; "
@@ -94,9 +247,10 @@ def main():
     ap.add_argument("--workload", default="dsv2lite")
     ap.add_argument("--consumers", type=int, default=-1)
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--sweep", action="store_true",
-                    help="also time C = 0..64 on the 12 sweep workloads (selector regret)")
-    ap.add_argument("--sweep-samples", type=int, default=15)
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--sweep-samples", type=int, default=7)
+    ap.add_argument("--calibrate", action="store_true",
+                    help="print the rho_ref calibration at C=32 and exit")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 3 device copies of MIB MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -120,37 +274,30 @@ def main():
         print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
         return
     B.lib()
-    dev = "cuda"
     log(f"generating workload {args.workload}")
     w = config(args.workload)
-    x = torch.from_numpy(w.x_perm.view(np.int16)).to(dev).view(torch.bfloat16)
-    w2 = torch.from_numpy(w.w2.view(np.int16)).to(dev).view(torch.bfloat16)
-    off = torch.from_numpy(w.expert_offsets).to(dev)
-    tid = torch.from_numpy(w.token_ids).to(dev)
-    g = torch.from_numpy(w.gate_w).to(dev)
-    out = torch.empty((w.T, w.H), dtype=torch.float32, device=dev)
-    wl, keep = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, w.counts)
-    ws = B.Workspace(B.workspace_size(wl))
+    dw = DevWorkload(w, B, torch)
+    if args.calibrate:
+        dw.run(32)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": calibrate(dw), "kernel_sha": kernel_sha()}), flush=True)
+        return
     stream = torch.cuda.current_stream()
 
-    def step(C=args.consumers):
-        return B.combine(x, w2, off, tid, g, T=w.T, splits=w.L, topk=w.topk,
-                         counts=w.counts, num_consumers=C, out=out, workspace=ws)[1]
-
     log("warmup")
-    C_used = step()
+    C_used = dw.run(args.consumers)
     for _ in range(args.warmup):
-        step()
+        dw.run(args.consumers)
     torch.cuda.synchronize()
-    st = ws.status()
+    st = dw.ws.status()
     assert st == 0, B.strerror(st)
 
     # selector cost on the host (pure C++, no HIP calls)
     params = B.default_params(0)
-    t0 = time.perf_counter()
     nsel = 20000
+    t0 = time.perf_counter()
     for _ in range(nsel):
-        B.lib().moe_select_partition(wl, params, None)
+        B.lib().moe_select_partition(dw.wl, params, None)
     sel_us = (time.perf_counter() - t0) / nsel * 1e6
 
     log(f"timing {args.steps} steps, C={C_used}")
@@ -160,7 +307,7 @@ def main():
     t0 = time.perf_counter()
     for i in range(args.steps):
         starts[i].record(stream)
-        step()
+        dw.run(args.consumers)
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -173,41 +320,21 @@ def main():
     achieved = flops / ker_avg_s / 1e12
 
     # cold-cache latency: 512 MiB scratch write between samples (untimed)
-    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     cold = []
     for i in range(10):
         scratch.fill_(i)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        step()
+        dw.run(args.consumers)
         b.record(stream)
         torch.cuda.synchronize()
         cold.append(a.elapsed_time(b))
     del scratch
 
-    # one traced launch: split the span into the compute role and the consumers
-    trace = torch.zeros(B.trace_size(wl) // 8, dtype=torch.int64, device=dev)
-    B.combine(x, w2, off, tid, g, T=w.T, splits=w.L, topk=w.topk, counts=w.counts,
-              num_consumers=C_used, out=out, workspace=ws, trace=trace)
-    torch.cuda.synchronize()
-    tr = trace.cpu().numpy().astype(np.int64)
-    part = B.select_partition(wl, params)[1]
-    n_tiles = int(part.W_comp) * w.L
-    tiles = tr[: 4 * n_tiles].reshape(-1, 4)[:, [0, 3]]
-    ntasks = int(part.W_comm) * w.L
-    tasks = tr[len(tr) - 4 * ntasks:].reshape(-1, 4) if ntasks else None
-    tick = 1e-8  # 100 MHz
-    gemm_span = (tiles[:, 1].max() - tiles[:, 0].min()) * tick
-    gemm_portion = {"span_us": gemm_span * 1e6, "tflops": flops / gemm_span / 1e12,
-                    "pct_peak": 100 * flops / gemm_span / 1e12 / PEAK_BF16_TFLOPS,
-                    "mean_tile_us": float((tiles[:, 1] - tiles[:, 0]).mean() * tick * 1e6)}
-    combine = None
-    if tasks is not None and tasks[:, 2].max() > 0:
-        busy = tasks[:, 2] - tasks[:, 1]
-        cspan = (tasks[:, 2].max() - tasks[:, 1].min()) * tick
-        combine = {"span_us": cspan * 1e6, "gbps": combine_bytes / cspan / 1e9,
-                   "mean_task_us": float(busy.mean() * tick * 1e6),
-                   "tail_after_gemm_us": float((tasks[:, 2].max() - tiles[:, 1].max()) * tick * 1e6)}
+    _, gemm_portion, combine = breakdown(dw, C_used)
+    st = dw.ws.status()
+    assert st == 0, B.strerror(st)
 
     res = {
         "metric": METRIC,
@@ -238,11 +365,16 @@ def main():
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic_entry(w.name),
                      "kernel": KERNEL_NAME, "kernel_sha": kernel_sha(),
-                     "avg_launch_us": round(ker_avg_s * 1e6, 2)},
+                     "avg_launch_us": round(ker_avg_s * 1e6, 2),
+                     "algorithmic_flops_per_launch": flops,
+                     "hbm_bytes_lower_bound": min_bytes,
+                     "hbm_bytes_with_y_staging": gemm_bytes + combine_bytes},
     }
-    if args.sweep:
-        from paper_2609_07536_amd import sweep as S
-        res["sweep"] = S.run_sweep(samples=args.sweep_samples, log=log)
+    if not args.no_sweep:
+        del dw
+        torch.cuda.empty_cache()
+        log("selector sweep")
+        res["sweep"] = run_sweep(B, torch, args.sweep_samples)
     if not args.no_cpu:
         log("timing the CPU oracle")
         res["cpu_baseline"] = cpu_baseline(w)

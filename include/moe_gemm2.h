@@ -79,7 +79,8 @@ typedef struct {
   int32_t comm_tile_m, comm_tile_n;  /* consumer task tile T_M^comm x T_N^comm */
   int32_t occ_comp, occ_comm;        /* resident workgroups per CU of each role */
   int32_t num_cus;                   /* G */
-  int32_t c_min, c_max;              /* legal candidates, eq:c-domain */
+  int32_t c_min, c_max;              /* legal candidates, eq:c-domain; c_min = 0 adds the
+                                        role-switch candidate (see moe_select_partition) */
   int32_t groups;                    /* g, input groups (1) */
   int64_t rho_ref_num, rho_ref_den;  /* rho_ref as a positive rational */
   int32_t k_ref, tile_m_ref, tile_n_ref, d_ref;
@@ -102,8 +103,13 @@ typedef struct {
  * T(C) = F_{L-1} (eq:makespan), ties to the least Delta_comp
  * (eq:tie-breaker), then to the least C.  Candidates with P(C) <= 0 are
  * illegal.  Arithmetic is exact (rational rho, integer time).
+ * Extension beyond the paper's legal set {1..C_max}: with c_min = 0 the
+ * candidate C = 0 is also evaluated, the role switch where all
+ * P0 = o_comp G slots run every compute tile and then all serve the consumer
+ * tasks: T(0) = ceil(L W_comp / P0) + rho ceil(L W_comm / P0), R = 0, P = P0,
+ * Delta = ceil(W_comp/P0) P0 - W_comp.
  * Pure host code: no HIP call, no allocation, thread-safe.
- * Returns C* >= 1 and fills *out when out != NULL; MOE_ERR_INVALID_ARG for a
+ * Returns C* >= c_min and fills *out when out != NULL; MOE_ERR_INVALID_ARG for a
  * null wl/p, non-positive dimensions or parameters, a negative host count or
  * arithmetic overflow; MOE_ERR_NO_LEGAL_PARTITION when no candidate is legal. */
 int moe_select_partition(const moe_workload_t* wl, const moe_select_params_t* p,
@@ -117,8 +123,10 @@ int moe_select_evaluate(const moe_workload_t* wl, const moe_select_params_t* p,
                         int64_t* T_num_out, int32_t n, int64_t* T_den_out);
 
 /* Parameters for the fused kernel on a HIP device: its tile shapes, its
- * occupancy from hipOccupancyMaxActiveBlocksPerMultiprocessor, the device's
- * CU count and the MI355X calibration of rho_ref.  Device facts are cached
+ * occupancy from hipOccupancyMaxActiveBlocksPerMultiprocessor (capped by its
+ * LDS and register budget), the device's CU count, the candidate set
+ * C = 0..64 (C = 0 is the role switch, a legal launch of this kernel) and
+ * the MI355X calibration of rho_ref.  Device facts are cached
  * on first use (Method, "System Integration and Correctness").  Returns 0 or
  * MOE_ERR_HIP / MOE_ERR_INVALID_ARG. */
 int moe_gemm2_default_params(int device, moe_select_params_t* out);

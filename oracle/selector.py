@@ -26,6 +26,11 @@ Readings where the paper is silent (each listed in the design notes):
   * a candidate whose P(C) <= 0 is not in the legal set;
   * ties left after Delta go to the smaller C;
   * D = 1 on one GPU, so the token count per rank is M itself.
+
+Extension beyond the paper's legal set (only when c_min = 0): the
+role-switch candidate C = 0, where all o_comp * G slots run every compute
+tile and then all of them serve the consumer tasks,
+T(0) = ceil(L W_comp / P0) + rho ceil(L W_comm / P0) with P0 = o_comp G.
 """
 from __future__ import annotations
 
@@ -81,6 +86,14 @@ def rho_scaled(rho_ref: Fraction, K: int, K_ref: int, tile_m: int, tile_n: int,
 def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
              o_comp: int, rho: Fraction) -> Optional[Candidate]:
     """The recurrence for one candidate C; None if P(C) <= 0 (illegal)."""
+    if C == 0:
+        P0 = o_comp * G
+        A_last = cdiv(L * W_comp, P0)
+        q = Fraction(rho) * cdiv(L * W_comm, P0)
+        T = A_last + q
+        V_comp = cdiv(W_comp, P0)
+        return Candidate(C=0, R=0, P=P0, A=[A_last], V_comm=cdiv(L * W_comm, P0), q=q,
+                         F=[T], T=T, V_comp=V_comp, delta=V_comp * P0 - W_comp)
     R = cdiv(C, o_comm)
     P = o_comp * (G - R)
     if P <= 0:

@@ -319,6 +319,26 @@ __device__ __forceinline__ void issue_stage(const KArgs& a, const TileCtx& t, in
   }
 }
 
+typedef const __attribute__((address_space(3))) uint16_t lds_u16;
+
+// MFMA operands of K=16 step ks from a ring slot: W2^T blocks by two
+// transposing 8-byte reads, x blocks by one 16-byte read.
+__device__ __forceinline__ void load_frags(lds_u16* As, lds_u16* Bs, const int (&offA)[kNB],
+                                           const int (&offB)[kBK / 16], int ks,
+                                           bf16x8 (&af)[kNB], bf16x8 (&bm)[kMB]) {
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb) {
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + offA[nb] + ks * 16 * kBN));
+    const i16x4 hi =
+        __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + offA[nb] + ks * 16 * kBN + 4 * kBN));
+    const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    af[nb] = __builtin_bit_cast(bf16x8, v);
+  }
+#pragma unroll
+  for (int mb = 0; mb < kMB; ++mb)
+    bm[mb] = *(const __attribute__((address_space(3))) bf16x8*)(As + offB[ks] + mb * 32 * kBK);
+}
+
 __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_valid, int n0,
                              int cols_valid, u64* t_mid) {
   const int lane = threadIdx.x & 63;
@@ -395,30 +415,22 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
     if (kt + kStages - 1 < nk) issue_stage(a, t, kt + kStages - 1, wave);
 
     const int slot = kt % kStages;
-    const __attribute__((address_space(3))) uint16_t* As =
-        (const __attribute__((address_space(3))) uint16_t*)(uintptr_t)(t.lds_a + slot * kStageElems * 2);
-    const __attribute__((address_space(3))) uint16_t* Bs =
-        (const __attribute__((address_space(3))) uint16_t*)(uintptr_t)(t.lds_b + slot * kStageElems * 2);
+    lds_u16* As = (lds_u16*)(uintptr_t)(t.lds_a + slot * kStageElems * 2);
+    lds_u16* Bs = (lds_u16*)(uintptr_t)(t.lds_b + slot * kStageElems * 2);
+    // four K=16 steps; the fragments of step ks+1 are read while the MFMAs
+    // of step ks run
+    bf16x8 af[2][kNB], bm[2][kMB];
+    load_frags(As, Bs, offA, offB, 0, af[0], bm[0]);
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
-      bf16x8 af[kNB], bm[kMB];
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) {
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_i16x4*)(Bs + offA[nb] + ks * 16 * kBN));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_i16x4*)(Bs + offA[nb] + ks * 16 * kBN + 4 * kBN));
-        const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        af[nb] = __builtin_bit_cast(bf16x8, v);
-      }
-#pragma unroll
-      for (int mb = 0; mb < kMB; ++mb)
-        bm[mb] = *(const __attribute__((address_space(3))) bf16x8*)(As + offB[ks] + mb * 32 * kBK);
+      if (ks + 1 < kBK / 16) load_frags(As, Bs, offA, offB, ks + 1, af[(ks + 1) & 1], bm[(ks + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);   // keep the next step's reads ahead of these MFMAs
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
         for (int mb = 0; mb < kMB; ++mb)
-          acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[nb], bm[mb], acc[nb][mb], 0, 0, 0);
+          acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks & 1][nb], bm[ks & 1][mb],
+                                                                acc[nb][mb], 0, 0, 0);
     }
   }
   // every wave is done with the ring before the next tile's prologue
@@ -795,11 +807,12 @@ int device_info(int dev, DevInfo* out) {
 }
 
 // rho_ref of the fused kernel on MI355X: mean consumer-task time over mean
-// compute-tile time, measured with the traced entry point at the
-// reference configuration below (T=16384, H=2048, I=704, E=32, top-6, L=2,
-// C=32).  MOE_GEMM2_RHO_REF="num/den" overrides it.
-constexpr int64_t kRhoRefNum = 4;
-constexpr int64_t kRhoRefDen = 3;
+// compute-tile time (one consumer wave over one compute wave), measured with
+// the traced entry point at the reference configuration (T=16384, H=2048,
+// I=704, E=32, top-6, L=2, C=32): 102.0 us / 60.2 us = 1.70.
+// MOE_GEMM2_RHO_REF="num/den" overrides it.
+constexpr int64_t kRhoRefNum = 17;
+constexpr int64_t kRhoRefDen = 10;
 constexpr int kDefaultFixedC = 8;
 
 void fill_params(const DevInfo& d, moe_select_params_t* p) {
@@ -810,7 +823,9 @@ void fill_params(const DevInfo& d, moe_select_params_t* p) {
   p->occ_comp = d.occ;
   p->occ_comm = d.occ;
   p->num_cus = d.cus;
-  p->c_min = 1;
+  // C = 0 (every workgroup computes, then every workgroup consumes) is a
+  // legal launch of this kernel, so it is part of the candidate set.
+  p->c_min = 0;
   p->c_max = 64;
   p->groups = 1;
   p->rho_ref_num = kRhoRefNum;

@@ -13,6 +13,11 @@
 //   q      = rho ceil(W_comm / C)                                   eq:comm-service
 //   F_s    = max(A_s, F_{s-1}) + q,  T(C) = F_{L-1}                 eq:split-finish, eq:makespan
 //   Delta  = ceil(W_comp/P) P - W_comp                              eq:tie-breaker
+//
+// Extension beyond the paper's legal set (used only when c_min == 0): the
+// role-switch candidate C = 0, where all o_comp G slots compute every tile
+// and then all of them serve the consumer tasks:
+//   T(0) = ceil(L W_comp / P0) + rho ceil(L W_comm / P0),   P0 = o_comp G.
 #include <cstdint>
 #include <cstdlib>
 
@@ -39,7 +44,7 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
       wl->splits <= 0 || wl->ranks <= 0 || wl->rows < 0)
     return MOE_ERR_INVALID_ARG;
   if (p->tile_m <= 0 || p->tile_n <= 0 || p->comm_tile_m <= 0 || p->comm_tile_n <= 0 ||
-      p->occ_comp <= 0 || p->occ_comm <= 0 || p->num_cus <= 0 || p->c_min < 1 ||
+      p->occ_comp <= 0 || p->occ_comm <= 0 || p->num_cus <= 0 || p->c_min < 0 ||
       p->c_max < p->c_min || p->groups <= 0 || p->rho_ref_num <= 0 || p->rho_ref_den <= 0 ||
       p->k_ref <= 0 || p->tile_m_ref <= 0 || p->tile_n_ref <= 0 || p->d_ref <= 0)
     return MOE_ERR_INVALID_ARG;
@@ -84,6 +89,20 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
 // overflow of the scaled integer time.
 bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int64_t* T_out,
                     int64_t* delta_out, int32_t* R_out, int32_t* P_out, int* status) {
+  if (C == 0) {
+    const int64_t P0 = (int64_t)p->occ_comp * p->num_cus;
+    const i128 A = (i128)cdiv64((int64_t)m.L * m.W_comp, P0) * m.rho_den;
+    const i128 F = A + (i128)m.rho_num * cdiv64((int64_t)m.L * m.W_comm, P0);
+    if (F > kI64Max) {
+      *status = MOE_ERR_INVALID_ARG;
+      return false;
+    }
+    *T_out = (int64_t)F;
+    *delta_out = cdiv64(m.W_comp, P0) * P0 - m.W_comp;
+    *R_out = 0;
+    *P_out = (int32_t)P0;
+    return true;
+  }
   const int64_t R = cdiv64(C, p->occ_comm);
   const int64_t P = (int64_t)p->occ_comp * ((int64_t)p->num_cus - R);
   if (P <= 0) return false;

@@ -85,7 +85,7 @@ def _random_case(rnd):
     p = _params(tile_m=rnd.choice([64, 128, 256]), tile_n=rnd.choice([64, 128, 256]),
                 comm_tile_m=rnd.choice([64, 128]), comm_tile_n=rnd.choice([512, 1024]),
                 occ_comp=rnd.randint(1, 3), occ_comm=rnd.randint(1, 3),
-                num_cus=rnd.choice([8, 64, 108, 256, 304]), c_min=1,
+                num_cus=rnd.choice([8, 64, 108, 256, 304]), c_min=rnd.choice([0, 1, 1, 1]),
                 c_max=rnd.randint(1, 80), rho_ref_num=rnd.randint(1, 100000),
                 rho_ref_den=rnd.randint(1, 10000), k_ref=rnd.choice([352, 704, 1408]),
                 tile_m_ref=rnd.choice([128, 256]), tile_n_ref=rnd.choice([128, 256]),
@@ -130,7 +130,7 @@ def test_selector_argument_errors():
     wl, keep = B.make_workload(T=100, H=2048, I=704, E=4, topk=2, splits=2,
                                counts=[50, 50, 50, 50])
     assert B.select_partition(wl, p)[0] >= 1
-    for field, bad in [("c_min", 0), ("occ_comp", 0), ("num_cus", 0), ("rho_ref_den", 0),
+    for field, bad in [("c_min", -1), ("occ_comp", 0), ("num_cus", 0), ("rho_ref_den", 0),
                        ("rho_ref_num", -3), ("tile_m", 0)]:
         q = _params(**{field: bad})
         assert B.select_partition(wl, q)[0] == B.MOE_ERR_INVALID_ARG, field

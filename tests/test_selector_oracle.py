@@ -130,3 +130,19 @@ def test_selection_is_the_exhaustive_argmin():
 def test_no_legal_partition():
     best, cands = sel.select_from_work(10, 10, 1, 2, 1, 1, Fraction(1), 2, 8)
     assert best is None and cands == []
+
+
+def test_role_switch_candidate_closed_form():
+    """C = 0 (an extension, only when c_min = 0): all o_comp G slots compute
+    every tile, then serve every consumer task."""
+    rho = Fraction(5, 2)
+    for W_comp, W_comm, L, G, o in [(1600, 128, 2, 256, 1), (30, 6, 2, 10, 2), (7, 1, 1, 3, 1)]:
+        c = sel.evaluate(0, W_comp, W_comm, L, G, 1, o, rho)
+        P0 = o * G
+        assert c.P == P0 and c.R == 0
+        assert c.T == sel.cdiv(L * W_comp, P0) + rho * sel.cdiv(L * W_comm, P0)
+    best, cands = sel.select_from_work(30, 6, 2, 10, 1, 2, Fraction(3, 2), 0, 6)
+    assert cands[0].C == 0 and cands[0].T == 3 + Fraction(3, 2) * 1
+    assert best.C == 0                      # 4.5 beats the paper's best (9)
+    best1, _ = sel.select_from_work(30, 6, 2, 10, 1, 2, Fraction(3, 2), 1, 6)
+    assert best1.C == 5
