@@ -211,7 +211,8 @@ __device__ void build_inverse(const KArgs& a, long long rows_dev) {
     }
     a.inv[(long long)t * a.topk + slot] = (int32_t)r;
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  // as for a tile: per-wave vmcnt(0), barrier, one release by thread 0
+  __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));
   __syncthreads();
   if (threadIdx.x == 0) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -690,8 +691,12 @@ moe_gemm2_fused(KArgs a) {
     const u64 t_start = now_100mhz();
     u64 t_mid[2];
     compute_tile(sm, a, e, r0, rows_valid, n0, cols_valid, t_mid);
-    // publish: every wave's Y stores reach agent scope before the flag
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    // publish: every wave waits until its Y stores are acknowledged by the
+    // L2 (vmcnt 0), the barrier orders those waits before thread 0, whose
+    // agent-scope release fence writes back the whole L2 (so every wave's
+    // stores) before the flag store.  One release per tile: a release in
+    // every wave cost ~10 us per tile in L2 write-back traffic.
+    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));   // vmcnt(0) lgkmcnt(0)
     __syncthreads();
     if (threadIdx.x == 0) {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
