@@ -814,10 +814,10 @@ int device_info(int dev, DevInfo* out) {
 // rho_ref of the fused kernel on MI355X: mean consumer-task time over mean
 // compute-tile time (one consumer wave over one compute wave), measured with
 // the traced entry point at the reference configuration (T=16384, H=2048,
-// I=704, E=32, top-6, L=2, C=32): 102.0 us / 60.2 us = 1.70.
+// I=704, E=32, top-6, L=2, C=32): 75.5 us / 34.2 us = 2.20.
 // MOE_GEMM2_RHO_REF="num/den" overrides it.
-constexpr int64_t kRhoRefNum = 17;
-constexpr int64_t kRhoRefDen = 10;
+constexpr int64_t kRhoRefNum = 11;
+constexpr int64_t kRhoRefDen = 5;
 constexpr int kDefaultFixedC = 8;
 
 void fill_params(const DevInfo& d, moe_select_params_t* p) {
