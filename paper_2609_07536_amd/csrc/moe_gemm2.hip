@@ -33,12 +33,12 @@
 
 namespace {
 
-constexpr int kThreads = 256;           // 4 waves of 64, one per SIMD
+constexpr int kThreads = 512;           // 8 waves of 64, two per SIMD
 constexpr int kBM = 256;                // compute tile rows (routed rows)
 constexpr int kBN = 256;                // compute tile columns (hidden)
 constexpr int kBK = 64;                 // reduction step of one LDS stage
 constexpr int kStages = 2;              // LDS ring depth
-constexpr int kResidentPerCu = 1;       // one workgroup (four waves, 512 registers each) per CU
+constexpr int kResidentPerCu = 1;       // one workgroup (eight waves, 256 registers each) per CU
 constexpr int kCommTM = 128;            // consumer task: tokens
 constexpr int kCommTN = 1024;           // consumer task: columns (at most)
 constexpr int kMaxE = 1024;
@@ -46,6 +46,7 @@ constexpr int kMaxSplits = 16;
 constexpr int kMaxTopk = 64;
 constexpr int kMaxGrid = 4096;
 
+constexpr size_t kZeroBlock = 128;     // offset of the zero block in the status region
 constexpr uint32_t kStBadRouting = 1u;
 constexpr uint32_t kStTimeout = 2u;
 
@@ -83,10 +84,11 @@ struct KArgs {
   int cb_per_split;           // consumer column blocks per split
   int tasks_per_split;
   uint32_t epoch;
+  const uint16_t* zeros;   // 16+ zero bytes (operand chunks past the reduction)
 };
 
 struct Smem {
-  uint16_t a[kStages][kBM * kBK];  // x tile: row m = 8 chunks of 8 k (swizzled)
+  uint16_t a[kStages][kBM * kBK];  // x tile: row m = kBK/8 chunks of 8 k (swizzled)
   uint16_t b[kStages][kBK * kBN];  // W2 tile: row k = 32 chunks of 8 n (swizzled)
   int start[kMaxE];           // sanitized first row of each expert
   int count[kMaxE];           // sanitized row count of each expert
@@ -223,15 +225,20 @@ __device__ void build_inverse(const KArgs& a, long long rows_dev) {
 
 // ---- compute role: one 256x256 tile ------------------------------------------
 // The MFMA computes D = Y^T for the tile: its A operand is W2^T (rows n) and
-// its B operand is x (columns m), 8 consecutive k per lane.  Four waves (one
-// per SIMD) each own 128 n x 128 m as 4 x 4 blocks of
-// v_mfma_f32_32x32x16_bf16.
+// its B operand is x (columns m), 8 consecutive k per lane.  Eight waves (two
+// per SIMD, 4 along n x 2 along m) each own 64 n x 128 m as 2 x 4 blocks of
+// v_mfma_f32_32x32x16_bf16: with two waves per SIMD one wave's MFMAs run
+// while the other waits for its LDS fragments, and the wave tile keeps the
+// costly transposing reads (W2) at one 16 KB pass per K=16 step per CU.
 //
 // Operands reach LDS by direct global->LDS loads (no registers) through a
-// ring of kStages stages of kBK reduction steps:
-//  * x stage: 256 rows of 128 bytes (8 chunks of 8 k, one cache line); chunk
-//    c of row m sits at chunk c ^ (m & 7);
-//  * W2 stage: 64 rows (k) of 512 bytes (32 chunks of 8 n); chunk c of row
+// ring of kStages stages of kBK reduction steps, kStages - 1 stages ahead of
+// the MFMAs:
+//  * x stage: 256 rows of 2 kBK bytes (kBK/8 chunks of 8 k); chunk c of row
+//    m sits at chunk c ^ ((m / r) % (kBK/8)), r = rows per 256-byte bank
+//    line, so the 16 rows one 16-lane group of a 16-byte read touches fill
+//    all 64 banks;
+//  * W2 stage: kBK rows (k) of 512 bytes (32 chunks of 8 n); chunk c of row
 //    k sits at chunk c ^ 2(k & 3).
 // x fragments are plain 16-byte LDS reads.  W2 is stored as in memory (n
 // contiguous) and read with ds_read_b64_tr_b16: in each group of 16 lanes,
@@ -241,13 +248,23 @@ __device__ void build_inverse(const KArgs& a, long long rows_dev) {
 // MFMA row rho = 8q + 4h + r (q < 4, h < 2, r < 4) of an n-block is mapped
 // to column 16(q/2) + 8h + 4(q%2) + r, so a lane's accumulators 8c..8c+7
 // are 8 consecutive columns of one row of Y (one 16-byte store).
-constexpr int kWN = 128;             // wave tile: n
+constexpr int kWaves = kThreads / 64;
+constexpr int kWN = 64;              // wave tile: n
 constexpr int kWM = 128;             // wave tile: m
+constexpr int kWavesN = kBN / kWN;
 constexpr int kNB = kWN / 32;
 constexpr int kMB = kWM / 32;
-constexpr int kStageElems = kBM * kBK;   // == kBK * kBN
-static_assert(kThreads == 256 && (kBN / kWN) * (kBM / kWM) == kThreads / 64, "wave grid");
+constexpr int kKS = kBK / 16;                          // MFMA K steps per stage
+constexpr int kStageElems = kBM * kBK;                 // == kBK * kBN
+constexpr int kLoadsPerOperand = kStageElems * 2 / 1024 / kWaves;   // 1 KB loads per wave
+constexpr int kLoadsPerStage = 2 * kLoadsPerOperand;
+constexpr int kXRowsPerLoad = 1024 / (2 * kBK);
+constexpr int kXChunks = kBK / 8;
+constexpr int kXRowsPerLine = 256 / (2 * kBK);
+static_assert((kBN / kWN) * (kBM / kWM) == kWaves, "wave grid");
 static_assert(kBM * kBK == kBK * kBN, "stage sizes");
+static_assert(kKS % 2 == 0, "fragment double buffer parity must carry across stages");
+static_assert(kStages >= 2 && (kStages - 1) * kLoadsPerStage <= 63, "vmcnt range");
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
@@ -265,16 +282,20 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
                : "memory", "m0");
 }
 
-// Waits until at most n of this wave's vector memory operations are
-// outstanding (n in {0, 8, 16}) and all its LDS operations are done.
-__device__ __forceinline__ void wait_vm(int n) {
+template <int N>
+__device__ __forceinline__ void waitcnt_vm() {
   // s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
-  if (n >= 16)
-    __builtin_amdgcn_s_waitcnt((16 & 15) | (7 << 4) | (0 << 8) | ((16 >> 4) << 14));
-  else if (n >= 8)
-    __builtin_amdgcn_s_waitcnt(8 | (7 << 4) | (0 << 8));
-  else
-    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
+
+// Waits until the stage that is `newer` stages older than the newest one
+// issued has landed for this wave (all its LDS operations done as well).
+__device__ __forceinline__ void wait_stage(int newer) {
+  static_assert(kStages <= 4, "extend wait_stage");
+  if (newer >= 3) waitcnt_vm<3 * kLoadsPerStage>();
+  else if (newer == 2) waitcnt_vm<2 * kLoadsPerStage>();
+  else if (newer == 1) waitcnt_vm<kLoadsPerStage>();
+  else waitcnt_vm<0>();
 }
 
 __device__ __forceinline__ void block_barrier() {
@@ -284,48 +305,39 @@ __device__ __forceinline__ void block_barrier() {
 }
 
 struct TileCtx {
-  const uint16_t* xg[8];   // this lane's x row for its 8 loads (k offset 0)
-  const uint16_t* wgp[8];  // this lane's W2 element for its 8 loads (k offset 0)
-  int xk[8];               // k offset of the chunk each x load fetches
-  int wk[8];               // k row (within a stage) each W2 load fetches
-  uint32_t lds_a, lds_b;   // LDS addresses of stage 0
+  const uint16_t* xg[kLoadsPerOperand];   // this lane's x row for its loads (k offset 0)
+  const uint16_t* wgp[kLoadsPerOperand];  // this lane's W2 column for its loads (k offset 0)
+  int xk[kLoadsPerOperand];               // k offset of the chunk each x load fetches
+  int wk[kLoadsPerOperand];               // k row (within a stage) each W2 load fetches
+  uint32_t lds_a, lds_b;                  // LDS addresses of stage 0
 };
 
-// Issue the 16 loads (8 of x, 8 of W2) of this wave for reduction stage kt
-// into ring slot kt % kStages.  Chunks with k >= I are zero-filled by LDS
-// writes instead.
-__device__ __forceinline__ void issue_stage(const KArgs& a, const TileCtx& t, int kt, int wave) {
+// Issue load q (q < kLoadsPerOperand) of each operand of reduction stage kt
+// into ring slot kt % kStages.  Every load is issued, so each stage adds
+// exactly kLoadsPerStage to vmcnt; lanes whose chunk lies past the
+// reduction (k >= I) load 16 zero bytes from the workspace instead, which
+// zeroes both operands there.
+__device__ __forceinline__ void issue_load(const KArgs& a, const TileCtx& t, int kt, int wave, int q) {
   const int slot = kt % kStages;
   const int k0 = kt * kBK;
-  const int lane = threadIdx.x & 63;
+  const uint32_t blk = (uint32_t)(slot * kStageElems + (kLoadsPerOperand * wave + q) * 512) * 2;
+  const int kx = k0 + t.xk[q];
+  dma16(kx < a.I ? t.xg[q] + kx : a.zeros, t.lds_a + blk);
+  const int kw = k0 + t.wk[q];
+  dma16(kw < a.I ? t.wgp[q] + (size_t)kw * a.H : a.zeros, t.lds_b + blk);
+}
+
+__device__ __forceinline__ void issue_stage(const KArgs& a, const TileCtx& t, int kt, int wave) {
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const uint32_t dst = t.lds_a + (uint32_t)(slot * kStageElems + (8 * wave + q) * 512) * 2;
-    const int k = k0 + t.xk[q];
-    if (k < a.I) {
-      dma16(t.xg[q] + k, dst);
-    } else {
-      *(__attribute__((address_space(3))) u32x4*)(uintptr_t)(dst + 16 * lane) = u32x4{0u, 0u, 0u, 0u};
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const uint32_t dst = t.lds_b + (uint32_t)(slot * kStageElems + (8 * wave + q) * 512) * 2;
-    const int k = k0 + t.wk[q];
-    if (k < a.I) {
-      dma16(t.wgp[q] + (size_t)k * a.H, dst);
-    } else {
-      *(__attribute__((address_space(3))) u32x4*)(uintptr_t)(dst + 16 * lane) = u32x4{0u, 0u, 0u, 0u};
-    }
-  }
+  for (int q = 0; q < kLoadsPerOperand; ++q) issue_load(a, t, kt, wave, q);
 }
 
 typedef const __attribute__((address_space(3))) uint16_t lds_u16;
 
-// MFMA operands of K=16 step ks from a ring slot: W2^T blocks by two
+// MFMA operands of K=16 step ks of a ring slot: W2^T blocks by two
 // transposing 8-byte reads, x blocks by one 16-byte read.
 __device__ __forceinline__ void load_frags(lds_u16* As, lds_u16* Bs, const int (&offA)[kNB],
-                                           const int (&offB)[kBK / 16], int ks,
+                                           const int (&offB)[kKS], int ks,
                                            bf16x8 (&af)[kNB], bf16x8 (&bm)[kMB]) {
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
@@ -340,6 +352,32 @@ __device__ __forceinline__ void load_frags(lds_u16* As, lds_u16* Bs, const int (
     bm[mb] = *(const __attribute__((address_space(3))) bf16x8*)(As + offB[ks] + mb * 32 * kBK);
 }
 
+// The 16 MFMAs of one K=16 step of the wave's 128 x 128 block.
+__device__ __forceinline__ void mfma_step(f32x16 (&acc)[kNB][kMB], const bf16x8 (&af)[kNB],
+                                          const bf16x8 (&bm)[kMB]) {
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < kMB; ++mb)
+      acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[nb], bm[mb], acc[nb][mb], 0, 0, 0);
+}
+
+// mfma_step with loads q0 .. q0+kNB-1 of stage kt issued one after each
+// n-block of MFMAs: spread out, the loads never hold the wave's in-order
+// issue long enough to starve the matrix core.
+__device__ __forceinline__ void mfma_step_loads(f32x16 (&acc)[kNB][kMB], const bf16x8 (&af)[kNB],
+                                                const bf16x8 (&bm)[kMB], const KArgs& a,
+                                                const TileCtx& t, int kt, int wave, int q0,
+                                                bool on) {
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb) {
+#pragma unroll
+    for (int mb = 0; mb < kMB; ++mb)
+      acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[nb], bm[mb], acc[nb][mb], 0, 0, 0);
+    if (on) issue_load(a, t, kt, wave, q0 + nb);
+  }
+}
+
 __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_valid, int n0,
                              int cols_valid, u64* t_mid) {
   const int lane = threadIdx.x & 63;
@@ -352,11 +390,11 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
   {
     const uint16_t* w2e = a.w2 + (size_t)e * a.I * a.H + n0;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int i = 8 * wave + q;            // 1 KB block of the stage
-      // x: rows 8i + L/8, physical chunk L%8
-      const int row = 8 * i + (lane >> 3);
-      const int lc = (lane & 7) ^ (row & 7);
+    for (int q = 0; q < kLoadsPerOperand; ++q) {
+      const int i = kLoadsPerOperand * wave + q;   // 1 KB block of the stage
+      // x: rows kXRowsPerLoad i + L / kXChunks, physical chunk L % kXChunks
+      const int row = kXRowsPerLoad * i + lane / kXChunks;
+      const int lc = (lane % kXChunks) ^ ((row / kXRowsPerLine) % kXChunks);
       const int grow = row < rows_valid ? row : rows_valid - 1;   // rows past the expert: unused
       t.xg[q] = a.x + (size_t)(r0 + grow) * a.I;
       t.xk[q] = 8 * lc;
@@ -370,8 +408,8 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
   }
 
   // per-lane LDS element offsets of the MFMA fragments (stage 0, step 0)
-  const int wn0 = (wave & 1) * kWN;
-  const int wm0 = (wave >> 1) * kWM;
+  const int wn0 = (wave % kWavesN) * kWN;
+  const int wm0 = (wave / kWavesN) * kWM;
   int offA[kNB];
   {
     const int j = lane & 15;
@@ -384,13 +422,13 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
       offA[nb] = krow * kBN + (((col >> 3) ^ (2 * (krow & 3))) << 3) + (col & 7);
     }
   }
-  int offB[kBK / 16];
+  int offB[kKS];
   {
     const int m = wm0 + (lane & 31);
 #pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
+    for (int ks = 0; ks < kKS; ++ks) {
       const int c = 2 * ks + (lane >> 5);
-      offB[ks] = m * kBK + ((c ^ (m & 7)) << 3);
+      offB[ks] = m * kBK + ((c ^ ((m / kXRowsPerLine) % kXChunks)) << 3);
     }
   }
 
@@ -402,52 +440,76 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // prologue: stages 0 .. kStages-2 in flight
+  // prologue: fill the ring, then wait for stage 0 (every wave's share)
 #pragma unroll
-  for (int s = 0; s < kStages - 1; ++s)
+  for (int s = 0; s < kStages; ++s)
     if (s < nk) issue_stage(a, t, s, wave);
+  wait_stage(min(kStages - 1, nk - 1));
+  block_barrier();
 
-  for (int kt = 0; kt < nk; ++kt) {
-    // stage kt landed for this wave (later stages may still fly) ...
-    const int ahead = min(kStages - 2, nk - 1 - kt);
-    wait_vm(16 * ahead);
-    // ... and for every wave; every wave is also done reading slot (kt-1)
+  // One flat pipeline over the K=16 steps: the fragments of step g+1 are
+  // read while the MFMAs of step g run, also across stage boundaries.  The
+  // stage boundary (stage kt+1 landed for every wave, every wave done
+  // reading slot kt) is one barrier, after which slot kt is refilled with
+  // stage kt + kStages.
+  bf16x8 af[2][kNB], bm[2][kMB];
+  auto slot_a = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_a + (kt % kStages) * kStageElems * 2); };
+  auto slot_b = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_b + (kt % kStages) * kStageElems * 2); };
+  // Steps are grouped so that the loop starts at a stage boundary (which
+  // waits for all LDS reads anyway) and every MFMA group follows the reads
+  // of the next step in straight-line code: the compiler's LDS waits before
+  // each group then cover only that group's own fragments.
+  load_frags(slot_a(0), slot_b(0), offA, offB, 0, af[0], bm[0]);
+#pragma unroll
+  for (int ks = 0; ks + 1 < kKS; ++ks) {
+    load_frags(slot_a(0), slot_b(0), offA, offB, ks + 1, af[(ks + 1) & 1], bm[(ks + 1) & 1]);
+    __builtin_amdgcn_sched_barrier(0);   // keep the next step's reads ahead of these MFMAs
+    mfma_step(acc, af[ks & 1], bm[ks & 1]);
+  }
+  static_assert(kLoadsPerOperand % kNB == 0 && kLoadsPerOperand / kNB <= kKS, "load spread");
+  constexpr int kLoadSteps = kLoadsPerOperand / kNB;   // steps that carry a stage's loads
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    // last step of stage kt: stage kt+1 landed for every wave and every wave
+    // is done reading slot kt, which is refilled with stage kt + kStages
+    // during the next kLoadSteps steps
+    wait_stage(min(kStages - 2, nk - 2 - kt));
     block_barrier();
-    if (kt + kStages - 1 < nk) issue_stage(a, t, kt + kStages - 1, wave);
-
-    const int slot = kt % kStages;
-    lds_u16* As = (lds_u16*)(uintptr_t)(t.lds_a + slot * kStageElems * 2);
-    lds_u16* Bs = (lds_u16*)(uintptr_t)(t.lds_b + slot * kStageElems * 2);
-    // four K=16 steps; the fragments of step ks+1 are read while the MFMAs
-    // of step ks run
-    bf16x8 af[2][kNB], bm[2][kMB];
-    load_frags(As, Bs, offA, offB, 0, af[0], bm[0]);
+    const bool refill = kt + kStages < nk;
+    load_frags(slot_a(kt + 1), slot_b(kt + 1), offA, offB, 0, af[0], bm[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step_loads(acc, af[(kKS - 1) & 1], bm[(kKS - 1) & 1], a, t, kt + kStages, wave, 0, refill);
+    // the other steps of stage kt+1
 #pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
-      if (ks + 1 < kBK / 16) load_frags(As, Bs, offA, offB, ks + 1, af[(ks + 1) & 1], bm[(ks + 1) & 1]);
-      __builtin_amdgcn_sched_barrier(0);   // keep the next step's reads ahead of these MFMAs
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb)
-#pragma unroll
-        for (int mb = 0; mb < kMB; ++mb)
-          acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks & 1][nb], bm[ks & 1][mb],
-                                                                acc[nb][mb], 0, 0, 0);
+    for (int ks = 0; ks + 1 < kKS; ++ks) {
+      load_frags(slot_a(kt + 1), slot_b(kt + 1), offA, offB, ks + 1, af[(ks + 1) & 1],
+                 bm[(ks + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+      if (ks + 1 < kLoadSteps)
+        mfma_step_loads(acc, af[ks & 1], bm[ks & 1], a, t, kt + kStages, wave, (ks + 1) * kNB, refill);
+      else
+        mfma_step(acc, af[ks & 1], bm[ks & 1]);
     }
   }
+  mfma_step(acc, af[(kKS - 1) & 1], bm[(kKS - 1) & 1]);
   // every wave is done with the ring before the next tile's prologue
   block_barrier();
   t_mid[0] = now_100mhz();
 
-  // epilogue: the wave's 128 x 128 block goes through LDS (the ring is free
-  // now) as bf16 rows of 256 bytes (16-byte chunk j of row r at chunk
-  // j ^ (r & 7)), then leaves as full 128-byte lines: each store writes 4
-  // rows x 256 bytes.
+  // epilogue: the wave's kWM x kWN block goes through LDS (the ring is free
+  // now) as bf16 rows of 2 kWN bytes, 16-byte chunk j of row r at chunk
+  // j ^ ((r / r1) % c), c = chunks per row, r1 = rows per 256-byte bank line
+  // (so 16 consecutive rows hit 16 distinct bank groups), then leaves as
+  // whole rows of 2 kWN bytes (full 128-byte lines).
+  constexpr int kEpChunks = kWN / 8;
+  constexpr int kEpRowsPerLine = 256 / (2 * kWN);
+  constexpr int kEpRowsPerStore = 64 / kEpChunks;
   const int h = lane >> 5;
   __attribute__((address_space(3))) uint16_t* ep =
       (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(t.lds_a) + wave * (kWM * kWN);
 #pragma unroll
   for (int mb = 0; mb < kMB; ++mb) {
     const int row = 32 * mb + (lane & 31);
+    const int sw = (row / kEpRowsPerLine) % kEpChunks;
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
@@ -456,19 +518,20 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[i] = (__bf16)acc[nb][mb][8 * c + i];
         const int chunk = 4 * nb + 2 * c + h;
-        *(__attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((chunk ^ (row & 7)) << 3)) = v;
+        *(__attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((chunk ^ sw) << 3)) = v;
       }
   }
   {
-    const int j = lane & 15;
+    const int j = lane % kEpChunks;
     const int n = wn0 + 8 * j;
     const bool n_ok = n < cols_valid;
 #pragma unroll 4
-    for (int it = 0; it < kWM / 4; ++it) {
-      const int row = 4 * it + (lane >> 4);
+    for (int it = 0; it < kWM / kEpRowsPerStore; ++it) {
+      const int row = kEpRowsPerStore * it + lane / kEpChunks;
       const int m = wm0 + row;
+      const int sw = (row / kEpRowsPerLine) % kEpChunks;
       const bf16x8 v =
-          *(const __attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((j ^ (row & 7)) << 3));
+          *(const __attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((j ^ sw) << 3));
       if (n_ok && m < rows_valid)
         __builtin_nontemporal_store(v, (bf16x8*)(a.Y + (size_t)(r0 + m) * a.H + n0 + n));
     }
@@ -651,7 +714,7 @@ __device__ __forceinline__ int compute_index(int b, int C, int N) {
   return c + below(b, xcd) - below(C, xcd);
 }
 
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 moe_gemm2_fused(KArgs a) {
   __shared__ Smem sm;
   load_experts(sm, a);
@@ -751,7 +814,7 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->tasks_per_split = ((wl->T + kCommTM - 1) / kCommTM) * L->cb_per_split;
   L->max_tiles = (long long)wl->splits * L->ntps * ((L->rows + kBM - 1) / kBM + wl->E);
   size_t off = 0;
-  L->status = off;
+  L->status = off;   // word 0: status bits; bytes kZeroBlock..255: zeros, never written
   off += 256;
   L->wg_flags = off;
   off += (size_t)kMaxGrid * 4;
@@ -814,10 +877,10 @@ int device_info(int dev, DevInfo* out) {
 // rho_ref of the fused kernel on MI355X: mean consumer-task time over mean
 // compute-tile time (one consumer wave over one compute wave), measured with
 // the traced entry point at the reference configuration (T=16384, H=2048,
-// I=704, E=32, top-6, L=2, C=32): 75.5 us / 34.2 us = 2.20.
+// I=704, E=32, top-6, L=2, C=32): 64.3 us / 28.2 us = 2.28.
 // MOE_GEMM2_RHO_REF="num/den" overrides it.
-constexpr int64_t kRhoRefNum = 11;
-constexpr int64_t kRhoRefDen = 5;
+constexpr int64_t kRhoRefNum = 57;
+constexpr int64_t kRhoRefDen = 25;
 constexpr int kDefaultFixedC = 8;
 
 void fill_params(const DevInfo& d, moe_select_params_t* p) {
@@ -928,6 +991,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.tok_cnt = reinterpret_cast<u64*>(ws + L.tok_cnt);
   a.inv = reinterpret_cast<int32_t*>(ws + L.inv);
   a.status = reinterpret_cast<uint32_t*>(ws + L.status);
+  a.zeros = reinterpret_cast<const uint16_t*>(ws + L.status + kZeroBlock);
   a.trace = reinterpret_cast<u64*>(trace);
   a.rows = L.rows;
   a.max_tiles = L.max_tiles;
