@@ -8,9 +8,9 @@
 //    expert, then m-tile, then n-tile; compute workgroup b takes tiles b,
 //    b+P, b+2P, ...), run one 256x256 tile of Y = x_perm @ W2[e] on bf16
 //    MFMA with LDS double buffering, store it to the bf16 staging buffer and
-//    publish it (per-tile flag and per-split counter, agent-scope release);
+//    publish it (one agent-scope release, then its per-tile flag);
 //  * consumer workgroups wait until every tile of a split is published
-//    (agent-scope acquire), then, per task of 128 tokens x 1024 columns,
+//    (agent-scope acquire), then, per task of 64 tokens x 1024 columns,
 //    gather each token's rows, weight them by the gates and write the
 //    token's output once, summing the rows in ascending row order so the
 //    result does not depend on the partition.
@@ -23,6 +23,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cstddef>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -39,7 +40,7 @@ constexpr int kBN = 256;                // compute tile columns (hidden)
 constexpr int kBK = 64;                 // reduction step of one LDS stage
 constexpr int kStages = 2;              // LDS ring depth
 constexpr int kResidentPerCu = 1;       // one workgroup (eight waves, 256 registers each) per CU
-constexpr int kCommTM = 128;            // consumer task: tokens
+constexpr int kCommTM = 64;             // consumer task: tokens
 constexpr int kCommTN = 1024;           // consumer task: columns (at most)
 constexpr int kMaxE = 1024;
 constexpr int kMaxSplits = 16;
@@ -543,49 +544,81 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
 __device__ __forceinline__ float bf16lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
-// The rows of token t sorted ascending, spread over the wave: lane j < n
-// holds the j-th row (rs) and its gate bits (gs).  Rows of a token are
-// distinct, so a lane's rank among the n rows is its sorted position.
-__device__ __forceinline__ int token_rows(const KArgs& a, int t, int* rs, int* gs) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t]), a.epoch);
-  const int n = (int)(have < (uint32_t)a.topk ? have : (uint32_t)a.topk);
-  int r = 0;
-  float g = 0.f;
-  if (lane < n) {
-    r = a.inv[(long long)t * a.topk + lane];
-    g = a.gate_w[r];
+// Metadata of one consumer task, staged in LDS (over the idle operand ring):
+// per token of the task, its row count and its rows and gate weights sorted
+// by row.  One pass for all tokens turns the dependent chain count/inverse
+// map -> gate into two dependent loads per task instead of per token pair.
+struct TaskMeta {
+  int n[kCommTM];
+  int row[kCommTM * kMaxTopk];
+  float gate[kCommTM * kMaxTopk];
+};
+
+static_assert(sizeof(TaskMeta) <= sizeof(Smem::a) + sizeof(Smem::b) &&
+                  offsetof(Smem, b) == offsetof(Smem, a) + sizeof(Smem::a),
+              "task metadata overlays the operand ring");
+__device__ TaskMeta& task_meta(Smem& sm) { return *reinterpret_cast<TaskMeta*>(&sm.a[0][0]); }
+
+__device__ void load_task_meta(TaskMeta& m, const KArgs& a, int t0, int ntok) {
+  const int K = a.topk;
+  for (int i = threadIdx.x; i < ntok * K; i += kThreads) {
+    const int t = i / K;
+    const int j = i - t * K;
+    const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t0 + t]), a.epoch);
+    const int n = (int)(have < (uint32_t)K ? have : (uint32_t)K);
+    int r = 0;
+    float g = 0.f;
+    if (j < n) {
+      r = a.inv[(long long)(t0 + t) * K + j];
+      g = a.gate_w[r];
+    }
+    m.row[i] = r;
+    m.gate[i] = g;
+    if (j == 0) m.n[t] = n;
   }
-  int rank = lane;
-  if (lane < n) {
-    rank = 0;
-    for (int i = 0; i < n; ++i) rank += __builtin_amdgcn_readlane(r, i) < r ? 1 : 0;
+  __syncthreads();
+  // rows of a token are distinct: sort them ascending (one thread per token)
+  for (int t = threadIdx.x; t < ntok; t += kThreads) {
+    const int n = m.n[t];
+    int* R = &m.row[t * K];
+    float* G = &m.gate[t * K];
+    for (int i = 1; i < n; ++i) {
+      const int r = R[i];
+      const float g = G[i];
+      int q = i - 1;
+      while (q >= 0 && R[q] > r) {
+        R[q + 1] = R[q];
+        G[q + 1] = G[q];
+        --q;
+      }
+      R[q + 1] = r;
+      G[q + 1] = g;
+    }
   }
-  *rs = __builtin_amdgcn_ds_permute(rank << 2, r);
-  *gs = __builtin_amdgcn_ds_permute(rank << 2, __float_as_int(g));
-  return n;
+  __syncthreads();
 }
 
-__device__ __forceinline__ void fma8(float (&acc)[8], float g, const u32x4& v) {
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+constexpr int kColBlocks = kCommTN / 256;   // 256-column blocks of a task, 4 columns per lane
+static_assert(kCommTN % 256 == 0, "task columns");
+
+__device__ __forceinline__ void fma4(float (&acc)[4], float g, const u32x2& v) {
   acc[0] = fmaf(g, bf16lo(v[0]), acc[0]);
   acc[1] = fmaf(g, bf16hi(v[0]), acc[1]);
   acc[2] = fmaf(g, bf16lo(v[1]), acc[2]);
   acc[3] = fmaf(g, bf16hi(v[1]), acc[3]);
-  acc[4] = fmaf(g, bf16lo(v[2]), acc[4]);
-  acc[5] = fmaf(g, bf16hi(v[2]), acc[5]);
-  acc[6] = fmaf(g, bf16lo(v[3]), acc[6]);
-  acc[7] = fmaf(g, bf16hi(v[3]), acc[7]);
 }
 
-// Rows j0 .. j0+U-1 of two tokens at two column chunks: all loads first
+// Rows j0 .. j0+U-1 of two tokens at every column block: all loads first
 // (a padding row j >= n re-reads row n-1 and gets weight 0), then the FMAs
 // in ascending row order.  n >= 1 for both tokens; every row read is one
 // this launch has written, so its values are finite and weight 0 adds 0.
 template <int U>
 __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&rs)[2],
                                             const int (&gs)[2], const int (&n)[2],
-                                            const int (&col)[2], float (&acc)[2][2][8]) {
-  u32x4 v[2][U][2];
+                                            const int (&col)[kColBlocks],
+                                            float (&acc)[2][kColBlocks][4]) {
+  u32x2 v[2][U][kColBlocks];
 #pragma unroll
   for (int p = 0; p < 2; ++p)
 #pragma unroll
@@ -593,7 +626,8 @@ __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&
       const int j = j0 + u < n[p] ? j0 + u : n[p] - 1;
       const uint16_t* yr = a.Y + (size_t)__builtin_amdgcn_readlane(rs[p], j) * a.H;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) v[p][u][h] = __builtin_nontemporal_load((const u32x4*)(yr + col[h]));
+      for (int b = 0; b < kColBlocks; ++b)
+        v[p][u][b] = __builtin_nontemporal_load((const u32x2*)(yr + col[b]));
     }
 #pragma unroll
   for (int p = 0; p < 2; ++p)
@@ -602,23 +636,26 @@ __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&
       const int j = j0 + u;
       const float gj = j < n[p] ? __int_as_float(__builtin_amdgcn_readlane(gs[p], j)) : 0.f;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) fma8(acc[p][h], gj, v[p][u][h]);
+      for (int b = 0; b < kColBlocks; ++b) fma4(acc[p][b], gj, v[p][u][b]);
     }
 }
 
-// out[t, col0 : col0+ncols] for the tokens [t0, t0+ntok): wave w takes the
-// token pairs w, w+4, ...; lane l owns columns 8l..8l+7 and 512+8l..512+8l+7.
-__device__ void consume_task(const KArgs& a, int t0, int ntok, int col0, int ncols) {
+// out[t, col0 : col0+ncols] for the tokens [t0, t0+ntok) whose metadata is in
+// m: wave w takes the token pairs w, w+nwaves, ...; lane l owns columns
+// 256b + 4l .. 256b + 4l + 3 of every block b, so each output store of a
+// wave writes 1 KB of one row contiguously (whole cache lines).
+__device__ void consume_task(const KArgs& a, const TaskMeta& m, int t0, int ntok, int col0,
+                             int ncols) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
-  int col[2];
-  bool cok[2];
+  int col[kColBlocks];
+  bool cok[kColBlocks];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int c = 512 * h + 8 * lane;
-    cok[h] = c < ncols;
-    col[h] = col0 + (cok[h] ? c : 0);   // in-range address; the store is skipped
+  for (int b = 0; b < kColBlocks; ++b) {
+    const int c = 256 * b + 4 * lane;
+    cok[b] = c < ncols;
+    col[b] = col0 + (cok[b] ? c : 0);   // in-range address; the store is skipped
   }
   for (int pp = 2 * wave; pp < ntok; pp += 2 * nwaves) {
     int rs[2], gs[2], n[2], t[2];
@@ -628,15 +665,22 @@ __device__ void consume_task(const KArgs& a, int t0, int ntok, int col0, int nco
       n[p] = 0;
       rs[p] = 0;
       gs[p] = 0;
-      if (pp + p < ntok) n[p] = token_rows(a, t[p], &rs[p], &gs[p]);
+      if (pp + p < ntok) {
+        const int q = pp + p;
+        n[p] = m.n[q];
+        if (lane < n[p]) {
+          rs[p] = m.row[q * a.topk + lane];
+          gs[p] = __float_as_int(m.gate[q * a.topk + lane]);
+        }
+      }
     }
-    float acc[2][2][8];
+    float acc[2][kColBlocks][4];
 #pragma unroll
     for (int p = 0; p < 2; ++p)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int b = 0; b < kColBlocks; ++b)
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[p][h][i] = 0.f;
+        for (int i = 0; i < 4; ++i) acc[p][b][i] = 0.f;
     // A token without rows borrows the other token's row list for its
     // loads, with all weights zero, so both tokens share one load stream.
     const int nl[2] = {n[0] > 0 ? n[0] : n[1], n[1] > 0 ? n[1] : n[0]};
@@ -659,12 +703,10 @@ __device__ void consume_task(const KArgs& a, int t0, int ntok, int col0, int nco
       if (pp + p >= ntok) continue;
       float* o = a.out + (size_t)t[p] * a.H;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        if (!cok[h]) continue;
-        const f32x4 lo = {acc[p][h][0], acc[p][h][1], acc[p][h][2], acc[p][h][3]};
-        const f32x4 hi = {acc[p][h][4], acc[p][h][5], acc[p][h][6], acc[p][h][7]};
-        __builtin_nontemporal_store(lo, (f32x4*)(o + col[h]));
-        __builtin_nontemporal_store(hi, (f32x4*)(o + col[h] + 4));
+      for (int b = 0; b < kColBlocks; ++b) {
+        if (!cok[b]) continue;
+        const f32x4 v = {acc[p][b][0], acc[p][b][1], acc[p][b][2], acc[p][b][3]};
+        __builtin_nontemporal_store(v, (f32x4*)(o + col[b]));
       }
     }
   }
@@ -675,6 +717,7 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int cid, int ncons, long
   const int total = a.L * a.tasks_per_split;
   u64* trace_tasks = a.trace ? a.trace + 4 * a.max_tiles : nullptr;
   int ready = -1;  // splits [0, ready] are known to be published
+  int meta_t0 = -1;  // token block whose metadata is in LDS
   for (int task = cid; task < total; task += ncons) {
     const int s = task / a.tasks_per_split;
     const int rem = task - s * a.tasks_per_split;
@@ -690,7 +733,13 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int cid, int ncons, long
     const int ntok = min(kCommTM, a.T - t0);
     const int col0 = s * a.nsplit + cb * a.comm_tn;
     const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
-    consume_task(a, t0, ntok, col0, ncols);
+    TaskMeta& m = task_meta(sm);
+    if (t0 != meta_t0) {
+      __syncthreads();   // every wave is done with the previous task's metadata
+      load_task_meta(m, a, t0, ntok);
+      meta_t0 = t0;
+    }
+    consume_task(a, m, t0, ntok, col0, ncols);
     if (trace_tasks) {
       __syncthreads();
       if (threadIdx.x == 0) {
@@ -772,7 +821,11 @@ moe_gemm2_fused(KArgs a) {
       }
     }
   }
-  if (a.drain) consumer_loop(sm, a, c, a.P, W_comp);
+  // after its tiles, a workgroup serves consumer tasks; they are dealt by
+  // block id, which the dispatcher spreads round-robin over the XCDs (the
+  // compute index packs them into one XCD, whose fabric link then limits
+  // a small task set)
+  if (a.drain) consumer_loop(sm, a, b - a.C, a.P, W_comp);
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -877,10 +930,10 @@ int device_info(int dev, DevInfo* out) {
 // rho_ref of the fused kernel on MI355X: mean consumer-task time over mean
 // compute-tile time (one consumer wave over one compute wave), measured with
 // the traced entry point at the reference configuration (T=16384, H=2048,
-// I=704, E=32, top-6, L=2, C=32): 64.3 us / 28.2 us = 2.28.
+// I=704, E=32, top-6, L=2, C=32): 30.6 us / 27.0 us = 1.13.
 // MOE_GEMM2_RHO_REF="num/den" overrides it.
-constexpr int64_t kRhoRefNum = 57;
-constexpr int64_t kRhoRefDen = 25;
+constexpr int64_t kRhoRefNum = 113;
+constexpr int64_t kRhoRefDen = 100;
 constexpr int kDefaultFixedC = 8;
 
 void fill_params(const DevInfo& d, moe_select_params_t* p) {
