@@ -379,12 +379,16 @@ __device__ __forceinline__ void mfma_step_loads(f32x16 (&acc)[kNB][kMB], const b
   }
 }
 
-__device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_valid, int n0,
-                             int cols_valid, u64* t_mid) {
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nk = (a.I + kBK - 1) / kBK;
+// One compute tile: expert e, rows r0 .. r0+rows_valid-1 of x_perm,
+// columns n0 .. n0+cols_valid-1 of Y.
+struct TileInfo {
+  int e, r0, rows_valid, n0, cols_valid;
+};
 
+// This lane's global addresses for its loads of a tile's stages.
+__device__ __forceinline__ TileCtx make_ctx(Smem& sm, const KArgs& a, const TileInfo& ti, int wave) {
+  const int lane = threadIdx.x & 63;
+  const int e = ti.e, r0 = ti.r0, rows_valid = ti.rows_valid, n0 = ti.n0, cols_valid = ti.cols_valid;
   TileCtx t;
   t.lds_a = lds_addr(&sm.a[0][0]);
   t.lds_b = lds_addr(&sm.b[0][0]);
@@ -407,6 +411,26 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
       t.wk[q] = krow;
     }
   }
+  return t;
+}
+
+// The loads of a tile's first min(kStages, nk) stages (its ring fill).
+__device__ __forceinline__ void issue_prologue(const KArgs& a, const TileCtx& t, int nk, int wave) {
+#pragma unroll
+  for (int s = 0; s < kStages; ++s)
+    if (s < nk) issue_stage(a, t, s, wave);
+}
+
+// Computes tile `ti` and stores it to Y.  Its ring fill was issued already
+// if `filled`; with `next`, the ring fill of tile `nt` is issued after this
+// tile's Y stores, so that its loads fly during the publish.
+__device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool filled, bool next,
+                             const TileInfo& nt, u64* t_mid) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nk = (a.I + kBK - 1) / kBK;
+  const int rows_valid = ti.rows_valid, cols_valid = ti.cols_valid, r0 = ti.r0, n0 = ti.n0;
+  const TileCtx t = make_ctx(sm, a, ti, wave);
 
   // per-lane LDS element offsets of the MFMA fragments (stage 0, step 0)
   const int wn0 = (wave % kWavesN) * kWN;
@@ -441,10 +465,9 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // prologue: fill the ring, then wait for stage 0 (every wave's share)
-#pragma unroll
-  for (int s = 0; s < kStages; ++s)
-    if (s < nk) issue_stage(a, t, s, wave);
+  // prologue: fill the ring (unless done during the previous tile's
+  // publish), then wait for stage 0 (every wave's share)
+  if (!filled) issue_prologue(a, t, nk, wave);
   wait_stage(min(kStages - 1, nk - 1));
   block_barrier();
 
@@ -536,6 +559,12 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, int e, int r0, int rows_v
       if (n_ok && m < rows_valid)
         __builtin_nontemporal_store(v, (bf16x8*)(a.Y + (size_t)(r0 + m) * a.H + n0 + n));
     }
+  }
+  if (next) {
+    // every wave has read its block back (its stores carry the data), so
+    // the ring may be refilled with the next tile's first stages
+    block_barrier();
+    issue_prologue(a, make_ctx(sm, a, nt, wave), nk, wave);
   }
   t_mid[1] = now_100mhz();
 }
@@ -784,7 +813,7 @@ moe_gemm2_fused(KArgs a) {
       __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return;
   }
-  for (long long g = c; g < total; g += a.P) {
+  auto decode = [&](long long g) {
     const int s = (int)(g / W_comp);
     const long long idx = g - (long long)s * W_comp;
     const int mt = (int)(idx / a.ntps);
@@ -795,20 +824,32 @@ moe_gemm2_fused(KArgs a) {
       const int mid = (lo + hi + 1) >> 1;
       if (sm.tile_prefix[mid] <= mt) lo = mid; else hi = mid - 1;
     }
-    const int e = lo;
-    const int r0 = sm.start[e] + (mt - sm.tile_prefix[e]) * kBM;
-    const int rows_valid = min(kBM, sm.start[e] + sm.count[e] - r0);
-    const int n0 = s * a.nsplit + nt * kBN;
-    const int cols_valid = min(kBN, (s + 1) * a.nsplit - n0);
+    TileInfo ti;
+    ti.e = lo;
+    ti.r0 = sm.start[lo] + (mt - sm.tile_prefix[lo]) * kBM;
+    ti.rows_valid = min(kBM, sm.start[lo] + sm.count[lo] - ti.r0);
+    ti.n0 = s * a.nsplit + nt * kBN;
+    ti.cols_valid = min(kBN, (s + 1) * a.nsplit - ti.n0);
+    return ti;
+  };
+  const int nk = (a.I + kBK - 1) / kBK;
+  TileInfo cur = {0, 0, 0, 0, 0};
+  if (c < total) cur = decode(c);
+  bool filled = false;
+  for (long long g = c; g < total; g += a.P) {
+    const bool next = g + a.P < total;
+    const TileInfo nt = next ? decode(g + a.P) : cur;
     const u64 t_start = now_100mhz();
     u64 t_mid[2];
-    compute_tile(sm, a, e, r0, rows_valid, n0, cols_valid, t_mid);
+    compute_tile(sm, a, cur, filled, next, nt, t_mid);
     // publish: every wave waits until its Y stores are acknowledged by the
-    // L2 (vmcnt 0), the barrier orders those waits before thread 0, whose
-    // agent-scope release fence writes back the whole L2 (so every wave's
-    // stores) before the flag store.  One release per tile: a release in
-    // every wave cost ~10 us per tile in L2 write-back traffic.
-    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));   // vmcnt(0) lgkmcnt(0)
+    // L2 (vmcnt counts in issue order, so only the next tile's ring fill,
+    // issued after them, may stay in flight), the barrier orders those
+    // waits before thread 0, whose agent-scope release fence writes back
+    // the whole L2 (so every wave's stores) before the flag store.  One
+    // release per tile: a release in every wave cost ~10 us per tile in L2
+    // write-back traffic.
+    wait_stage(next ? min(kStages, nk) : 0);
     __syncthreads();
     if (threadIdx.x == 0) {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -820,6 +861,8 @@ moe_gemm2_fused(KArgs a) {
         a.trace[4 * g + 3] = now_100mhz();
       }
     }
+    cur = nt;
+    filled = next;
   }
   // after its tiles, a workgroup serves consumer tasks; they are dealt by
   // block id, which the dispatcher spreads round-robin over the XCDs (the
