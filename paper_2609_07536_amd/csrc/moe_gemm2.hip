@@ -240,7 +240,8 @@ __device__ void build_inverse(const KArgs& a, long long rows_dev) {
 //    line, so the 16 rows one 16-lane group of a 16-byte read touches fill
 //    all 64 banks;
 //  * W2 stage: kBK rows (k) of 512 bytes (32 chunks of 8 n); chunk c of row
-//    k sits at chunk c ^ 2(k & 3).
+//    k sits at chunk c ^ 4(k & 3), so the 32 lanes of a transposing read
+//    (4 rows x 64 bytes) hit 64 distinct banks.
 // x fragments are plain 16-byte LDS reads.  W2 is stored as in memory (n
 // contiguous) and read with ds_read_b64_tr_b16: in each group of 16 lanes,
 // lane i receives element i%4 of the 8-byte reads of lanes 4p + i/4
@@ -405,7 +406,7 @@ __device__ __forceinline__ TileCtx make_ctx(Smem& sm, const KArgs& a, const Tile
       t.xk[q] = 8 * lc;
       // W2: rows 2i + L/32, physical chunk L%32
       const int krow = 2 * i + (lane >> 5);
-      const int wc = (lane & 31) ^ (2 * (krow & 3));
+      const int wc = (lane & 31) ^ (4 * (krow & 3));
       const int n = 8 * wc < cols_valid ? 8 * wc : 0;               // columns past the tile: unused
       t.wgp[q] = w2e + n;
       t.wk[q] = krow;
@@ -444,7 +445,7 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) {
       const int col = wn0 + 32 * nb + 16 * rg + 8 * (u & 1) + 4 * (u >> 1);
-      offA[nb] = krow * kBN + (((col >> 3) ^ (2 * (krow & 3))) << 3) + (col & 7);
+      offA[nb] = krow * kBN + (((col >> 3) ^ (4 * (krow & 3))) << 3) + (col & 7);
     }
   }
   int offB[kKS];
