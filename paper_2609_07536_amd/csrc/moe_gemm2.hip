@@ -86,6 +86,7 @@ struct KArgs {
   int tasks_per_split;
   uint32_t epoch;
   const uint16_t* zeros;   // 16+ zero bytes (operand chunks past the reduction)
+  uint32_t* task_ctr;        // next consumer task (reset by workgroup 0 each launch)
 };
 
 struct Smem {
@@ -96,6 +97,7 @@ struct Smem {
   int tile_prefix[kMaxE + 1]; // exclusive prefix of ceil(count/kBM)
   int scan[kThreads];
   int flag;
+  int task;                   // consumer task claimed by the workgroup
 };
 
 // ---- memory-model helpers ----------------------------------------------------
@@ -214,6 +216,10 @@ __device__ void build_inverse(const KArgs& a, long long rows_dev) {
     }
     a.inv[(long long)t * a.topk + slot] = (int32_t)r;
   }
+  // workgroup 0 resets the consumer task counter; every claim comes after
+  // the claimer has seen all workgroups' flags, so after this store
+  if (blockIdx.x == 0 && threadIdx.x == 0)
+    __hip_atomic_store(a.task_ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   // as for a tile: per-wave vmcnt(0), barrier, one release by thread 0
   __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));
   __syncthreads();
@@ -423,8 +429,9 @@ __device__ __forceinline__ void issue_prologue(const KArgs& a, const TileCtx& t,
 }
 
 // Computes tile `ti` and stores it to Y.  Its ring fill was issued already
-// if `filled`; with `next`, the ring fill of tile `nt` is issued after this
-// tile's Y stores, so that its loads fly during the publish.
+// if `filled`; with `next`, the ring fill of tile `nt` is issued from this
+// tile's epilogue (stage 0 before the Y stores, stage 1 after them), so
+// that its loads fly during the stores and the publish.
 __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool filled, bool next,
                              const TileInfo& nt, u64* t_mid) {
   const int lane = threadIdx.x & 63;
@@ -520,40 +527,54 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
   block_barrier();
   t_mid[0] = now_100mhz();
 
-  // epilogue: the wave's kWM x kWN block goes through LDS (the ring is free
-  // now) as bf16 rows of 2 kWN bytes, 16-byte chunk j of row r at chunk
-  // j ^ ((r / r1) % c), c = chunks per row, r1 = rows per 256-byte bank line
-  // (so 16 consecutive rows hit 16 distinct bank groups), then leaves as
-  // whole rows of 2 kWN bytes (full 128-byte lines).
+  // The next tile's stage 0 goes into ring slot 0 now, ahead of this
+  // tile's Y stores in the load/store queue; slot 1 carries the epilogue,
+  // and the next tile's stage 1 follows the stores.
+  static_assert(kStages == 2, "the epilogue uses the second ring slot");
+  if (next) issue_stage(a, make_ctx(sm, a, nt, wave), 0, wave);
+
+  // epilogue: the wave's kWM x kWN block goes through LDS in two halves of
+  // 64 rows (8 KB per wave, in slot 1) as bf16 rows of 2 kWN bytes, 16-byte
+  // chunk j of row r at chunk j ^ ((r / r1) % c), c = chunks per row,
+  // r1 = rows per 256-byte bank line (so 16 consecutive rows hit 16 distinct
+  // bank groups), then leaves as whole rows of 2 kWN bytes (full 128-byte
+  // lines).  A wave's LDS operations run in order, so the second half may
+  // overwrite the first once its reads were issued.
   constexpr int kEpChunks = kWN / 8;
   constexpr int kEpRowsPerLine = 256 / (2 * kWN);
   constexpr int kEpRowsPerStore = 64 / kEpChunks;
+  constexpr int kEpRows = 64;                       // rows per half
+  static_assert(kWaves == 8 && kEpRows * kWN * 2 * 4 == kStageElems * 2, "epilogue halves fill slot 1");
   const int h = lane >> 5;
   __attribute__((address_space(3))) uint16_t* ep =
-      (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(t.lds_a) + wave * (kWM * kWN);
+      (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(wave < 4 ? lds_addr(&sm.a[1][0])
+                                                                         : lds_addr(&sm.b[1][0])) +
+      (wave & 3) * (kEpRows * kWN);
+  const int j = lane % kEpChunks;
+  const int n = wn0 + 8 * j;
+  const bool n_ok = n < cols_valid;
 #pragma unroll
-  for (int mb = 0; mb < kMB; ++mb) {
-    const int row = 32 * mb + (lane & 31);
-    const int sw = (row / kEpRowsPerLine) % kEpChunks;
+  for (int half = 0; half < kMB / 2; ++half) {
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb)
+    for (int mh = 0; mh < 2; ++mh) {
+      const int mb = 2 * half + mh;
+      const int row = 32 * mh + (lane & 31);
+      const int sw = (row / kEpRowsPerLine) % kEpChunks;
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        bf16x8 v;
+      for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = (__bf16)acc[nb][mb][8 * c + i];
-        const int chunk = 4 * nb + 2 * c + h;
-        *(__attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((chunk ^ sw) << 3)) = v;
-      }
-  }
-  {
-    const int j = lane % kEpChunks;
-    const int n = wn0 + 8 * j;
-    const bool n_ok = n < cols_valid;
+        for (int c = 0; c < 2; ++c) {
+          bf16x8 v;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) v[i] = (__bf16)acc[nb][mb][8 * c + i];
+          const int chunk = 4 * nb + 2 * c + h;
+          *(__attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((chunk ^ sw) << 3)) = v;
+        }
+    }
 #pragma unroll 4
-    for (int it = 0; it < kWM / kEpRowsPerStore; ++it) {
+    for (int it = 0; it < kEpRows / kEpRowsPerStore; ++it) {
       const int row = kEpRowsPerStore * it + lane / kEpChunks;
-      const int m = wm0 + row;
+      const int m = wm0 + kEpRows * half + row;
       const int sw = (row / kEpRowsPerLine) % kEpChunks;
       const bf16x8 v =
           *(const __attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((j ^ sw) << 3));
@@ -561,11 +582,11 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
         __builtin_nontemporal_store(v, (bf16x8*)(a.Y + (size_t)(r0 + m) * a.H + n0 + n));
     }
   }
-  if (next) {
+  if (next && nk > 1) {
     // every wave has read its block back (its stores carry the data), so
-    // the ring may be refilled with the next tile's first stages
+    // slot 1 may take the next tile's stage 1
     block_barrier();
-    issue_prologue(a, make_ctx(sm, a, nt, wave), nk, wave);
+    issue_stage(a, make_ctx(sm, a, nt, wave), 1, wave);
   }
   t_mid[1] = now_100mhz();
 }
@@ -742,13 +763,24 @@ __device__ void consume_task(const KArgs& a, const TaskMeta& m, int t0, int ntok
   }
 }
 
-__device__ void consumer_loop(Smem& sm, const KArgs& a, int cid, int ncons, long long W_comp) {
+// Serves consumer tasks until none is left.  Tasks are claimed one at a time
+// from a counter, in order (split 0 first), so whichever workgroup is free
+// takes the next one: consumers that finish early, or compute workgroups
+// with fewer tiles, absorb more of the earlier splits' work.
+__device__ void consumer_loop(Smem& sm, const KArgs& a, long long W_comp) {
   if (!wait_flags(sm, a.wg_flags, gridDim.x, a)) return;
   const int total = a.L * a.tasks_per_split;
   u64* trace_tasks = a.trace ? a.trace + 4 * a.max_tiles : nullptr;
   int ready = -1;  // splits [0, ready] are known to be published
   int meta_t0 = -1;  // token block whose metadata is in LDS
-  for (int task = cid; task < total; task += ncons) {
+  while (true) {
+    if (threadIdx.x == 0)
+      sm.task = (int)min(__hip_atomic_fetch_add(a.task_ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+                         (uint32_t)total);
+    __syncthreads();
+    const int task = sm.task;
+    __syncthreads();   // sm.task is rewritten by the next claim
+    if (task >= total) break;
     const int s = task / a.tasks_per_split;
     const int rem = task - s * a.tasks_per_split;
     const int tb = rem / a.cb_per_split;
@@ -804,7 +836,7 @@ moe_gemm2_fused(KArgs a) {
 
   const int b = blockIdx.x;
   if (b < a.C) {
-    consumer_loop(sm, a, b, a.C, W_comp);
+    consumer_loop(sm, a, W_comp);
     return;
   }
   const int c = compute_index(b, a.C, (int)gridDim.x);
@@ -844,13 +876,13 @@ moe_gemm2_fused(KArgs a) {
     u64 t_mid[2];
     compute_tile(sm, a, cur, filled, next, nt, t_mid);
     // publish: every wave waits until its Y stores are acknowledged by the
-    // L2 (vmcnt counts in issue order, so only the next tile's ring fill,
+    // L2 (vmcnt counts in issue order, so only the next tile's stage 1,
     // issued after them, may stay in flight), the barrier orders those
     // waits before thread 0, whose agent-scope release fence writes back
     // the whole L2 (so every wave's stores) before the flag store.  One
     // release per tile: a release in every wave cost ~10 us per tile in L2
     // write-back traffic.
-    wait_stage(next ? min(kStages, nk) : 0);
+    wait_stage(next && nk > 1 ? 1 : 0);
     __syncthreads();
     if (threadIdx.x == 0) {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -865,11 +897,8 @@ moe_gemm2_fused(KArgs a) {
     cur = nt;
     filled = next;
   }
-  // after its tiles, a workgroup serves consumer tasks; they are dealt by
-  // block id, which the dispatcher spreads round-robin over the XCDs (the
-  // compute index packs them into one XCD, whose fabric link then limits
-  // a small task set)
-  if (a.drain) consumer_loop(sm, a, b - a.C, a.P, W_comp);
+  // after its tiles, a workgroup serves consumer tasks
+  if (a.drain) consumer_loop(sm, a, W_comp);
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -911,7 +940,8 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->tasks_per_split = ((wl->T + kCommTM - 1) / kCommTM) * L->cb_per_split;
   L->max_tiles = (long long)wl->splits * L->ntps * ((L->rows + kBM - 1) / kBM + wl->E);
   size_t off = 0;
-  L->status = off;   // word 0: status bits; bytes kZeroBlock..255: zeros, never written
+  L->status = off;   // word 0: status bits; word 16: consumer task counter;
+                     // bytes kZeroBlock..255: zeros, never written
   off += 256;
   L->wg_flags = off;
   off += (size_t)kMaxGrid * 4;
@@ -1089,6 +1119,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.inv = reinterpret_cast<int32_t*>(ws + L.inv);
   a.status = reinterpret_cast<uint32_t*>(ws + L.status);
   a.zeros = reinterpret_cast<const uint16_t*>(ws + L.status + kZeroBlock);
+  a.task_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 64);
   a.trace = reinterpret_cast<u64*>(trace);
   a.rows = L.rows;
   a.max_tiles = L.max_tiles;
