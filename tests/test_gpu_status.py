@@ -1,0 +1,133 @@
+"""GPU: the traced entry point, the device status word (bad routing, the
+consumer watchdog) and recovery after an error.
+
+Every failure here is forced from the host (bad ids in the routing arrays,
+a tiny spin limit on the kernel's own bounded waits); every launch still
+ends normally."""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import combine as oc
+from workloads import custom
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(got, ref, what=""):
+    rl2 = oc.rel_l2(got, ref)
+    mab = oc.max_abs_ratio(got, ref)
+    print(f"{what}: rel_l2={rl2:.3e} max_abs/max_ref={mab:.3e}", flush=True)
+    assert np.isfinite(got).all()
+    assert rl2 <= oc.REL_L2_TOL, (what, rl2)
+    assert mab <= oc.MAX_ABS_TOL, (what, mab)
+
+
+def _small(seed=5):
+    return custom(T=700, H=512, I=96, E=6, topk=3, L=2, routing=("zipf", 1.0), seed=seed)
+
+
+def test_traced_matches_untraced(gpu_lib):
+    import torch
+
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    w = _small()
+    dev = gpu_util.to_device(w)
+    for C in (0, 4):
+        plain, used, ws = gpu_util.run(w, C=C, dev=dev)
+        wl, _ = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, w.counts)
+        trace = torch.zeros(B.trace_size(wl) // 8, dtype=torch.int64, device="cuda")
+        traced, used2, _ = gpu_util.run(w, C=C, dev=dev, workspace=ws, trace=trace)
+        assert used2 == used
+        assert np.array_equal(traced.view(np.uint32), plain.view(np.uint32))
+        tr = trace.cpu().numpy().astype(np.int64)
+        p = B.default_params(0)
+        r, part = B.select_partition(wl, p)
+        n_tiles = int(part.W_comp) * w.L
+        t = tr[:4 * n_tiles].reshape(-1, 4)
+        assert (t[:, 3] > 0).all(), "every tile publishes"
+        assert (np.diff(t, axis=1) >= 0).all(), "tile timestamps ordered"
+        n_tasks = w.L * ((w.T + 63) // 64) * ((w.H // w.L + 1023) // 1024)
+        k = tr[len(tr) - 4 * n_tasks:].reshape(-1, 4)
+        assert (k[:, 2] > 0).all(), "every consumer task recorded"
+        assert (k[:, 1] >= k[:, 0]).all() and (k[:, 2] >= k[:, 1]).all()
+        assert (k[:, 3] >= 0).all() and (k[:, 3] < 4096).all()   # block ids
+
+
+def test_bad_token_ids_flagged_and_skipped(gpu_lib):
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    w = _small(seed=6)
+    rng = np.random.default_rng(1)
+    bad = rng.choice(w.token_ids.size, size=9, replace=False)
+    gate_ref = w.gate_w.copy()
+    gate_ref[bad] = 0.0                        # a skipped row contributes nothing
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, gate_ref, w.T)
+    w.token_ids = w.token_ids.copy()
+    w.token_ids[bad[:5]] = w.T + 7             # past the last token
+    w.token_ids[bad[5:]] = -3                  # negative
+    for C in (0, 3):
+        got, used, ws = gpu_util.run(w, C=C, check_status=False)
+        assert ws.status() == B.MOE_ERR_BAD_ROUTING
+        assert ws.status(clear=True) == B.MOE_ERR_BAD_ROUTING
+        assert ws.status() == 0                # cleared
+        _check(got, ref, f"bad ids C={used}")
+
+
+def test_token_with_too_many_rows_flagged(gpu_lib):
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    w = _small(seed=7)
+    # give token 0 one row more than top-k (taken from some other token)
+    rows0 = np.flatnonzero(w.token_ids == 0)
+    assert rows0.size == w.topk
+    donor_row = int(np.flatnonzero(w.token_ids != 0)[0])
+    donor = int(w.token_ids[donor_row])
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+    w.token_ids = w.token_ids.copy()
+    w.token_ids[donor_row] = 0
+    got, used, ws = gpu_util.run(w, C=2, check_status=False)
+    assert ws.status(clear=True) == B.MOE_ERR_BAD_ROUTING
+    keep = np.ones(w.T, dtype=bool)
+    keep[[0, donor]] = False                   # which of token 0's rows is dropped is unordered
+    _check(got[keep], ref[keep], "too many rows")
+    assert np.isfinite(got).all()
+
+
+def test_bad_expert_offsets_clamped(gpu_lib):
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    w = _small(seed=8)
+    off = w.expert_offsets.copy()
+    off[2], off[3] = off[3] + 5, off[2]        # decreasing, and past its neighbour
+    off[-1] = off[-1] + 1000                   # past the rows (clamped to rows)
+    w.expert_offsets = off
+    got, used, ws = gpu_util.run(w, C=0, counts=False, check_status=False)
+    assert ws.status(clear=True) == B.MOE_ERR_BAD_ROUTING
+    assert np.isfinite(got).all()
+
+
+def test_watchdog_expires_and_next_launch_is_clean(gpu_lib):
+    """A spin limit of 1 makes every consumer wait give up at once: the
+    launch ends with MOE_ERR_TIMEOUT; the next launch on the same workspace
+    is correct."""
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    w = _small(seed=9)
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+    dev = gpu_util.to_device(w)
+    old = os.environ.get("MOE_GEMM2_SPIN_LIMIT")
+    os.environ["MOE_GEMM2_SPIN_LIMIT"] = "1"
+    try:
+        _, used, ws = gpu_util.run(w, C=8, dev=dev, check_status=False)
+        st = ws.status(clear=True)
+    finally:
+        if old is None:
+            del os.environ["MOE_GEMM2_SPIN_LIMIT"]
+        else:
+            os.environ["MOE_GEMM2_SPIN_LIMIT"] = old
+    assert st == B.MOE_ERR_TIMEOUT, B.strerror(st)
+    got, used, ws = gpu_util.run(w, C=8, dev=dev, workspace=ws)
+    _check(got, ref, "after timeout")
