@@ -9,9 +9,11 @@
  *   out[t, :] = sum over rows r with token_ids[r] == t of gate_w[r] * Y[r, :]
  *
  * computed by one persistent kernel whose workgroups take one of two roles:
- * compute workgroups run the grouped GEMM tile by tile and publish each
- * finished tile with a readiness flag and a per-split counter; consumer
- * workgroups wait until a split is published and then gather each token's
+ * compute workgroups run the grouped GEMM tile by tile and publish their
+ * tiles with per-tile readiness flags (one release per workgroup and split,
+ * after its last tile of the split); consumer workgroups (or, with C = 0,
+ * every workgroup once its tiles are done) claim tasks in order, wait until
+ * the task's split is published and then gather each token's
  * rows, weight them by the gates and write the token's output once.  The
  * number of consumer workgroups C is the paper's decision variable; the
  * selector below evaluates its wave-quantized makespan model (Method,
@@ -177,7 +179,8 @@ int moe_gemm2_combine(const void* x_perm, const void* w2, const int32_t* expert_
  * constant 100 MHz clock) into trace (device, 8-byte aligned, at least
  * moe_gemm2_trace_size(wl) bytes).  Layout, uint64 words: for each compute
  * tile g of the global sequence, words 4g..4g+3 = start, end of the
- * reduction loop, end of the Y stores, publish; then, from word
+ * reduction loop, end of the Y stores, end of the tile (after the split's
+ * publish for a workgroup's last tile of a split); then, from word
  * 4 * max_tiles (max_tiles = splits * ceil(H/splits/256) *
  * (ceil(rows/256) + E)), for each consumer task j, words 4j..4j+3 = wait
  * start, wait end, finish, workgroup id.  The arithmetic and the result are

@@ -7,8 +7,9 @@
 //  * compute workgroups walk the global tile sequence (split-major, then
 //    expert, then m-tile, then n-tile; compute workgroup b takes tiles b,
 //    b+P, b+2P, ...), run one 256x256 tile of Y = x_perm @ W2[e] on bf16
-//    MFMA with LDS double buffering, store it to the bf16 staging buffer and
-//    publish it (one agent-scope release, then its per-tile flag);
+//    MFMA with LDS double buffering and store it to the bf16 staging
+//    buffer; after its last tile of a split a workgroup publishes all its
+//    tiles of that split (one agent-scope release, then their flags);
 //  * consumer workgroups wait until every tile of a split is published
 //    (agent-scope acquire), then, per task of 64 tokens x 1024 columns,
 //    gather each token's rows, weight them by the gates and write the
@@ -869,30 +870,37 @@ moe_gemm2_fused(KArgs a) {
   TileInfo cur = {0, 0, 0, 0, 0};
   if (c < total) cur = decode(c);
   bool filled = false;
+  long long split_first = c;   // this workgroup's first tile of the current split
   for (long long g = c; g < total; g += a.P) {
     const bool next = g + a.P < total;
     const TileInfo nt = next ? decode(g + a.P) : cur;
     const u64 t_start = now_100mhz();
     u64 t_mid[2];
     compute_tile(sm, a, cur, filled, next, nt, t_mid);
-    // publish: every wave waits until its Y stores are acknowledged by the
-    // L2 (vmcnt counts in issue order, so only the next tile's stage 1,
-    // issued after them, may stay in flight), the barrier orders those
-    // waits before thread 0, whose agent-scope release fence writes back
-    // the whole L2 (so every wave's stores) before the flag store.  One
-    // release per tile: a release in every wave cost ~10 us per tile in L2
-    // write-back traffic.
-    wait_stage(next && nk > 1 ? 1 : 0);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-      __hip_atomic_store(&a.tile_flags[g], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (a.trace) {
-        a.trace[4 * g + 0] = t_start;
-        a.trace[4 * g + 1] = t_mid[0];
-        a.trace[4 * g + 2] = t_mid[1];
-        a.trace[4 * g + 3] = now_100mhz();
+    // Publish once per split: consumers wait for whole splits, so the tiles
+    // of a split are published together after this workgroup's last tile of
+    // it (an agent-scope release writes back the whole L2; once per tile it
+    // cost ~3.6 us per tile).  Every wave waits until its Y stores are
+    // acknowledged by the L2 (vmcnt counts in issue order, so only the next
+    // tile's stage 1, issued after them, may stay in flight), the barrier
+    // orders those waits before thread 0, whose release fence writes back
+    // the L2 before it stores the flags.
+    const bool last_of_split = !next || (g + a.P) / W_comp != g / W_comp;
+    if (last_of_split) {
+      wait_stage(next && nk > 1 ? 1 : 0);
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        for (long long gg = split_first; gg <= g; gg += a.P)
+          __hip_atomic_store(&a.tile_flags[gg], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
+      split_first = g + a.P;
+    }
+    if (a.trace && threadIdx.x == 0) {
+      a.trace[4 * g + 0] = t_start;
+      a.trace[4 * g + 1] = t_mid[0];
+      a.trace[4 * g + 2] = t_mid[1];
+      a.trace[4 * g + 3] = now_100mhz();
     }
     cur = nt;
     filled = next;
