@@ -126,9 +126,12 @@ __device__ __forceinline__ uint32_t epoch_count(u64 v, uint32_t epoch) {
 __device__ __forceinline__ u64 now_100mhz() { return __builtin_amdgcn_s_memrealtime(); }
 
 // Wave 0 polls flags[0..n) until every flag equals the epoch (bounded),
-// advancing past the leading run of set flags; then the whole workgroup
-// acquires.  Returns false (and records a timeout) if the bound expired.
-__device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& a) {
+// advancing past the leading run of set flags; then, with `acquire`, the
+// whole workgroup acquires (without it, a later acquire must precede any
+// read of the data these flags publish).  Returns false (and records a
+// timeout) if the bound expired.
+__device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& a,
+                           bool acquire = true) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
     long long i = 0, spins = 0;
@@ -156,7 +159,7 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
   }
   __syncthreads();
   const bool ok = sm.flag != 0;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  if (acquire) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();  // sm.flag may be rewritten by the next wait
   return ok;
 }
@@ -769,7 +772,10 @@ __device__ void consume_task(const KArgs& a, const TaskMeta& m, int t0, int ntok
 // takes the next one: consumers that finish early, or compute workgroups
 // with fewer tiles, absorb more of the earlier splits' work.
 __device__ void consumer_loop(Smem& sm, const KArgs& a, long long W_comp) {
-  if (!wait_flags(sm, a.wg_flags, gridDim.x, a)) return;
+  // An acquire invalidates this XCD's L2 (also under the compute workgroups
+  // still running there), so there is one per split: the inverse map's
+  // flags are acquired together with the first split's, before any read.
+  if (!wait_flags(sm, a.wg_flags, gridDim.x, a, W_comp == 0)) return;
   const int total = a.L * a.tasks_per_split;
   u64* trace_tasks = a.trace ? a.trace + 4 * a.max_tiles : nullptr;
   int ready = -1;  // splits [0, ready] are known to be published
