@@ -1018,10 +1018,10 @@ int device_info(int dev, DevInfo* out) {
 // rho_ref of the fused kernel on MI355X: mean consumer-task time over mean
 // compute-tile time (one consumer wave over one compute wave), measured with
 // the traced entry point at the reference configuration (T=16384, H=2048,
-// I=704, E=32, top-6, L=2, C=32): 30.6 us / 27.0 us = 1.13.
+// I=704, E=32, top-6, L=2, C=32): 28.4 us / 22.5 us = 1.26.
 // MOE_GEMM2_RHO_REF="num/den" overrides it.
-constexpr int64_t kRhoRefNum = 113;
-constexpr int64_t kRhoRefDen = 100;
+constexpr int64_t kRhoRefNum = 63;
+constexpr int64_t kRhoRefDen = 50;
 constexpr int kDefaultFixedC = 8;
 
 void fill_params(const DevInfo& d, moe_select_params_t* p) {
