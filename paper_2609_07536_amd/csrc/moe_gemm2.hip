@@ -204,8 +204,11 @@ __device__ void load_experts(Smem& sm, const KArgs& a) {
   __syncthreads();
 }
 
-// Rows of each token, for the owner-write combine.
-__device__ void build_inverse(const KArgs& a, long long rows_dev) {
+// Rows of each token, for the owner-write combine.  With `publish`, the
+// workgroup's share is published at once (release + its workgroup flag);
+// otherwise the caller publishes it later, with its first split's tiles
+// (one L2 write-back for both).
+__device__ void build_inverse(const KArgs& a, long long rows_dev, bool publish) {
   const long long stride = (long long)gridDim.x * kThreads;
   for (long long r = (long long)blockIdx.x * kThreads + threadIdx.x; r < rows_dev; r += stride) {
     const int t = a.token_ids[r];
@@ -224,7 +227,8 @@ __device__ void build_inverse(const KArgs& a, long long rows_dev) {
   // the claimer has seen all workgroups' flags, so after this store
   if (blockIdx.x == 0 && threadIdx.x == 0)
     __hip_atomic_store(a.task_ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  // as for a tile: per-wave vmcnt(0), barrier, one release by thread 0
+  if (!publish) return;
+  // as for a split: per-wave vmcnt(0), barrier, one release by thread 0
   __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -837,17 +841,20 @@ moe_gemm2_fused(KArgs a) {
   __shared__ Smem sm;
   load_experts(sm, a);
   const long long rows_dev = a.E > 0 ? (long long)sm.start[a.E - 1] + sm.count[a.E - 1] : 0;
-  build_inverse(a, rows_dev);
   const long long m_tiles = sm.tile_prefix[a.E];
   const long long W_comp = m_tiles * a.ntps;
-
   const int b = blockIdx.x;
+  const int c = b < a.C ? 0 : compute_index(b, a.C, (int)gridDim.x);
+  const long long total = W_comp * a.L;
+  // A compute workgroup with a tile in split 0 publishes its share of the
+  // inverse map with that split (consumers read it only after a split).
+  const bool defer_inverse = b >= a.C && c < W_comp && total <= a.max_tiles;
+  build_inverse(a, rows_dev, !defer_inverse);
+
   if (b < a.C) {
     consumer_loop(sm, a, W_comp);
     return;
   }
-  const int c = compute_index(b, a.C, (int)gridDim.x);
-  const long long total = W_comp * a.L;
   if (total > a.max_tiles) {  // cannot happen with sanitized offsets; stay in bounds
     if (threadIdx.x == 0)
       __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -899,6 +906,9 @@ moe_gemm2_fused(KArgs a) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         for (long long gg = split_first; gg <= g; gg += a.P)
           __hip_atomic_store(&a.tile_flags[gg], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (defer_inverse && split_first == c)   // first publish: also the inverse map
+          __hip_atomic_store(&a.wg_flags[blockIdx.x], a.epoch, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
       }
       split_first = g + a.P;
     }
