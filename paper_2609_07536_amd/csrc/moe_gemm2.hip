@@ -849,17 +849,6 @@ moe_gemm2_fused(KArgs a) {
   // A compute workgroup with a tile in split 0 publishes its share of the
   // inverse map with that split (consumers read it only after a split).
   const bool defer_inverse = b >= a.C && c < W_comp && total <= a.max_tiles;
-  build_inverse(a, rows_dev, !defer_inverse);
-
-  if (b < a.C) {
-    consumer_loop(sm, a, W_comp);
-    return;
-  }
-  if (total > a.max_tiles) {  // cannot happen with sanitized offsets; stay in bounds
-    if (threadIdx.x == 0)
-      __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return;
-  }
   auto decode = [&](long long g) {
     const int s = (int)(g / W_comp);
     const long long idx = g - (long long)s * W_comp;
@@ -880,9 +869,27 @@ moe_gemm2_fused(KArgs a) {
     return ti;
   };
   const int nk = (a.I + kBK - 1) / kBK;
+  // A compute workgroup issues its first tile's ring fill before building
+  // its share of the inverse map, so those loads fly during its atomics.
   TileInfo cur = {0, 0, 0, 0, 0};
-  if (c < total) cur = decode(c);
   bool filled = false;
+  if (b >= a.C && total <= a.max_tiles && c < total) {
+    cur = decode(c);
+    issue_prologue(a, make_ctx(sm, a, cur, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)), nk,
+                   __builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
+    filled = true;
+  }
+  build_inverse(a, rows_dev, !defer_inverse);
+
+  if (b < a.C) {
+    consumer_loop(sm, a, W_comp);
+    return;
+  }
+  if (total > a.max_tiles) {  // cannot happen with sanitized offsets; stay in bounds
+    if (threadIdx.x == 0)
+      __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
   long long split_first = c;   // this workgroup's first tile of the current split
   for (long long g = c; g < total; g += a.P) {
     const bool next = g + a.P < total;
