@@ -70,7 +70,7 @@ struct KArgs {
   uint16_t* Y;                // [rows, H] bf16 staging
   uint32_t* tile_flags;       // [max_tiles]: epoch once tile g is published
   uint32_t* wg_flags;         // [kMaxGrid]: epoch once workgroup b added its inverse-map rows
-  u64* tok_cnt;               // [T]: epoch-tagged count of each token's rows
+  u64* tok_cnt;               // [T]: launch-tagged count of each token's rows
   int32_t* inv;               // [T, topk]
   uint32_t* status;           // [1]
   u64* trace;                 // optional
@@ -85,7 +85,8 @@ struct KArgs {
   int comm_tn;                // consumer task width (<= kCommTN)
   int cb_per_split;           // consumer column blocks per split
   int tasks_per_split;
-  uint32_t epoch;
+  uint32_t epoch;             // launch epoch (flags: low 32 bits of the launch counter)
+  u64 cnt_epoch;              // launch counter mod 2^40, << 24 (token counters)
   const uint16_t* zeros;   // 16+ zero bytes (operand chunks past the reduction)
   uint32_t* task_ctr;        // next consumer task (reset by workgroup 0 each launch)
 };
@@ -106,21 +107,14 @@ __device__ __forceinline__ u64 ld_relaxed(u64* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Increment an epoch-tagged counter (high 32 bits: epoch, low: count); a
-// counter from an older epoch counts as zero.  Returns the count before.
-__device__ uint32_t epoch_inc(u64* p, uint32_t epoch) {
-  u64 old = ld_relaxed(p);
-  while (true) {
-    const bool cur = (uint32_t)(old >> 32) == epoch;
-    const u64 nw = cur ? old + 1ull : (((u64)epoch << 32) | 1ull);
-    if (__hip_atomic_compare_exchange_strong(p, &old, nw, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_AGENT))
-      return cur ? (uint32_t)old : 0u;
-  }
-}
+// Per-token row counters: the launch counter (mod 2^40) in the high 40
+// bits, the count in the low 24; a counter from an older launch counts as
+// zero.  Launch counters only grow, so an atomic max opens a launch's count.
+constexpr int kCntBits = 24;
+constexpr u64 kCntMask = (1ull << kCntBits) - 1;
 
-__device__ __forceinline__ uint32_t epoch_count(u64 v, uint32_t epoch) {
-  return (uint32_t)(v >> 32) == epoch ? (uint32_t)v : 0u;
+__device__ __forceinline__ uint32_t epoch_count(u64 v, u64 cnt_epoch) {
+  return (v & ~kCntMask) == cnt_epoch ? (uint32_t)(v & kCntMask) : 0u;
 }
 
 __device__ __forceinline__ u64 now_100mhz() { return __builtin_amdgcn_s_memrealtime(); }
@@ -216,7 +210,14 @@ __device__ void build_inverse(const KArgs& a, long long rows_dev, bool publish) 
       __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       continue;
     }
-    const uint32_t slot = epoch_inc(&a.tok_cnt[t], a.epoch);
+    // Open this launch's count (a counter from an older launch holds a
+    // smaller epoch in its high word), then take a slot.  The two atomics
+    // of a thread on one address are performed in order, so the add always
+    // sees this epoch; no compare-and-swap, no dependent round trip.
+    __hip_atomic_fetch_max(&a.tok_cnt[t], a.cnt_epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const u64 old = __hip_atomic_fetch_add(&a.tok_cnt[t], 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t slot =
+        (old & ~kCntMask) == a.cnt_epoch ? (uint32_t)(old & kCntMask) : 0xffffffffu;
     if (slot >= (uint32_t)a.topk) {
       __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       continue;
@@ -623,7 +624,7 @@ __device__ void load_task_meta(TaskMeta& m, const KArgs& a, int t0, int ntok) {
   for (int i = threadIdx.x; i < ntok * K; i += kThreads) {
     const int t = i / K;
     const int j = i - t * K;
-    const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t0 + t]), a.epoch);
+    const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t0 + t]), a.cnt_epoch);
     const int n = (int)(have < (uint32_t)K ? have : (uint32_t)K);
     int r = 0;
     float g = 0.f;
@@ -995,7 +996,7 @@ struct DevInfo {
 };
 std::mutex g_mu;
 DevInfo g_dev[64];
-std::atomic<uint32_t> g_epoch{0};
+std::atomic<uint64_t> g_epoch{0};
 
 int device_info(int dev, DevInfo* out) {
   if (dev < 0 || dev >= 64) return MOE_ERR_INVALID_ARG;
@@ -1173,9 +1174,10 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.comm_tn = L.comm_tn;
   a.cb_per_split = L.cb_per_split;
   a.tasks_per_split = L.tasks_per_split;
-  uint32_t ep = g_epoch.fetch_add(1) + 1;
-  if (ep == 0) ep = g_epoch.fetch_add(1) + 1;  // 0 is the cleared state
-  a.epoch = ep;
+  uint64_t ep = g_epoch.fetch_add(1) + 1;
+  if ((uint32_t)ep == 0) ep = g_epoch.fetch_add(1) + 1;  // flag value 0 is the cleared state
+  a.epoch = (uint32_t)ep;
+  a.cnt_epoch = (ep & ((1ull << (64 - kCntBits)) - 1)) << kCntBits;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipLaunchKernelGGL(moe_gemm2_fused, dim3(C + P), dim3(kThreads), 0, s, a);
