@@ -78,6 +78,11 @@ def lib() -> ctypes.CDLL:
                 raise ImportError(
                     f"{LIB_PATH} is missing: build it with "
                     "`python -m paper_2609_07536_amd.build`")
+            # torch first: it brings its own HIP runtime, which then also
+            # serves this library (same soname).  Loaded the other way
+            # round, the process would hold two HIP runtimes, and torch's
+            # device memory and streams would be invalid in ours.
+            import torch  # noqa: F401
             L = ctypes.CDLL(LIB_PATH)
             vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
             L.moe_select_partition.argtypes = [ctypes.POINTER(Workload),

@@ -131,3 +131,36 @@ def test_watchdog_expires_and_next_launch_is_clean(gpu_lib):
     assert st == B.MOE_ERR_TIMEOUT, B.strerror(st)
     got, used, ws = gpu_util.run(w, C=8, dev=dev, workspace=ws)
     _check(got, ref, "after timeout")
+
+
+def test_two_streams_at_once(gpu_lib):
+    """Two launches in flight together on two streams with two workspaces
+    (each with its own consumers or the role switch) both come out right:
+    launches share nothing but the library's launch counter, and a
+    persistent grid that cannot be fully resident still drains because
+    compute workgroups never wait."""
+    import torch
+
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    wa = _small(seed=11)
+    wb = custom(T=1500, H=1024, I=128, E=12, topk=4, L=2, routing=("zipf", 0.8), seed=12)
+    refs = [oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+            for w in (wa, wb)]
+    devs = [gpu_util.to_device(w) for w in (wa, wb)]
+    outs = [torch.empty((w.T, w.H), dtype=torch.float32, device="cuda") for w in (wa, wb)]
+    wss = []
+    for w in (wa, wb):
+        wl, _ = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, w.counts)
+        wss.append(B.Workspace(B.workspace_size(wl)))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]   # default priority
+    for Cs in ((0, 4), (8, 0), (3, 3)):
+        for w, d, o, ws, st, C in zip((wa, wb), devs, outs, wss, streams, Cs):
+            x, w2, off, tid, g = d
+            B.combine(x, w2, off, tid, g, T=w.T, splits=w.L, topk=w.topk, counts=w.counts,
+                      num_consumers=C, out=o, workspace=ws, stream=st)
+        torch.cuda.synchronize()
+        for w, o, ws, ref, C in zip((wa, wb), outs, wss, refs, Cs):
+            assert ws.status() == 0
+            _check(o.cpu().numpy(), ref, f"two streams C={C}")
