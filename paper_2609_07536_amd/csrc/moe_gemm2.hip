@@ -87,8 +87,8 @@ struct KArgs {
   int tasks_per_split;
   uint32_t epoch;             // launch epoch (flags: low 32 bits of the launch counter)
   u64 cnt_epoch;              // launch counter mod 2^40, << 24 (token counters)
-  const uint16_t* zeros;   // 16+ zero bytes (operand chunks past the reduction)
-  uint32_t* task_ctr;        // next consumer task (reset by workgroup 0 each launch)
+  const uint16_t* zeros;      // 16+ zero bytes (operand chunks past the reduction)
+  uint32_t* task_ctr;         // next consumer task (reset by workgroup 0 each launch)
 };
 
 struct Smem {
@@ -159,8 +159,11 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
 }
 
 // ---- prologue: expert ranges and the routed-tile prefix ----------------------
-// Offsets are clamped into [0, rows] and made non-decreasing so every row
-// range stays inside the buffers even for bad input (which is flagged).
+// Each expert's row range is clamped into [0, rows] with end >= start, so
+// every row range stays inside the buffers even for bad input (which is
+// flagged); overlapping ranges from bad input compute some rows twice (with
+// meaningless values), and a tile count past the workspace's capacity makes
+// the compute workgroups stop (flagged) instead of indexing past it.
 __device__ void load_experts(Smem& sm, const KArgs& a) {
   const int tid = threadIdx.x;
   bool bad = false;
