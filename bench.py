@@ -94,31 +94,37 @@ class DevWorkload:
         self.wl, self._keep = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, w.counts)
         self.ws = B.Workspace(B.workspace_size(self.wl))
 
-    def run(self, C=-1, trace=None):
+    def run(self, C=-1, trace=None, mode=None):
+        """One launch; mode None is moe_gemm2_combine (owner-write), 0/1 go
+        through moe_gemm2_combine_ex."""
         w = self.w
         return self.B.combine(self.x, self.w2, self.off, self.tid, self.g, T=w.T, splits=w.L,
                               topk=w.topk, counts=w.counts, num_consumers=C, out=self.out,
-                              workspace=self.ws, trace=trace)[1]
+                              workspace=self.ws, trace=trace, mode=mode)[1]
 
-    def trace(self, C):
+    def trace(self, C, mode=None):
         """One traced launch: (C used, tiles [n,4], tasks [m,4]) timestamps."""
-        torch, B = self.torch, self.B
+        torch, B, w = self.torch, self.B, self.w
         buf = torch.zeros(B.trace_size(self.wl) // 8, dtype=torch.int64, device="cuda")
-        used = self.run(C, trace=buf)
+        used = self.run(C, trace=buf, mode=mode)
         torch.cuda.synchronize()
         tr = buf.cpu().numpy().astype(np.int64)
         part = B.select_partition(self.wl, B.default_params(0))[1]
-        n_tiles = int(part.W_comp) * self.w.L
-        ntasks = int(part.W_comm) * self.w.L
+        n_tiles = int(part.W_comp) * w.L
+        ntasks = n_tiles if mode == 1 else int(part.W_comm) * w.L
+        # tile records first (room for max_tiles), then the task records
+        max_tiles = w.L * (-(-(w.H // w.L) // 256)) * (-(-w.Mtot // 256) + w.E)
         tiles = tr[: 4 * n_tiles].reshape(-1, 4)
-        tasks = tr[len(tr) - 4 * ntasks:].reshape(-1, 4) if ntasks else np.zeros((0, 4), np.int64)
+        tasks = tr[4 * max_tiles: 4 * (max_tiles + ntasks)].reshape(-1, 4)
         return used, tiles, tasks
 
 
-def breakdown(dw, C):
+def breakdown(dw, C, mode=None):
     w = dw.w
     flops, gemm_bytes, combine_bytes, _ = algorithmic(w)
-    used, tiles, tasks = dw.trace(C)
+    used, tiles, tasks = dw.trace(C, mode)
+    if mode == 1:   # Y read, ids and gates, one fp32 atomic per routed element, zeroing
+        combine_bytes = w.Mtot * w.H * 2 + w.Mtot * 8 + w.Mtot * w.H * 4 + w.T * w.H * 4
     gemm_span = (tiles[:, 3].max() - tiles[:, 0].min()) * TICK_S
     gp = {"span_us": gemm_span * 1e6, "tflops": flops / gemm_span / 1e12,
           "pct_peak": 100 * flops / gemm_span / 1e12 / PEAK_BF16_TFLOPS,
@@ -135,12 +141,12 @@ def breakdown(dw, C):
     return used, gp, comb
 
 
-def calibrate(dw, C_ref=32, reps=5):
+def calibrate(dw, C_ref=32, reps=5, mode=None):
     """rho_ref: one consumer-task wave over one compute-tile wave, measured at
     a fixed consumer count (the paper's calibration procedure)."""
     task_t, tile_t = [], []
     for _ in range(reps):
-        _, tiles, tasks = dw.trace(C_ref)
+        _, tiles, tasks = dw.trace(C_ref, mode)
         tile_t.append((tiles[:, 3] - tiles[:, 0]).mean())
         task_t.append((tasks[:, 2] - tasks[:, 1]).mean())
     tile_us = float(np.median(tile_t)) * TICK_S * 1e6
@@ -150,11 +156,16 @@ def calibrate(dw, C_ref=32, reps=5):
 
 
 def time_launches(dw, Cs, samples, torch):
-    """Median event time per C, samples interleaved forward/backward (ABBA)."""
+    """Median event time per C, samples interleaved forward/backward (ABBA).
+    A C may be a (C, mode) pair to time moe_gemm2_combine_ex in that mode."""
     stream = torch.cuda.current_stream()
     times = {C: [] for C in Cs}
+
+    def launch(C):
+        return dw.run(C[0], mode=C[1]) if isinstance(C, tuple) else dw.run(C)
+
     for C in Cs:               # warm-up of every partition
-        dw.run(C)
+        launch(C)
     torch.cuda.synchronize()
     for s in range(samples):
         order = list(Cs) if s % 2 == 0 else list(reversed(Cs))
@@ -162,7 +173,7 @@ def time_launches(dw, Cs, samples, torch):
         for C in order:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            dw.run(C)
+            launch(C)
             b.record(stream)
             evs.append((C, a, b))
         torch.cuda.synchronize()
@@ -250,7 +261,9 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--sweep-samples", type=int, default=7)
     ap.add_argument("--calibrate", action="store_true",
-                    help="print the rho_ref calibration at C=32 and exit")
+                    help="print the rho_ref calibration at C=32 (both consumer modes) and exit")
+    ap.add_argument("--no-scatter", action="store_true",
+                    help="skip the comparison with the atomic-scatter consumer mode")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 3 device copies of MIB MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -279,8 +292,11 @@ def main():
     dw = DevWorkload(w, B, torch)
     if args.calibrate:
         dw.run(32)
+        dw.run(32, mode=1)
         torch.cuda.synchronize()
-        print(json.dumps({"calibration": calibrate(dw), "kernel_sha": kernel_sha()}), flush=True)
+        print(json.dumps({"calibration": calibrate(dw),
+                          "calibration_scatter": calibrate(dw, mode=1),
+                          "kernel_sha": kernel_sha()}), flush=True)
         return
     stream = torch.cuda.current_stream()
 
@@ -336,6 +352,25 @@ def main():
     st = dw.ws.status()
     assert st == 0, B.strerror(st)
 
+    scatter = None
+    if not args.no_scatter:
+        # the atomic-scatter consumer (mode 1) against the owner-write one,
+        # launch for launch (ABBA), each with the selector's pick and C = 0
+        log("owner-write vs atomic scatter")
+        C_sc = dw.run(-1, mode=1)
+        torch.cuda.synchronize()
+        keys = sorted({(C_used, 0), (0, 0), (C_sc, 1), (0, 1)})
+        med = time_launches(dw, keys, 15, torch)
+        st = dw.ws.status()
+        assert st == 0, B.strerror(st)
+        _, gp_sc, comb_sc = breakdown(dw, C_sc, mode=1)
+        scatter = {"selector_C": C_sc,
+                   "us_per_layer": {f"mode{m}_C{c}": round(v * 1e3, 1)
+                                    for (c, m), v in med.items()},
+                   "scatter_over_owner_write": round(med[(C_sc, 1)] / med[(C_used, 0)], 4),
+                   "gemm_portion": {k: round(v, 3) for k, v in gp_sc.items()},
+                   "combine": {k: round(v, 3) for k, v in comb_sc.items()} if comb_sc else None}
+
     res = {
         "metric": METRIC,
         "value": round(tflops, 2),
@@ -360,6 +395,7 @@ def main():
         "selector_us": round(sel_us, 3),
         "gemm_portion": {k: round(v, 3) for k, v in gemm_portion.items()},
         "combine": {k: round(v, 3) for k, v in combine.items()} if combine else None,
+        "scatter_mode": scatter,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),

@@ -133,6 +133,16 @@ int moe_select_evaluate(const moe_workload_t* wl, const moe_select_params_t* p,
  * MOE_ERR_HIP / MOE_ERR_INVALID_ARG. */
 int moe_gemm2_default_params(int device, moe_select_params_t* out);
 
+/* The same for a consumer mode (see moe_gemm2_combine_ex): mode 0 gives
+ * what moe_gemm2_default_params gives; mode 1 (atomic scatter, one consumer
+ * task per compute tile) sets the consumer tile to
+ * max(1, tile_m / topk) tokens x tile_n columns, so that W_comm counts
+ * about one task per compute tile, and rho_ref to that mode's calibration
+ * (MOE_GEMM2_RHO_REF_SCATTER="num/den" overrides it).  Returns 0 or
+ * MOE_ERR_HIP / MOE_ERR_INVALID_ARG (also for a mode other than 0 or 1 or
+ * topk <= 0). */
+int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk, moe_select_params_t* out);
+
 /* Bytes of workspace moe_gemm2_combine needs for this workload (flags,
  * counters, the token->rows inverse map and the bf16 staging of Y).
  * Returns 0 for an invalid workload. */
@@ -191,7 +201,35 @@ int moe_gemm2_combine_traced(const void* x_perm, const void* w2, const int32_t* 
                              void* workspace, size_t workspace_bytes, void* stream,
                              uint64_t* trace, size_t trace_bytes);
 
-/* Bytes the trace buffer needs for this workload (0 for an invalid one). */
+/* The stage with a choice of consumer (Method, "System Integration and
+ * Correctness": the paper's consumers write each token's output once; a
+ * scatter of fp32 atomic additions is the other way to combine):
+ *   mode 0  owner-write, exactly as moe_gemm2_combine (deterministic: the
+ *           result does not depend on C or on timing);
+ *   mode 1  atomic scatter: the kernel first zeroes out (each workgroup its
+ *           share, published like the inverse map of mode 0), then a
+ *           consumer task is one published compute tile, whose rows r it
+ *           adds, weighted by gate_w[r], into out[token_ids[r], :] with
+ *           fp32 atomic additions at device scope.  The order of the
+ *           additions varies from run to run, so the result does too, by
+ *           rounding only.  Rows with an out-of-range token id are skipped
+ *           and flagged; the topk bound per token is not checked (every
+ *           in-range row is added).
+ * trace: NULL, or a buffer as for moe_gemm2_combine_traced (in mode 1 the
+ * consumer-task words hold one record per compute tile of the global
+ * sequence).  With num_consumers = -1 the selector runs with
+ * moe_gemm2_default_params_ex(device, mode, topk).  Everything else is as
+ * for moe_gemm2_combine; MOE_ERR_INVALID_ARG for a mode other than 0 or 1. */
+int moe_gemm2_combine_ex(const void* x_perm, const void* w2, const int32_t* expert_offsets,
+                         const int32_t* token_ids, const float* gate_w, float* out,
+                         const moe_workload_t* wl, int32_t num_consumers, int32_t mode,
+                         void* workspace, size_t workspace_bytes, void* stream,
+                         uint64_t* trace, size_t trace_bytes);
+
+/* Bytes the trace buffer needs for this workload (0 for an invalid one):
+ * 4 * max_tiles words for the compute tiles, then 4 words for each of
+ * max(splits * ceil(T/64) * ceil(H/splits/1024), max_tiles) consumer
+ * tasks. */
 size_t moe_gemm2_trace_size(const moe_workload_t* wl);
 
 /* Synchronises stream, then reports the device-side status of the last

@@ -30,8 +30,12 @@ EXPORTED = (
     "moe_select_partition", "moe_select_evaluate", "moe_gemm2_default_params",
     "moe_gemm2_workspace_size", "moe_gemm2_workspace_init", "moe_gemm2_combine",
     "moe_gemm2_combine_traced", "moe_gemm2_trace_size", "moe_gemm2_status",
-    "moe_strerror", "moe_gemm2_abi_version",
+    "moe_strerror", "moe_gemm2_abi_version", "moe_gemm2_default_params_ex",
+    "moe_gemm2_combine_ex",
 )
+
+MODE_OWNER_WRITE = 0
+MODE_ATOMIC_SCATTER = 1
 
 
 class Workload(ctypes.Structure):
@@ -96,6 +100,9 @@ def lib() -> ctypes.CDLL:
             L.moe_select_evaluate.restype = ctypes.c_int
             L.moe_gemm2_default_params.argtypes = [ctypes.c_int, ctypes.POINTER(SelectParams)]
             L.moe_gemm2_default_params.restype = ctypes.c_int
+            L.moe_gemm2_default_params_ex.argtypes = [ctypes.c_int, i32, i32,
+                                                      ctypes.POINTER(SelectParams)]
+            L.moe_gemm2_default_params_ex.restype = ctypes.c_int
             L.moe_gemm2_workspace_size.argtypes = [ctypes.POINTER(Workload)]
             L.moe_gemm2_workspace_size.restype = sz
             L.moe_gemm2_trace_size.argtypes = [ctypes.POINTER(Workload)]
@@ -109,6 +116,10 @@ def lib() -> ctypes.CDLL:
                                                    ctypes.POINTER(Workload), i32, vp, sz, vp,
                                                    vp, sz]
             L.moe_gemm2_combine_traced.restype = ctypes.c_int
+            L.moe_gemm2_combine_ex.argtypes = [vp, vp, vp, vp, vp, vp,
+                                               ctypes.POINTER(Workload), i32, i32, vp, sz,
+                                               vp, vp, sz]
+            L.moe_gemm2_combine_ex.restype = ctypes.c_int
             L.moe_gemm2_status.argtypes = [vp, vp, ctypes.c_int]
             L.moe_gemm2_status.restype = ctypes.c_int
             L.moe_strerror.argtypes = [ctypes.c_int]
@@ -150,9 +161,13 @@ def select_evaluate(wl: Workload, params: SelectParams):
     return r, [buf[i] for i in range(max(r, 0))], den.value
 
 
-def default_params(device: int = 0) -> SelectParams:
+def default_params(device: int = 0, mode: Optional[int] = None, topk: int = 1) -> SelectParams:
+    """moe_gemm2_default_params, or moe_gemm2_default_params_ex for a mode."""
     p = SelectParams()
-    r = lib().moe_gemm2_default_params(device, ctypes.byref(p))
+    if mode is None:
+        r = lib().moe_gemm2_default_params(device, ctypes.byref(p))
+    else:
+        r = lib().moe_gemm2_default_params_ex(device, int(mode), int(topk), ctypes.byref(p))
     if r < 0:
         raise MoeError(r, "moe_gemm2_default_params")
     return p
@@ -194,8 +209,10 @@ class Workspace:
 def combine(x_perm, w2, expert_offsets, token_ids, gate_w, T: int, splits: int = 1,
             topk: Optional[int] = None, counts: Optional[Sequence[int]] = None,
             num_consumers: int = -1, out=None, workspace: Optional[Workspace] = None,
-            stream=None, trace=None):
-    """Run moe_gemm2_combine on torch device tensors.
+            stream=None, trace=None, mode: Optional[int] = None):
+    """Run the stage on torch device tensors: moe_gemm2_combine (or
+    moe_gemm2_combine_traced with a trace buffer) when mode is None,
+    moe_gemm2_combine_ex with that mode otherwise.
 
     x_perm bf16 [rows, I], w2 bf16 [E, I, H], expert_offsets int32 [E+1],
     token_ids int32 [rows], gate_w fp32 [rows]; returns (out [T, H] fp32, C).
@@ -223,7 +240,11 @@ def combine(x_perm, w2, expert_offsets, token_ids, gate_w, T: int, splits: int =
             vp(token_ids.data_ptr()), vp(gate_w.data_ptr()), vp(out.data_ptr()),
             ctypes.byref(wl), int(num_consumers), vp(workspace.ptr),
             ctypes.c_size_t(workspace.nbytes), _stream(stream)]
-    if trace is None:
+    if mode is not None:
+        tp = vp(trace.data_ptr()) if trace is not None else vp(0)
+        tb = trace.numel() * trace.element_size() if trace is not None else 0
+        r = lib().moe_gemm2_combine_ex(*args[:8], int(mode), *args[8:], tp, ctypes.c_size_t(tb))
+    elif trace is None:
         r = lib().moe_gemm2_combine(*args)
     else:
         r = lib().moe_gemm2_combine_traced(*args, vp(trace.data_ptr()),

@@ -89,6 +89,7 @@ struct KArgs {
   u64 cnt_epoch;              // launch counter mod 2^40, << 24 (token counters)
   const uint16_t* zeros;      // 16+ zero bytes (operand chunks past the reduction)
   uint32_t* task_ctr;         // next consumer task (reset by workgroup 0 each launch)
+  int mode;                   // 0 owner-write, 1 fp32 atomic scatter
 };
 
 struct Smem {
@@ -201,12 +202,25 @@ __device__ void load_experts(Smem& sm, const KArgs& a) {
   __syncthreads();
 }
 
-// Rows of each token, for the owner-write combine.  With `publish`, the
-// workgroup's share is published at once (release + its workgroup flag);
-// otherwise the caller publishes it later, with its first split's tiles
-// (one L2 write-back for both).
-__device__ void build_inverse(const KArgs& a, long long rows_dev, bool publish) {
+// What the consumers need before their first task, built by every
+// workgroup for its share: for the owner-write combine, the rows of each
+// token (the inverse map); for the atomic scatter, a zeroed output.  With
+// `publish`, the workgroup's share is published at once (release + its
+// workgroup flag); otherwise the caller publishes it later, with its first
+// split's tiles (one L2 write-back for both).
+__device__ void consumer_prologue(const KArgs& a, long long rows_dev, bool publish) {
   const long long stride = (long long)gridDim.x * kThreads;
+  if (a.mode == 1) {
+    // out as 16-byte words, split into one contiguous range per workgroup
+    const long long words = (long long)a.T * a.H / 4;
+    const long long per = (words + gridDim.x - 1) / gridDim.x;
+    const long long lo = (long long)blockIdx.x * per;
+    const long long hi = min(words, lo + per);
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    for (long long i = lo + threadIdx.x; i < hi; i += kThreads)
+      __builtin_nontemporal_store(z, (f32x4*)a.out + i);
+    rows_dev = 0;   // no inverse map
+  }
   for (long long r = (long long)blockIdx.x * kThreads + threadIdx.x; r < rows_dev; r += stride) {
     const int t = a.token_ids[r];
     if (t < 0 || t >= a.T) {
@@ -403,6 +417,27 @@ __device__ __forceinline__ void mfma_step_loads(f32x16 (&acc)[kNB][kMB], const b
 struct TileInfo {
   int e, r0, rows_valid, n0, cols_valid;
 };
+
+// Tile g of the global sequence (split-major, then expert, m-tile, n-tile).
+__device__ TileInfo decode_tile(const Smem& sm, const KArgs& a, long long W_comp, long long g) {
+  const int s = (int)(g / W_comp);
+  const long long idx = g - (long long)s * W_comp;
+  const int mt = (int)(idx / a.ntps);
+  const int nt = (int)(idx - (long long)mt * a.ntps);
+  // expert owning m-tile mt: last e with tile_prefix[e] <= mt
+  int lo = 0, hi = a.E - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (sm.tile_prefix[mid] <= mt) lo = mid; else hi = mid - 1;
+  }
+  TileInfo ti;
+  ti.e = lo;
+  ti.r0 = sm.start[lo] + (mt - sm.tile_prefix[lo]) * kBM;
+  ti.rows_valid = min(kBM, sm.start[lo] + sm.count[lo] - ti.r0);
+  ti.n0 = s * a.nsplit + nt * kBN;
+  ti.cols_valid = min(kBN, (s + 1) * a.nsplit - ti.n0);
+  return ti;
+}
 
 // This lane's global addresses for its loads of a tile's stages.
 __device__ __forceinline__ TileCtx make_ctx(Smem& sm, const KArgs& a, const TileInfo& ti, int wave) {
@@ -775,6 +810,61 @@ __device__ void consume_task(const KArgs& a, const TaskMeta& m, int t0, int ntok
   }
 }
 
+// ---- consumer role, atomic scatter: one compute tile ---------------------------
+// fp32 add at agent scope, as the hardware's no-return atomic instruction
+// (the output is ordinary device memory of this process, not fine-grained
+// or peer memory, so no compare-and-swap loop is needed).
+__device__ __forceinline__ void atomic_add_f32(float* p, float v) {
+  (void)__builtin_amdgcn_global_atomic_fadd_f32((__attribute__((address_space(1))) float*)p, v);
+}
+
+// out[token_ids[r], n0 + c] += gate_w[r] * Y[r, n0 + c] for every row r and
+// column c of tile ti.  Wave w takes rows w*U .. w*U+U-1, then the next
+// kWaves*U rows; lane l takes columns l, l+64, l+128, l+192, so every load
+// and every atomic instruction of a wave covers one contiguous run of its
+// row.  Rows whose token id is out of range are skipped (and flagged).
+__device__ void scatter_tile(const KArgs& a, const TileInfo& ti) {
+  constexpr int U = 4;
+  constexpr int kCols = kBN / 64;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  bool bad = false;
+  for (int m0 = wave * U; m0 < ti.rows_valid; m0 += kWaves * U) {
+    int tok[U];
+    float g[U];
+    uint16_t y[U][kCols];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int m = m0 + u < ti.rows_valid ? m0 + u : ti.rows_valid - 1;
+      const long long r = (long long)ti.r0 + m;
+      tok[u] = a.token_ids[r];
+      g[u] = m0 + u < ti.rows_valid ? a.gate_w[r] : 0.f;
+      const uint16_t* yr = a.Y + r * a.H + ti.n0;
+#pragma unroll
+      for (int i = 0; i < kCols; ++i) {
+        const int c = lane + 64 * i;
+        y[u][i] = __builtin_nontemporal_load(yr + (c < ti.cols_valid ? c : 0));
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (m0 + u >= ti.rows_valid) continue;
+      if (tok[u] < 0 || tok[u] >= a.T) {
+        bad = true;
+        continue;
+      }
+      float* o = a.out + (long long)tok[u] * a.H + ti.n0;
+#pragma unroll
+      for (int i = 0; i < kCols; ++i) {
+        const int c = lane + 64 * i;
+        if (c < ti.cols_valid) atomic_add_f32(o + c, g[u] * __uint_as_float((uint32_t)y[u][i] << 16));
+      }
+    }
+  }
+  if (bad && lane == 0)
+    __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Serves consumer tasks until none is left.  Tasks are claimed one at a time
 // from a counter, in order (split 0 first), so whichever workgroup is free
 // takes the next one: consumers that finish early, or compute workgroups
@@ -783,8 +873,14 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, long long W_comp) {
   // An acquire invalidates this XCD's L2 (also under the compute workgroups
   // still running there), so there is one per split: the inverse map's
   // flags are acquired together with the first split's, before any read.
+  // overlapping expert ranges (bad offsets, flagged) may need more tiles
+  // than the flag array holds; the compute workgroups then stop at once
+  if (W_comp * a.L > a.max_tiles) return;
   if (!wait_flags(sm, a.wg_flags, gridDim.x, a, W_comp == 0)) return;
-  const int total = a.L * a.tasks_per_split;
+  // owner-write: tasks of kCommTM tokens x comm_tn columns; atomic scatter:
+  // one task per compute tile
+  const int tps = a.mode == 1 ? (int)W_comp : a.tasks_per_split;
+  const int total = a.L * tps;
   u64* trace_tasks = a.trace ? a.trace + 4 * a.max_tiles : nullptr;
   int ready = -1;  // splits [0, ready] are known to be published
   int meta_t0 = -1;  // token block whose metadata is in LDS
@@ -796,27 +892,31 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, long long W_comp) {
     const int task = sm.task;
     __syncthreads();   // sm.task is rewritten by the next claim
     if (task >= total) break;
-    const int s = task / a.tasks_per_split;
-    const int rem = task - s * a.tasks_per_split;
-    const int tb = rem / a.cb_per_split;
-    const int cb = rem - tb * a.cb_per_split;
+    const int s = task / tps;
+    const int rem = task - s * tps;
     const u64 t_wait = now_100mhz();
     if (s > ready) {
       if (W_comp > 0 && !wait_flags(sm, a.tile_flags + (long long)s * W_comp, W_comp, a)) return;
       ready = s;
     }
     const u64 t_go = now_100mhz();
-    const int t0 = tb * kCommTM;
-    const int ntok = min(kCommTM, a.T - t0);
-    const int col0 = s * a.nsplit + cb * a.comm_tn;
-    const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
-    TaskMeta& m = task_meta(sm);
-    if (t0 != meta_t0) {
-      __syncthreads();   // every wave is done with the previous task's metadata
-      load_task_meta(m, a, t0, ntok);
-      meta_t0 = t0;
+    if (a.mode == 1) {
+      scatter_tile(a, decode_tile(sm, a, W_comp, task));
+    } else {
+      const int tb = rem / a.cb_per_split;
+      const int cb = rem - tb * a.cb_per_split;
+      const int t0 = tb * kCommTM;
+      const int ntok = min(kCommTM, a.T - t0);
+      const int col0 = s * a.nsplit + cb * a.comm_tn;
+      const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
+      TaskMeta& m = task_meta(sm);
+      if (t0 != meta_t0) {
+        __syncthreads();   // every wave is done with the previous task's metadata
+        load_task_meta(m, a, t0, ntok);
+        meta_t0 = t0;
+      }
+      consume_task(a, m, t0, ntok, col0, ncols);
     }
-    consume_task(a, m, t0, ntok, col0, ncols);
     if (trace_tasks) {
       __syncthreads();
       if (threadIdx.x == 0) {
@@ -853,25 +953,7 @@ moe_gemm2_fused(KArgs a) {
   // A compute workgroup with a tile in split 0 publishes its share of the
   // inverse map with that split (consumers read it only after a split).
   const bool defer_inverse = b >= a.C && c < W_comp && total <= a.max_tiles;
-  auto decode = [&](long long g) {
-    const int s = (int)(g / W_comp);
-    const long long idx = g - (long long)s * W_comp;
-    const int mt = (int)(idx / a.ntps);
-    const int nt = (int)(idx - (long long)mt * a.ntps);
-    // expert owning m-tile mt: last e with tile_prefix[e] <= mt
-    int lo = 0, hi = a.E - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (sm.tile_prefix[mid] <= mt) lo = mid; else hi = mid - 1;
-    }
-    TileInfo ti;
-    ti.e = lo;
-    ti.r0 = sm.start[lo] + (mt - sm.tile_prefix[lo]) * kBM;
-    ti.rows_valid = min(kBM, sm.start[lo] + sm.count[lo] - ti.r0);
-    ti.n0 = s * a.nsplit + nt * kBN;
-    ti.cols_valid = min(kBN, (s + 1) * a.nsplit - ti.n0);
-    return ti;
-  };
+  auto decode = [&](long long g) { return decode_tile(sm, a, W_comp, g); };
   const int nk = (a.I + kBK - 1) / kBK;
   // A compute workgroup issues its first tile's ring fill before building
   // its share of the inverse map, so those loads fly during its atomics.
@@ -883,7 +965,7 @@ moe_gemm2_fused(KArgs a) {
                    __builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
     filled = true;
   }
-  build_inverse(a, rows_dev, !defer_inverse);
+  consumer_prologue(a, rows_dev, !defer_inverse);
 
   if (b < a.C) {
     consumer_loop(sm, a, W_comp);
@@ -1043,13 +1125,23 @@ int device_info(int dev, DevInfo* out) {
 // MOE_GEMM2_RHO_REF="num/den" overrides it.
 constexpr int64_t kRhoRefNum = 63;
 constexpr int64_t kRhoRefDen = 50;
+// The same ratio for the atomic scatter (one task = one compute tile's
+// rows), measured the same way: 18.6 us / 24.6 us = 0.76.
+constexpr int64_t kRhoScatterNum = 19;
+constexpr int64_t kRhoScatterDen = 25;
 constexpr int kDefaultFixedC = 8;
 
-void fill_params(const DevInfo& d, moe_select_params_t* p) {
+void fill_params(const DevInfo& d, int mode, int topk, moe_select_params_t* p) {
   p->tile_m = kBM;
   p->tile_n = kBN;
   p->comm_tile_m = kCommTM;
   p->comm_tile_n = kCommTN;
+  if (mode == 1) {
+    // a scatter task is one compute tile: kBM routed rows, i.e. about
+    // kBM / topk tokens' worth of rows, by kBN columns
+    p->comm_tile_m = topk > 0 && kBM / topk > 0 ? kBM / topk : 1;
+    p->comm_tile_n = kBN;
+  }
   p->occ_comp = d.occ;
   p->occ_comm = d.occ;
   p->num_cus = d.cus;
@@ -1058,9 +1150,9 @@ void fill_params(const DevInfo& d, moe_select_params_t* p) {
   p->c_min = 0;
   p->c_max = 64;
   p->groups = 1;
-  p->rho_ref_num = kRhoRefNum;
-  p->rho_ref_den = kRhoRefDen;
-  if (const char* s = std::getenv("MOE_GEMM2_RHO_REF")) {
+  p->rho_ref_num = mode == 1 ? kRhoScatterNum : kRhoRefNum;
+  p->rho_ref_den = mode == 1 ? kRhoScatterDen : kRhoRefDen;
+  if (const char* s = std::getenv(mode == 1 ? "MOE_GEMM2_RHO_REF_SCATTER" : "MOE_GEMM2_RHO_REF")) {
     long long n = 0, q = 0;
     if (std::sscanf(s, "%lld/%lld", &n, &q) == 2 && n > 0 && q > 0) {
       p->rho_ref_num = n;
@@ -1077,10 +1169,11 @@ inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
            const int32_t* token_ids, const float* gate_w, float* out, const moe_workload_t* wl,
-           int32_t num_consumers, void* workspace, size_t workspace_bytes, void* stream,
-           uint64_t* trace, size_t trace_bytes) {
+           int32_t num_consumers, int32_t mode, void* workspace, size_t workspace_bytes,
+           void* stream, uint64_t* trace, size_t trace_bytes) {
   int st = check_shape(wl);
   if (st != MOE_OK) return st;
+  if (mode != 0 && mode != 1) return MOE_ERR_INVALID_ARG;
   Layout L;
   if (!make_layout(wl, &L)) return MOE_ERR_INVALID_ARG;
   if (!expert_offsets || !out || (L.rows > 0 && (!x_perm || !token_ids || !gate_w)) || !w2)
@@ -1118,7 +1211,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
       C = kDefaultFixedC;
     } else {
       moe_select_params_t p;
-      fill_params(d, &p);
+      fill_params(d, mode, wl->topk, &p);
       moe_workload_t w = *wl;
       if (w.ranks <= 0) w.ranks = 1;
       moe_partition_t part;
@@ -1177,6 +1270,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.comm_tn = L.comm_tn;
   a.cb_per_split = L.cb_per_split;
   a.tasks_per_split = L.tasks_per_split;
+  a.mode = mode;
   uint64_t ep = g_epoch.fetch_add(1) + 1;
   if ((uint32_t)ep == 0) ep = g_epoch.fetch_add(1) + 1;  // flag value 0 is the cleared state
   a.epoch = (uint32_t)ep;
@@ -1198,7 +1292,10 @@ extern "C" size_t moe_gemm2_workspace_size(const moe_workload_t* wl) {
 extern "C" size_t moe_gemm2_trace_size(const moe_workload_t* wl) {
   Layout L;
   if (!make_layout(wl, &L)) return 0;
-  return (size_t)(4 * L.max_tiles + 4LL * wl->splits * L.tasks_per_split) * 8;
+  // compute tiles, then consumer tasks (owner-write tasks or, for the
+  // atomic scatter, one per compute tile)
+  const long long tasks = (long long)wl->splits * L.tasks_per_split;
+  return (size_t)(4 * L.max_tiles + 4 * (tasks > L.max_tiles ? tasks : L.max_tiles)) * 8;
 }
 
 extern "C" int moe_gemm2_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
@@ -1216,7 +1313,17 @@ extern "C" int moe_gemm2_default_params(int device, moe_select_params_t* out) {
   DevInfo d;
   const int st = device_info(device, &d);
   if (st != MOE_OK) return st;
-  fill_params(d, out);
+  fill_params(d, 0, 0, out);
+  return MOE_OK;
+}
+
+extern "C" int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk,
+                                           moe_select_params_t* out) {
+  if (!out || (mode != 0 && mode != 1) || topk <= 0) return MOE_ERR_INVALID_ARG;
+  DevInfo d;
+  const int st = device_info(device, &d);
+  if (st != MOE_OK) return st;
+  fill_params(d, mode, topk, out);
   return MOE_OK;
 }
 
@@ -1225,8 +1332,8 @@ extern "C" int moe_gemm2_combine(const void* x_perm, const void* w2,
                                  const float* gate_w, float* out, const moe_workload_t* wl,
                                  int32_t num_consumers, void* workspace, size_t workspace_bytes,
                                  void* stream) {
-  return launch(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl, num_consumers, workspace,
-                workspace_bytes, stream, nullptr, 0);
+  return launch(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl, num_consumers, 0,
+                workspace, workspace_bytes, stream, nullptr, 0);
 }
 
 extern "C" int moe_gemm2_combine_traced(const void* x_perm, const void* w2,
@@ -1236,8 +1343,18 @@ extern "C" int moe_gemm2_combine_traced(const void* x_perm, const void* w2,
                                         void* workspace, size_t workspace_bytes, void* stream,
                                         uint64_t* trace, size_t trace_bytes) {
   if (!trace) return MOE_ERR_INVALID_ARG;
-  return launch(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl, num_consumers, workspace,
-                workspace_bytes, stream, trace, trace_bytes);
+  return launch(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl, num_consumers, 0,
+                workspace, workspace_bytes, stream, trace, trace_bytes);
+}
+
+extern "C" int moe_gemm2_combine_ex(const void* x_perm, const void* w2,
+                                    const int32_t* expert_offsets, const int32_t* token_ids,
+                                    const float* gate_w, float* out, const moe_workload_t* wl,
+                                    int32_t num_consumers, int32_t mode, void* workspace,
+                                    size_t workspace_bytes, void* stream, uint64_t* trace,
+                                    size_t trace_bytes) {
+  return launch(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl, num_consumers, mode,
+                workspace, workspace_bytes, stream, trace, trace_bytes);
 }
 
 extern "C" int moe_gemm2_status(void* workspace, void* stream, int clear) {

@@ -16,8 +16,9 @@ def to_device(w, device="cuda"):
 
 
 def run(w, C=-1, dev=None, workspace=None, counts=True, splits=None, trace=None,
-        check_status=True):
-    """Returns (out numpy [T, H], C used, workspace)."""
+        check_status=True, mode=None, out=None):
+    """Returns (out numpy [T, H], C used, workspace).  mode None calls
+    moe_gemm2_combine(_traced), else moe_gemm2_combine_ex with that mode."""
     dev = dev if dev is not None else to_device(w)
     x, w2, off, tid, g = dev
     cnt = w.counts if counts else None
@@ -26,7 +27,8 @@ def run(w, C=-1, dev=None, workspace=None, counts=True, splits=None, trace=None,
                                 rows=int(w.x_perm.shape[0]))
         workspace = B.Workspace(B.workspace_size(wl))
     out, c = B.combine(x, w2, off, tid, g, T=w.T, splits=splits or w.L, topk=w.topk,
-                       counts=cnt, num_consumers=C, workspace=workspace, trace=trace)
+                       counts=cnt, num_consumers=C, workspace=workspace, trace=trace,
+                       mode=mode, out=out)
     torch.cuda.synchronize()
     if check_status:
         st = workspace.status()

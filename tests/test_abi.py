@@ -27,7 +27,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(B.EXPORTED)
-    assert L.moe_gemm2_abi_version() == 100
+    assert L.moe_gemm2_abi_version() == 101
 
 
 def _params(**kw):
@@ -181,6 +181,19 @@ def test_combine_host_validation_without_gpu():
     w3, k3 = B.make_workload(T=256, H=1024, I=512, E=8, topk=2, splits=1,
                              counts=[64] * 7 + [63])         # sums to 511 != 512
     assert call(wlp=w3) == B.MOE_ERR_INVALID_ARG
+    # the mode entry point: same checks, and only modes 0 and 1
+
+    def call_ex(mode, C=-1, wlp=wl, out=A):
+        return L.moe_gemm2_combine_ex(vp(A), vp(A), vp(A), vp(A), vp(A), vp(out),
+                                      ctypes.byref(wlp), C, mode, vp(A), ctypes.c_size_t(need),
+                                      vp(0), vp(0), ctypes.c_size_t(0))
+
+    for mode in (-1, 2, 7):
+        assert call_ex(mode) == B.MOE_ERR_INVALID_ARG, mode
+    for mode in (0, 1):
+        assert call_ex(mode, out=A + 4) == B.MOE_ERR_ALIGNMENT
+        assert call_ex(mode, C=-2) == B.MOE_ERR_INVALID_ARG
+    assert L.moe_gemm2_default_params_ex(0, 2, 1, None) == B.MOE_ERR_INVALID_ARG
     assert L.moe_gemm2_workspace_init(None, 0, None) == B.MOE_ERR_INVALID_ARG
     assert L.moe_gemm2_status(None, None, 0) == B.MOE_ERR_INVALID_ARG
 

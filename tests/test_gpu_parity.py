@@ -131,3 +131,85 @@ def test_no_rows_at_all(gpu_lib):
     w.gate_w = np.zeros(1, dtype=np.float32)
     got, used, _ = gpu_util.run(w, C=2, counts=False)
     assert np.all(got == 0)
+
+
+# ---- the atomic-scatter consumer (moe_gemm2_combine_ex, mode 1) --------------
+# Its additions happen in whatever order the atomics land, so results are
+# compared with the oracle to the same bar, never bitwise.
+
+@pytest.mark.parametrize("name", ["tiny", "granite", "qwen", "dsv2lite"])
+def test_scatter_parity_configs(gpu_lib, name):
+    import gpu_util
+    w, ref = _workload(name)
+    dev = gpu_util.to_device(w)
+    for C in (-1, 0, 5):
+        got, used, _ = gpu_util.run(w, C=C, dev=dev, mode=1)
+        _check(got, ref, f"{name} scatter C={used}")
+
+
+def test_scatter_overwrites_out_and_matches_owner_write(gpu_lib):
+    """The kernel zeroes out itself (a stale output never leaks in), and the
+    two modes agree to the bar on every token, also across repeated
+    launches that alternate modes on one workspace."""
+    import torch
+
+    import gpu_util
+    w, ref = _workload("qwen")
+    dev = gpu_util.to_device(w)
+    ws = None
+    owner = None
+    for i, (mode, C) in enumerate([(0, 8), (1, 8), (1, 0), (0, 0), (1, 31), (0, 31)]):
+        out = torch.full((w.T, w.H), 7.0, dtype=torch.float32, device="cuda")
+        got, used, ws = gpu_util.run(w, C=C, dev=dev, workspace=ws, mode=mode, out=out)
+        assert used == C
+        _check(got, ref, f"qwen mode={mode} C={C}")
+        if mode == 0:
+            if owner is None:
+                owner = got
+            assert np.array_equal(got.view(np.uint32), owner.view(np.uint32)), i
+        else:
+            _check(got, owner, f"scatter vs owner-write C={C}")
+
+
+@pytest.mark.parametrize("case", EDGE, ids=[c[0] for c in EDGE])
+def test_scatter_edge_shapes(gpu_lib, case):
+    import gpu_util
+    name, T, H, I, E, k, L, routing = case
+    w = custom(T=T, H=H, I=I, E=E, topk=k, L=L, routing=routing, seed=11)
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+    for C in (-1, 0, 3):
+        got, used, _ = gpu_util.run(w, C=C, mode=1)
+        _check(got, ref, f"{name} scatter C={used}")
+
+
+def test_scatter_dropped_slots_and_no_rows(gpu_lib):
+    import torch
+
+    import gpu_util
+    rng = np.random.default_rng(4)
+    T, H, I, E, k = 300, 512, 64, 6, 4
+    sel, gates = [], []
+    for t in range(T):
+        n = int(rng.integers(0, k + 1))
+        es = rng.choice([0, 2, 3, 5], size=min(n, 4), replace=False)
+        sel.append(list(es))
+        gates.append(list(rng.random(len(es)).astype(np.float32)))
+    w = explicit(T, H, I, E, sel, gates)
+    w.topk = k
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+    empty = [t for t in range(T) if len(sel[t]) == 0]
+    assert empty
+    for C in (-1, 0, 3):
+        out = torch.full((T, H), -1.0, dtype=torch.float32, device="cuda")
+        got, used, _ = gpu_util.run(w, C=C, mode=1, out=out)
+        _check(got, ref, f"dropped scatter C={used}")
+        assert np.all(got[empty] == 0)
+    # no rows at all: the output is zeroed and nothing waits
+    w0 = explicit(50, 256, 32, 4, [[] for _ in range(50)], [[] for _ in range(50)])
+    w0.topk = 2
+    w0.x_perm = np.zeros((1, 32), dtype=np.uint16)
+    w0.token_ids = np.zeros(1, dtype=np.int32)
+    w0.gate_w = np.zeros(1, dtype=np.float32)
+    out = torch.full((50, 256), 3.0, dtype=torch.float32, device="cuda")
+    got, used, _ = gpu_util.run(w0, C=2, counts=False, mode=1, out=out)
+    assert np.all(got == 0)

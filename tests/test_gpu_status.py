@@ -50,7 +50,9 @@ def test_traced_matches_untraced(gpu_lib):
         assert (t[:, 3] > 0).all(), "every tile publishes"
         assert (np.diff(t, axis=1) >= 0).all(), "tile timestamps ordered"
         n_tasks = w.L * ((w.T + 63) // 64) * ((w.H // w.L + 1023) // 1024)
-        k = tr[len(tr) - 4 * n_tasks:].reshape(-1, 4)
+        rows = w.x_perm.shape[0]
+        max_tiles = w.L * (-(-(w.H // w.L) // 256)) * (-(-rows // 256) + w.E)
+        k = tr[4 * max_tiles:4 * max_tiles + 4 * n_tasks].reshape(-1, 4)
         assert (k[:, 2] > 0).all(), "every consumer task recorded"
         assert (k[:, 1] >= k[:, 0]).all() and (k[:, 2] >= k[:, 1]).all()
         assert (k[:, 3] >= 0).all() and (k[:, 3] < 4096).all()   # block ids
@@ -164,3 +166,48 @@ def test_two_streams_at_once(gpu_lib):
         for w, o, ws, ref, C in zip((wa, wb), outs, wss, refs, Cs):
             assert ws.status() == 0
             _check(o.cpu().numpy(), ref, f"two streams C={C}")
+
+
+def test_scatter_bad_token_ids_flagged_and_skipped(gpu_lib):
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    w = _small(seed=16)
+    rng = np.random.default_rng(2)
+    bad = rng.choice(w.token_ids.size, size=9, replace=False)
+    gate_ref = w.gate_w.copy()
+    gate_ref[bad] = 0.0
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, gate_ref, w.T)
+    w.token_ids = w.token_ids.copy()
+    w.token_ids[bad[:5]] = w.T
+    w.token_ids[bad[5:]] = -1
+    for C in (0, 3):
+        got, used, ws = gpu_util.run(w, C=C, check_status=False, mode=1)
+        assert ws.status(clear=True) == B.MOE_ERR_BAD_ROUTING
+        _check(got, ref, f"scatter bad ids C={used}")
+
+
+def test_scatter_traced_records_every_tile_task(gpu_lib):
+    import torch
+
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    w = _small(seed=17)
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+    wl, _ = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, w.counts)
+    r, part = B.select_partition(wl, B.default_params(0))
+    n_tiles = int(part.W_comp) * w.L
+    for C in (0, 4):
+        trace = torch.zeros(B.trace_size(wl) // 8, dtype=torch.int64, device="cuda")
+        got, used, _ = gpu_util.run(w, C=C, trace=trace, mode=1)
+        _check(got, ref, f"scatter traced C={used}")
+        tr = trace.cpu().numpy().astype(np.int64)
+        rows = w.x_perm.shape[0]
+        max_tiles = w.L * (-(-(w.H // w.L) // 256)) * (-(-rows // 256) + w.E)
+        owner_tasks = w.L * (-(-w.T // 64)) * (-(-(w.H // w.L) // 1024))
+        assert len(tr) == 4 * max_tiles + 4 * max(owner_tasks, max_tiles)
+        t = tr[:4 * n_tiles].reshape(-1, 4)
+        assert (t[:, 3] > 0).all()
+        k = tr[4 * max_tiles:4 * max_tiles + 4 * n_tiles].reshape(-1, 4)
+        assert (k[:, 2] > 0).all(), "every tile scattered once"
+        assert (k[:, 1] >= k[:, 0]).all() and (k[:, 2] >= k[:, 1]).all()
+        assert (tr[4 * max_tiles + 4 * n_tiles:] == 0).all()
