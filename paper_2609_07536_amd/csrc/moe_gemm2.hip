@@ -48,7 +48,11 @@ constexpr int kMaxSplits = 16;
 constexpr int kMaxTopk = 64;
 constexpr int kMaxGrid = 4096;
 
-constexpr size_t kZeroBlock = 128;     // offset of the zero block in the status region
+constexpr size_t kZeroBlock = 128;
+// Y rows are padded by 128 bytes: with a power-of-two pitch (H = 2048: 4 KB)
+// the rows of a tile fall on few memory channels, which cost ~18% of the
+// write bandwidth of row-strided stores in a microbenchmark.
+constexpr int kYPad = 64;     // offset of the zero block in the status region
 constexpr uint32_t kStBadRouting = 1u;
 constexpr uint32_t kStTimeout = 2u;
 
@@ -67,7 +71,7 @@ struct KArgs {
   const int32_t* token_ids;   // [rows]
   const float* gate_w;        // [rows]
   float* out;                 // [T, H]
-  uint16_t* Y;                // [rows, H] bf16 staging
+  uint16_t* Y;                // [rows, ypitch] bf16 staging
   uint32_t* tile_flags;       // [max_tiles]: epoch once tile g is published
   uint32_t* wg_flags;         // [kMaxGrid]: epoch once workgroup b added its inverse-map rows
   u64* tok_cnt;               // [T]: launch-tagged count of each token's rows
@@ -78,6 +82,7 @@ struct KArgs {
   long long max_tiles;        // capacity of tile_flags
   long long spin_limit;
   int T, H, I, E, topk, L;
+  int ypitch;                 // row pitch of Y in elements (H + kYPad)
   int nsplit;                 // columns per split (H / L)
   int ntps;                   // compute n-tiles per split
   int C, P;                   // consumer and compute workgroups
@@ -88,8 +93,13 @@ struct KArgs {
   uint32_t epoch;             // launch epoch (flags: low 32 bits of the launch counter)
   u64 cnt_epoch;              // launch counter mod 2^40, << 24 (token counters)
   const uint16_t* zeros;      // 16+ zero bytes (operand chunks past the reduction)
-  uint32_t* task_ctr;         // next consumer task (reset by workgroup 0 each launch)
+  uint32_t* task_ctr;         // [kMaxSplits]: next consumer task of each split (reset by
+                              // workgroup 0 each launch)
+  u64* split_cnt;             // [kMaxSplits]: launch-tagged count of published tiles
+  uint32_t* split_ready;      // [kMaxSplits]: epoch once every tile of the split is published
   int mode;                   // 0 owner-write, 1 fp32 atomic scatter
+  int interleave;             // role switch: take ready splits' tasks between tiles
+  int spread;                 // ... workgroup c from its (c % spread)-th tile of a split on
 };
 
 struct Smem {
@@ -101,6 +111,7 @@ struct Smem {
   int scan[kThreads];
   int flag;
   int task;                   // consumer task claimed by the workgroup
+  uint32_t probe;             // a split's readiness flag, loaded while a tile computes
 };
 
 // ---- memory-model helpers ----------------------------------------------------
@@ -119,6 +130,16 @@ __device__ __forceinline__ uint32_t epoch_count(u64 v, u64 cnt_epoch) {
 }
 
 __device__ __forceinline__ u64 now_100mhz() { return __builtin_amdgcn_s_memrealtime(); }
+
+// threadIdx.x, opaque to the compiler: per-lane addresses derived from it
+// are then recomputed where used instead of being hoisted out of the tile
+// loop, where the register budget would spill them (and a spill reload's
+// wait would also wait for the ring loads in flight).
+__device__ __forceinline__ int opaque_tid() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
 
 // Wave 0 polls flags[0..n) until every flag equals the epoch (bounded),
 // advancing past the leading run of set flags; then, with `acquire`, the
@@ -241,10 +262,11 @@ __device__ void consumer_prologue(const KArgs& a, long long rows_dev, bool publi
     }
     a.inv[(long long)t * a.topk + slot] = (int32_t)r;
   }
-  // workgroup 0 resets the consumer task counter; every claim comes after
-  // the claimer has seen all workgroups' flags, so after this store
-  if (blockIdx.x == 0 && threadIdx.x == 0)
-    __hip_atomic_store(a.task_ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // workgroup 0 resets the consumer task counters; every claim of split s
+  // comes after the claimer has seen workgroup 0's release (its inverse-map
+  // flag, or its publish of split s), so after these stores
+  if (blockIdx.x == 0 && threadIdx.x < a.L)
+    __hip_atomic_store(&a.task_ctr[threadIdx.x], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (!publish) return;
   // as for a split: per-wave vmcnt(0), barrier, one release by thread 0
   __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));
@@ -306,6 +328,15 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
+// One 4-byte global -> LDS load by the calling lanes: lane L's dword lands
+// at lds_base + 4 L.
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"
+               :
+               : "s"(lds_base), "v"(g)
+               : "memory", "m0");
+}
+
 // One 16-byte-per-lane global -> LDS load: lane L's 16 bytes land at
 // lds_base + 16 L.  Issued as asm so the compiler does not serialise later
 // LDS reads behind it; completion is tracked with explicit vmcnt waits.
@@ -314,6 +345,20 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
                :
                : "s"(lds_base), "v"(g)
                : "memory", "m0");
+}
+
+// Stores issued as asm, like the ring loads: the compiler then does not
+// track them, and so does not wait for them (a wait that, vmcnt being in
+// order, would also wait for the next tile's ring stages issued after
+// them) before it reuses their source registers at the next tile's start.
+// The data registers are read shortly after issue; the s_nop covers the
+// hazard of overwriting them in the next instructions.  Completion is
+// ordered by the explicit vmcnt waits before a publish.
+__device__ __forceinline__ void store16_nt(void* p, u32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off nt\n\ts_nop 1" : : "v"(p), "v"(v) : "memory");
+}
+__device__ __forceinline__ void store8(void* p, u64 v) {
+  asm volatile("global_store_dwordx2 %0, %1, off\n\ts_nop 1" : : "v"(p), "v"(v) : "memory");
 }
 
 template <int N>
@@ -419,11 +464,13 @@ struct TileInfo {
 };
 
 // Tile g of the global sequence (split-major, then expert, m-tile, n-tile).
-__device__ TileInfo decode_tile(const Smem& sm, const KArgs& a, long long W_comp, long long g) {
-  const int s = (int)(g / W_comp);
-  const long long idx = g - (long long)s * W_comp;
-  const int mt = (int)(idx / a.ntps);
-  const int nt = (int)(idx - (long long)mt * a.ntps);
+// Every tile count fits in 32 bits (checked on the host for the worst case
+// of overlapping expert ranges).
+__device__ TileInfo decode_tile(const Smem& sm, const KArgs& a, int W_comp, int g) {
+  const int s = g / W_comp;
+  const int idx = g - s * W_comp;
+  const int mt = idx / a.ntps;
+  const int nt = idx - mt * a.ntps;
   // expert owning m-tile mt: last e with tile_prefix[e] <= mt
   int lo = 0, hi = a.E - 1;
   while (lo < hi) {
@@ -475,13 +522,58 @@ __device__ __forceinline__ void issue_prologue(const KArgs& a, const TileCtx& t,
     if (s < nk) issue_stage(a, t, s, wave);
 }
 
+// A consumer task taken by a compute workgroup between two of its tiles (the
+// role switch, C = 0): when a tile starts, thread 0 reads the published-tile
+// count of the oldest split that may still have tasks; once the reduction
+// loop is done, a task of that split is claimed if the split is complete
+// and every workgroup's inverse-map share is published.  Nothing here
+// waits for another workgroup.
+struct Interleave {
+  bool may;          // a probe was issued for this tile (workgroup-uniform)
+  bool inv_ok;       // every workgroup's inverse-map flag was seen
+  int split;         // the split probed (its readiness flag lands in sm.probe)
+  int W_comp;        // tiles per split
+  int tps;           // consumer tasks per split
+  int task;          // result: claimed task of the split, -1 none, -2 split exhausted
+};
+
+__device__ void interleave_claim(Smem& sm, const KArgs& a, Interleave& il) {
+  if (threadIdx.x < 64) {
+    bool inv = il.inv_ok;
+    if (!inv) {
+      bool all = true;
+      for (int i = opaque_tid(); i < (int)gridDim.x; i += 64)
+        all &= __hip_atomic_load(&a.wg_flags[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               a.epoch;
+      inv = __ballot(!all) == 0;
+    }
+    if (threadIdx.x == 0) {
+      int r = -1;
+      if (inv && sm.probe == a.epoch) {
+        const uint32_t k = __hip_atomic_fetch_add(&a.task_ctr[il.split], 1u, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+        r = k < (uint32_t)il.tps ? (int)k : -2;
+      }
+      sm.task = r;
+      sm.flag = inv;
+    }
+  }
+  __syncthreads();
+  il.task = sm.task;
+  il.inv_ok = sm.flag != 0;
+  __syncthreads();
+}
+
 // Computes tile `ti` and stores it to Y.  Its ring fill was issued already
 // if `filled`; with `next`, the ring fill of tile `nt` is issued from this
 // tile's epilogue (stage 0 before the Y stores, stage 1 after them), so
-// that its loads fly during the stores and the publish.
+// that its loads fly during the stores and the publish, unless a consumer
+// task is claimed after the reduction loop (`il`), which then runs first.
 __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool filled, bool next,
-                             const TileInfo& nt, u64* t_mid) {
-  const int lane = threadIdx.x & 63;
+                             const TileInfo& nt, u64* t_mid, Interleave& il) {
+  // The lane's LDS offsets are recomputed for every tile (a few VALU
+  // operations) rather than kept across the tile loop.
+  const int lane = opaque_tid() & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nk = (a.I + kBK - 1) / kBK;
   const int rows_valid = ti.rows_valid, cols_valid = ti.cols_valid, r0 = ti.r0, n0 = ti.n0;
@@ -573,6 +665,10 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
   // every wave is done with the ring before the next tile's prologue
   block_barrier();
   t_mid[0] = now_100mhz();
+  if (il.may) {
+    interleave_claim(sm, a, il);
+    if (il.task >= 0) next = false;   // the task uses the idle ring's LDS
+  }
 
   // The next tile's stage 0 goes into ring slot 0 now, ahead of this
   // tile's Y stores in the load/store queue; slot 1 carries the epilogue,
@@ -626,7 +722,7 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
       const bf16x8 v =
           *(const __attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((j ^ sw) << 3));
       if (n_ok && m < rows_valid)
-        __builtin_nontemporal_store(v, (bf16x8*)(a.Y + (size_t)(r0 + m) * a.H + n0 + n));
+        store16_nt(a.Y + (size_t)(r0 + m) * a.ypitch + n0 + n, __builtin_bit_cast(u32x4, v));
     }
   }
   if (next && nk > 1) {
@@ -659,7 +755,7 @@ __device__ TaskMeta& task_meta(Smem& sm) { return *reinterpret_cast<TaskMeta*>(&
 
 __device__ void load_task_meta(TaskMeta& m, const KArgs& a, int t0, int ntok) {
   const int K = a.topk;
-  for (int i = threadIdx.x; i < ntok * K; i += kThreads) {
+  for (int i = opaque_tid(); i < ntok * K; i += kThreads) {
     const int t = i / K;
     const int j = i - t * K;
     const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t0 + t]), a.cnt_epoch);
@@ -722,7 +818,7 @@ __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = j0 + u < n[p] ? j0 + u : n[p] - 1;
-      const uint16_t* yr = a.Y + (size_t)__builtin_amdgcn_readlane(rs[p], j) * a.H;
+      const uint16_t* yr = a.Y + (size_t)__builtin_amdgcn_readlane(rs[p], j) * a.ypitch;
 #pragma unroll
       for (int b = 0; b < kColBlocks; ++b)
         v[p][u][b] = __builtin_nontemporal_load((const u32x2*)(yr + col[b]));
@@ -839,7 +935,7 @@ __device__ void scatter_tile(const KArgs& a, const TileInfo& ti) {
       const long long r = (long long)ti.r0 + m;
       tok[u] = a.token_ids[r];
       g[u] = m0 + u < ti.rows_valid ? a.gate_w[r] : 0.f;
-      const uint16_t* yr = a.Y + r * a.H + ti.n0;
+      const uint16_t* yr = a.Y + r * a.ypitch + ti.n0;
 #pragma unroll
       for (int i = 0; i < kCols; ++i) {
         const int c = lane + 64 * i;
@@ -865,66 +961,83 @@ __device__ void scatter_tile(const KArgs& a, const TileInfo& ti) {
     __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Serves consumer tasks until none is left.  Tasks are claimed one at a time
-// from a counter, in order (split 0 first), so whichever workgroup is free
-// takes the next one: consumers that finish early, or compute workgroups
-// with fewer tiles, absorb more of the earlier splits' work.
-__device__ void consumer_loop(Smem& sm, const KArgs& a, long long W_comp) {
+// What a workgroup knows while it serves consumer tasks.
+struct Consumer {
+  int ready;     // splits [0, ready] were acquired by this workgroup
+  int split;     // the first split that may still have unclaimed tasks
+  int meta_t0;   // token block whose metadata is in LDS (-1: none)
+  bool inv_ok;   // every workgroup's inverse-map share is published and acquired
+};
+
+// Task idx of split s (owner-write: token block idx / cb_per_split, column
+// block idx % cb_per_split; atomic scatter: compute tile idx of the split).
+__device__ void run_task(Smem& sm, const KArgs& a, int W_comp, int tps, int s, int idx,
+                         Consumer& cs, u64 t_wait, u64 t_go) {
+  if (a.mode == 1) {
+    scatter_tile(a, decode_tile(sm, a, W_comp, s * W_comp + idx));
+  } else {
+    const int tb = idx / a.cb_per_split;
+    const int cb = idx - tb * a.cb_per_split;
+    const int t0 = tb * kCommTM;
+    const int ntok = min(kCommTM, a.T - t0);
+    const int col0 = s * a.nsplit + cb * a.comm_tn;
+    const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
+    TaskMeta& m = task_meta(sm);
+    if (t0 != cs.meta_t0) {
+      __syncthreads();   // every wave is done with the previous task's metadata
+      load_task_meta(m, a, t0, ntok);
+      cs.meta_t0 = t0;
+    }
+    consume_task(a, m, t0, ntok, col0, ncols);
+  }
+  if (a.trace) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      u64* rec = a.trace + 4 * a.max_tiles + 4 * ((long long)s * tps + idx);
+      rec[0] = t_wait;
+      rec[1] = t_go;
+      rec[2] = now_100mhz();
+      rec[3] = blockIdx.x;
+    }
+  }
+}
+
+// Serves consumer tasks until none is left.  Each split has its own task
+// counter and its tasks are claimed in order, split 0 first, so whichever
+// workgroup is free takes the next one: consumers that finish early, or
+// compute workgroups with fewer tiles, absorb more of the earlier splits'
+// work.
+__device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs) {
+  // overlapping expert ranges (bad offsets, flagged) may need more tiles
+  // than the flag array holds; the compute workgroups then stop at once
+  if ((long long)W_comp * a.L > a.max_tiles) return;
   // An acquire invalidates this XCD's L2 (also under the compute workgroups
   // still running there), so there is one per split: the inverse map's
   // flags are acquired together with the first split's, before any read.
-  // overlapping expert ranges (bad offsets, flagged) may need more tiles
-  // than the flag array holds; the compute workgroups then stop at once
-  if (W_comp * a.L > a.max_tiles) return;
-  if (!wait_flags(sm, a.wg_flags, gridDim.x, a, W_comp == 0)) return;
+  if (!cs.inv_ok) {
+    if (!wait_flags(sm, a.wg_flags, gridDim.x, a, W_comp == 0)) return;
+    cs.inv_ok = true;
+  }
   // owner-write: tasks of kCommTM tokens x comm_tn columns; atomic scatter:
   // one task per compute tile
   const int tps = a.mode == 1 ? (int)W_comp : a.tasks_per_split;
-  const int total = a.L * tps;
-  u64* trace_tasks = a.trace ? a.trace + 4 * a.max_tiles : nullptr;
-  int ready = -1;  // splits [0, ready] are known to be published
-  int meta_t0 = -1;  // token block whose metadata is in LDS
-  while (true) {
-    if (threadIdx.x == 0)
-      sm.task = (int)min(__hip_atomic_fetch_add(a.task_ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
-                         (uint32_t)total);
-    __syncthreads();
-    const int task = sm.task;
-    __syncthreads();   // sm.task is rewritten by the next claim
-    if (task >= total) break;
-    const int s = task / tps;
-    const int rem = task - s * tps;
-    const u64 t_wait = now_100mhz();
-    if (s > ready) {
-      if (W_comp > 0 && !wait_flags(sm, a.tile_flags + (long long)s * W_comp, W_comp, a)) return;
-      ready = s;
-    }
-    const u64 t_go = now_100mhz();
-    if (a.mode == 1) {
-      scatter_tile(a, decode_tile(sm, a, W_comp, task));
-    } else {
-      const int tb = rem / a.cb_per_split;
-      const int cb = rem - tb * a.cb_per_split;
-      const int t0 = tb * kCommTM;
-      const int ntok = min(kCommTM, a.T - t0);
-      const int col0 = s * a.nsplit + cb * a.comm_tn;
-      const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
-      TaskMeta& m = task_meta(sm);
-      if (t0 != meta_t0) {
-        __syncthreads();   // every wave is done with the previous task's metadata
-        load_task_meta(m, a, t0, ntok);
-        meta_t0 = t0;
-      }
-      consume_task(a, m, t0, ntok, col0, ncols);
-    }
-    if (trace_tasks) {
+  for (; cs.split < a.L; ++cs.split) {
+    const int s = cs.split;
+    while (true) {
+      const u64 t_wait = now_100mhz();
+      if (threadIdx.x == 0)
+        sm.task = (int)min(__hip_atomic_fetch_add(&a.task_ctr[s], 1u, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT),
+                           (uint32_t)tps);
       __syncthreads();
-      if (threadIdx.x == 0) {
-        trace_tasks[4 * (long long)task + 0] = t_wait;
-        trace_tasks[4 * (long long)task + 1] = t_go;
-        trace_tasks[4 * (long long)task + 2] = now_100mhz();
-        trace_tasks[4 * (long long)task + 3] = blockIdx.x;
+      const int idx = sm.task;
+      __syncthreads();   // sm.task is rewritten by the next claim
+      if (idx >= tps) break;
+      if (s > cs.ready) {
+        if (W_comp > 0 && !wait_flags(sm, a.tile_flags + (long long)s * W_comp, W_comp, a)) return;
+        cs.ready = s;
       }
+      run_task(sm, a, W_comp, tps, s, idx, cs, t_wait, now_100mhz());
     }
   }
 }
@@ -945,30 +1058,34 @@ moe_gemm2_fused(KArgs a) {
   __shared__ Smem sm;
   load_experts(sm, a);
   const long long rows_dev = a.E > 0 ? (long long)sm.start[a.E - 1] + sm.count[a.E - 1] : 0;
-  const long long m_tiles = sm.tile_prefix[a.E];
-  const long long W_comp = m_tiles * a.ntps;
+  const int m_tiles = sm.tile_prefix[a.E];
+  const int W_comp = m_tiles * a.ntps;
   const int b = blockIdx.x;
   const int c = b < a.C ? 0 : compute_index(b, a.C, (int)gridDim.x);
-  const long long total = W_comp * a.L;
+  const int total = W_comp * a.L;
+  // compute workgroup c takes tiles c, c+P, c+2P, ... (XCD-aware: the
+  // workgroups of consecutive c share an XCD, and so do their tiles)
+  const int g_first = b >= a.C && c < total ? c : -1;
   // A compute workgroup with a tile in split 0 publishes its share of the
   // inverse map with that split (consumers read it only after a split).
-  const bool defer_inverse = b >= a.C && c < W_comp && total <= a.max_tiles;
-  auto decode = [&](long long g) { return decode_tile(sm, a, W_comp, g); };
+  const bool defer_inverse = g_first >= 0 && g_first < W_comp && total <= a.max_tiles;
+  auto decode = [&](int g) { return decode_tile(sm, a, W_comp, g); };
   const int nk = (a.I + kBK - 1) / kBK;
   // A compute workgroup issues its first tile's ring fill before building
   // its share of the inverse map, so those loads fly during its atomics.
   TileInfo cur = {0, 0, 0, 0, 0};
   bool filled = false;
-  if (b >= a.C && total <= a.max_tiles && c < total) {
-    cur = decode(c);
+  if (total <= a.max_tiles && g_first >= 0) {
+    cur = decode(g_first);
     issue_prologue(a, make_ctx(sm, a, cur, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)), nk,
                    __builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
     filled = true;
   }
   consumer_prologue(a, rows_dev, !defer_inverse);
 
+  Consumer cs = {-1, 0, -1, false};
   if (b < a.C) {
-    consumer_loop(sm, a, W_comp);
+    consumer_loop(sm, a, W_comp, cs);
     return;
   }
   if (total > a.max_tiles) {  // cannot happen with sanitized offsets; stay in bounds
@@ -976,13 +1093,38 @@ moe_gemm2_fused(KArgs a) {
       __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return;
   }
-  long long split_first = c;   // this workgroup's first tile of the current split
-  for (long long g = c; g < total; g += a.P) {
-    const bool next = g + a.P < total;
-    const TileInfo nt = next ? decode(g + a.P) : cur;
+  int split_first = g_first;   // this workgroup's first tile of the current split
+  int in_split = 0;            // tiles of the current split done so far
+  // the inverse-map stores are done before the tile loop (once), so that
+  // the compiler has nothing in flight to wait for inside it
+  waitcnt_vm<0>();
+  Interleave il;
+  il.inv_ok = false;
+  il.W_comp = W_comp;
+  il.tps = a.mode == 1 ? (int)W_comp : a.tasks_per_split;
+  il.task = -1;
+  // role switch: workgroup c takes tasks of finished splits from its
+  // (c % spread)-th tile of a split on, so that the workgroups' tasks are
+  // spread over the split instead of all starting when the previous split
+  // completes (the combine then uses the HBM bandwidth the GEMM leaves)
+  const int spread = a.spread > 0 ? a.spread : max(1, W_comp / a.P);
+  const int slot = c % spread;
+  for (int g = g_first; g >= 0;) {
+    const int g_next = g + a.P < total ? g + a.P : -1;
+    const bool next = g_next >= 0;
+    const TileInfo nt = next ? decode(g_next) : cur;
     const u64 t_start = now_100mhz();
     u64 t_mid[2];
-    compute_tile(sm, a, cur, filled, next, nt, t_mid);
+    const int s_cur = g / W_comp;
+    il.may = a.interleave && next && cs.split < s_cur && in_split >= slot;
+    il.split = cs.split;
+    il.task = -1;
+    // the readiness flag is loaded straight into LDS, so that no register
+    // holds it across the reduction loop (whose stage waits cover this
+    // older load as well)
+    if (il.may && threadIdx.x == 0) dma4(&a.split_ready[cs.split], lds_addr(&sm.probe));
+    compute_tile(sm, a, cur, filled, next, nt, t_mid, il);
+    const bool prefetched = next && il.task < 0;
     // Publish once per split: consumers wait for whole splits, so the tiles
     // of a split are published together after this workgroup's last tile of
     // it (an agent-scope release writes back the whole L2; once per tile it
@@ -991,31 +1133,72 @@ moe_gemm2_fused(KArgs a) {
     // tile's stage 1, issued after them, may stay in flight), the barrier
     // orders those waits before thread 0, whose release fence writes back
     // the L2 before it stores the flags.
-    const bool last_of_split = !next || (g + a.P) / W_comp != g / W_comp;
+    const bool last_of_split = !next || g_next / W_comp != g / W_comp;
     if (last_of_split) {
-      wait_stage(next && nk > 1 ? 1 : 0);
+      wait_stage(prefetched && nk > 1 ? 1 : 0);
       __syncthreads();
       if (threadIdx.x == 0) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        for (long long gg = split_first; gg <= g; gg += a.P)
+        for (int gg = split_first; gg <= g; gg += a.P)
           __hip_atomic_store(&a.tile_flags[gg], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (defer_inverse && split_first == c)   // first publish: also the inverse map
+        if (defer_inverse && split_first == g_first)   // first publish: also the inverse map
           __hip_atomic_store(&a.wg_flags[blockIdx.x], a.epoch, __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
+        // the split's count of published tiles (opened for this launch by
+        // an atomic max, as the per-token counters are); the workgroup that
+        // completes it acquires the others' releases and publishes the
+        // split's readiness flag, which a role-switch workgroup can read
+        // with a single load
+        const int sp = g / W_comp;
+        const int n = (g - split_first) / a.P + 1;
+        u64* cnt = &a.split_cnt[sp];
+        __hip_atomic_fetch_max(cnt, a.cnt_epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const u64 old = __hip_atomic_fetch_add(cnt, (u64)n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((long long)epoch_count(old, a.cnt_epoch) + n == W_comp) {
+          __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
+          __hip_atomic_store(&a.split_ready[sp], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
       }
-      split_first = g + a.P;
+      // nothing the compiler tracks stays in flight past the publish: else
+      // it would wait for it (and, in order, for the ring loads issued
+      // since) at the next tile's start, on every tile
+      waitcnt_vm<0>();
+      split_first = g_next;
+      in_split = 0;
+    } else {
+      ++in_split;
     }
     if (a.trace && threadIdx.x == 0) {
-      a.trace[4 * g + 0] = t_start;
-      a.trace[4 * g + 1] = t_mid[0];
-      a.trace[4 * g + 2] = t_mid[1];
-      a.trace[4 * g + 3] = now_100mhz();
+      store8(&a.trace[4 * g + 0], t_start);
+      store8(&a.trace[4 * g + 1], t_mid[0]);
+      store8(&a.trace[4 * g + 2], t_mid[1]);
+      store8(&a.trace[4 * g + 3], now_100mhz());
+    }
+    if (il.may) {
+      if (il.task == -2) {
+        ++cs.split;   // every task of that split is taken
+      } else if (il.task >= 0) {
+        const u64 t_go = now_100mhz();
+        cs.inv_ok = true;
+        if (il.split > cs.ready) {   // the split's tiles and the inverse map
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          cs.ready = il.split;
+        }
+        cs.meta_t0 = -1;   // the tiles overwrote the task metadata
+        run_task(sm, a, W_comp, il.tps, il.split, il.task, cs, t_go, t_go);
+        waitcnt_vm<0>();   // as after a publish
+        __syncthreads();   // the task is done with the LDS before the next ring fill
+      }
     }
     cur = nt;
-    filled = next;
+    filled = prefetched;
+    g = g_next;
   }
   // after its tiles, a workgroup serves consumer tasks
-  if (a.drain) consumer_loop(sm, a, W_comp);
+  if (a.drain) {
+    cs.meta_t0 = -1;
+    consumer_loop(sm, a, W_comp, cs);
+  }
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -1044,6 +1227,11 @@ int check_shape(const moe_workload_t* wl) {
   const long long rows = wl->rows > 0 ? wl->rows : (long long)wl->T * wl->topk;
   if (rows > (long long)INT32_MAX || (long long)wl->T * wl->topk > (long long)INT32_MAX)
     return MOE_ERR_UNSUPPORTED;
+  // tile indices are 32-bit on the device, also for the most tiles that
+  // bad offsets (every expert spanning all rows) could make
+  const long long ntps = (wl->H / wl->splits + kBN - 1) / kBN;
+  if ((long long)wl->E * ((rows + kBM - 1) / kBM + 1) * ntps * wl->splits > (long long)INT32_MAX / 2)
+    return MOE_ERR_UNSUPPORTED;
   return MOE_OK;
 }
 
@@ -1057,9 +1245,11 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->tasks_per_split = ((wl->T + kCommTM - 1) / kCommTM) * L->cb_per_split;
   L->max_tiles = (long long)wl->splits * L->ntps * ((L->rows + kBM - 1) / kBM + wl->E);
   size_t off = 0;
-  L->status = off;   // word 0: status bits; word 16: consumer task counter;
-                     // bytes kZeroBlock..255: zeros, never written
-  off += 256;
+  L->status = off;   // word 0: status bits; bytes kZeroBlock..255: zeros, never
+                     // written; 256..383: per-split published-tile counts;
+                     // 384..447: per-split consumer task counters; 448..511:
+                     // per-split readiness flags
+  off += 512;
   L->wg_flags = off;
   off += (size_t)kMaxGrid * 4;
   L->flags = off;
@@ -1069,7 +1259,7 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->inv = off;
   off = round_up(off + (size_t)wl->T * wl->topk * 4, 256);
   L->Y = off;
-  off = round_up(off + (size_t)L->rows * wl->H * 2, 256);
+  off = round_up(off + (size_t)L->rows * (wl->H + kYPad) * 2, 256);
   L->total = off;
   return true;
 }
@@ -1247,7 +1437,9 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.inv = reinterpret_cast<int32_t*>(ws + L.inv);
   a.status = reinterpret_cast<uint32_t*>(ws + L.status);
   a.zeros = reinterpret_cast<const uint16_t*>(ws + L.status + kZeroBlock);
-  a.task_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 64);
+  a.split_cnt = reinterpret_cast<u64*>(ws + L.status + 256);
+  a.task_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 384);
+  a.split_ready = reinterpret_cast<uint32_t*>(ws + L.status + 448);
   a.trace = reinterpret_cast<u64*>(trace);
   a.rows = L.rows;
   a.max_tiles = L.max_tiles;
@@ -1258,6 +1450,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   }
   a.T = wl->T;
   a.H = wl->H;
+  a.ypitch = wl->H + kYPad;
   a.I = wl->I;
   a.E = wl->E;
   a.topk = wl->topk;
@@ -1271,6 +1464,14 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.cb_per_split = L.cb_per_split;
   a.tasks_per_split = L.tasks_per_split;
   a.mode = mode;
+  // with MOE_GEMM2_INTERLEAVE=1 the role switch takes finished splits'
+  // tasks between tiles; MOE_GEMM2_SPREAD overrides the spread (default:
+  // tiles per split / compute workgroups)
+  a.interleave = 0;
+  a.spread = 0;
+  if (const char* e = std::getenv("MOE_GEMM2_INTERLEAVE"))
+    if (e[0] == '1') a.interleave = drain;
+  if (const char* e = std::getenv("MOE_GEMM2_SPREAD")) a.spread = std::atoi(e) > 0 ? std::atoi(e) : 0;
   uint64_t ep = g_epoch.fetch_add(1) + 1;
   if ((uint32_t)ep == 0) ep = g_epoch.fetch_add(1) + 1;  // flag value 0 is the cleared state
   a.epoch = (uint32_t)ep;
