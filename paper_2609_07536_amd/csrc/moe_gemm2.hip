@@ -95,11 +95,7 @@ struct KArgs {
   const uint16_t* zeros;      // 16+ zero bytes (operand chunks past the reduction)
   uint32_t* task_ctr;         // [kMaxSplits]: next consumer task of each split (reset by
                               // workgroup 0 each launch)
-  u64* split_cnt;             // [kMaxSplits]: launch-tagged count of published tiles
-  uint32_t* split_ready;      // [kMaxSplits]: epoch once every tile of the split is published
   int mode;                   // 0 owner-write, 1 fp32 atomic scatter
-  int interleave;             // role switch: take ready splits' tasks between tiles
-  int spread;                 // ... workgroup c from its (c % spread)-th tile of a split on
 };
 
 struct Smem {
@@ -111,7 +107,6 @@ struct Smem {
   int scan[kThreads];
   int flag;
   int task;                   // consumer task claimed by the workgroup
-  uint32_t probe;             // a split's readiness flag, loaded while a tile computes
 };
 
 // ---- memory-model helpers ----------------------------------------------------
@@ -328,22 +323,13 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-// One 4-byte global -> LDS load by the calling lanes: lane L's dword lands
-// at lds_base + 4 L.
-__device__ __forceinline__ void dma4(const void* g, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"
-               :
-               : "s"(lds_base), "v"(g)
-               : "memory", "m0");
-}
-
 // One 16-byte-per-lane global -> LDS load: lane L's 16 bytes land at
 // lds_base + 16 L.  Issued as asm so the compiler does not serialise later
 // LDS reads behind it; completion is tracked with explicit vmcnt waits.
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
                :
-               : "s"(lds_base), "v"(g)
+               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(g)
                : "memory", "m0");
 }
 
@@ -522,55 +508,12 @@ __device__ __forceinline__ void issue_prologue(const KArgs& a, const TileCtx& t,
     if (s < nk) issue_stage(a, t, s, wave);
 }
 
-// A consumer task taken by a compute workgroup between two of its tiles (the
-// role switch, C = 0): when a tile starts, thread 0 reads the published-tile
-// count of the oldest split that may still have tasks; once the reduction
-// loop is done, a task of that split is claimed if the split is complete
-// and every workgroup's inverse-map share is published.  Nothing here
-// waits for another workgroup.
-struct Interleave {
-  bool may;          // a probe was issued for this tile (workgroup-uniform)
-  bool inv_ok;       // every workgroup's inverse-map flag was seen
-  int split;         // the split probed (its readiness flag lands in sm.probe)
-  int W_comp;        // tiles per split
-  int tps;           // consumer tasks per split
-  int task;          // result: claimed task of the split, -1 none, -2 split exhausted
-};
-
-__device__ void interleave_claim(Smem& sm, const KArgs& a, Interleave& il) {
-  if (threadIdx.x < 64) {
-    bool inv = il.inv_ok;
-    if (!inv) {
-      bool all = true;
-      for (int i = opaque_tid(); i < (int)gridDim.x; i += 64)
-        all &= __hip_atomic_load(&a.wg_flags[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-               a.epoch;
-      inv = __ballot(!all) == 0;
-    }
-    if (threadIdx.x == 0) {
-      int r = -1;
-      if (inv && sm.probe == a.epoch) {
-        const uint32_t k = __hip_atomic_fetch_add(&a.task_ctr[il.split], 1u, __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
-        r = k < (uint32_t)il.tps ? (int)k : -2;
-      }
-      sm.task = r;
-      sm.flag = inv;
-    }
-  }
-  __syncthreads();
-  il.task = sm.task;
-  il.inv_ok = sm.flag != 0;
-  __syncthreads();
-}
-
 // Computes tile `ti` and stores it to Y.  Its ring fill was issued already
 // if `filled`; with `next`, the ring fill of tile `nt` is issued from this
 // tile's epilogue (stage 0 before the Y stores, stage 1 after them), so
-// that its loads fly during the stores and the publish, unless a consumer
-// task is claimed after the reduction loop (`il`), which then runs first.
+// that its loads fly during the stores and the publish.
 __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool filled, bool next,
-                             const TileInfo& nt, u64* t_mid, Interleave& il) {
+                             const TileInfo& nt, u64* t_mid) {
   // The lane's LDS offsets are recomputed for every tile (a few VALU
   // operations) rather than kept across the tile loop.
   const int lane = opaque_tid() & 63;
@@ -665,10 +608,6 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
   // every wave is done with the ring before the next tile's prologue
   block_barrier();
   t_mid[0] = now_100mhz();
-  if (il.may) {
-    interleave_claim(sm, a, il);
-    if (il.task >= 0) next = false;   // the task uses the idle ring's LDS
-  }
 
   // The next tile's stage 0 goes into ring slot 0 now, ahead of this
   // tile's Y stores in the load/store queue; slot 1 carries the epilogue,
@@ -758,6 +697,8 @@ __device__ void load_task_meta(TaskMeta& m, const KArgs& a, int t0, int ntok) {
   for (int i = opaque_tid(); i < ntok * K; i += kThreads) {
     const int t = i / K;
     const int j = i - t * K;
+    // the count and the entry are loaded together (one round trip); an
+    // entry past the count is stale and ignored
     const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t0 + t]), a.cnt_epoch);
     const int n = (int)(have < (uint32_t)K ? have : (uint32_t)K);
     int r = 0;
@@ -1083,122 +1024,67 @@ moe_gemm2_fused(KArgs a) {
   }
   consumer_prologue(a, rows_dev, !defer_inverse);
 
+  if (b >= a.C) {   // compute role
+    if (total > a.max_tiles) {  // cannot happen with sanitized offsets; stay in bounds
+      if (threadIdx.x == 0)
+        __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    int split_first = g_first;   // this workgroup's first tile of the current split
+    // the inverse-map stores are done before the tile loop (once), so that
+    // the compiler has nothing in flight to wait for inside it
+    waitcnt_vm<0>();
+    for (int g = g_first; g >= 0;) {
+      const int g_next = g + a.P < total ? g + a.P : -1;
+      const bool next = g_next >= 0;
+      const TileInfo nt = next ? decode(g_next) : cur;
+      const u64 t_start = now_100mhz();
+      u64 t_mid[2];
+      compute_tile(sm, a, cur, filled, next, nt, t_mid);
+      // Publish once per split: consumers wait for whole splits, so the tiles
+      // of a split are published together after this workgroup's last tile of
+      // it (an agent-scope release writes back the whole L2; once per tile it
+      // cost ~3.6 us per tile).  Every wave waits until its Y stores are
+      // acknowledged by the L2 (vmcnt counts in issue order, so only the next
+      // tile's stage 1, issued after them, may stay in flight), the barrier
+      // orders those waits before thread 0, whose release fence writes back
+      // the L2 before it stores the flags.
+      const bool last_of_split = !next || g_next / W_comp != g / W_comp;
+      if (last_of_split) {
+        wait_stage(next && nk > 1 ? 1 : 0);
+        __syncthreads();
+        if (threadIdx.x == 0) {
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+          for (int gg = split_first; gg <= g; gg += a.P)
+            __hip_atomic_store(&a.tile_flags[gg], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (defer_inverse && split_first == g_first)   // first publish: also the inverse map
+            __hip_atomic_store(&a.wg_flags[blockIdx.x], a.epoch, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+        // nothing the compiler tracks stays in flight past the publish: else
+        // it would wait for it (and, in order, for the ring loads issued
+        // since) at the next tile's start, on every tile
+        waitcnt_vm<0>();
+        split_first = g_next;
+      }
+      if (a.trace && threadIdx.x == 0) {
+        store8(&a.trace[4 * g + 0], t_start);
+        store8(&a.trace[4 * g + 1], t_mid[0]);
+        store8(&a.trace[4 * g + 2], t_mid[1]);
+        store8(&a.trace[4 * g + 3], now_100mhz());
+      }
+      cur = nt;
+      filled = next;
+      g = g_next;
+    }
+    // after its tiles, a compute workgroup serves consumer tasks only with
+    // C = 0 (the role switch)
+    if (!a.drain) return;
+  }
+  // consumers, and role-switch workgroups after their tiles (one call site,
+  // so that the loop is inlined)
   Consumer cs = {-1, 0, -1, false};
-  if (b < a.C) {
-    consumer_loop(sm, a, W_comp, cs);
-    return;
-  }
-  if (total > a.max_tiles) {  // cannot happen with sanitized offsets; stay in bounds
-    if (threadIdx.x == 0)
-      __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return;
-  }
-  int split_first = g_first;   // this workgroup's first tile of the current split
-  int in_split = 0;            // tiles of the current split done so far
-  // the inverse-map stores are done before the tile loop (once), so that
-  // the compiler has nothing in flight to wait for inside it
-  waitcnt_vm<0>();
-  Interleave il;
-  il.inv_ok = false;
-  il.W_comp = W_comp;
-  il.tps = a.mode == 1 ? (int)W_comp : a.tasks_per_split;
-  il.task = -1;
-  // role switch: workgroup c takes tasks of finished splits from its
-  // (c % spread)-th tile of a split on, so that the workgroups' tasks are
-  // spread over the split instead of all starting when the previous split
-  // completes (the combine then uses the HBM bandwidth the GEMM leaves)
-  const int spread = a.spread > 0 ? a.spread : max(1, W_comp / a.P);
-  const int slot = c % spread;
-  for (int g = g_first; g >= 0;) {
-    const int g_next = g + a.P < total ? g + a.P : -1;
-    const bool next = g_next >= 0;
-    const TileInfo nt = next ? decode(g_next) : cur;
-    const u64 t_start = now_100mhz();
-    u64 t_mid[2];
-    const int s_cur = g / W_comp;
-    il.may = a.interleave && next && cs.split < s_cur && in_split >= slot;
-    il.split = cs.split;
-    il.task = -1;
-    // the readiness flag is loaded straight into LDS, so that no register
-    // holds it across the reduction loop (whose stage waits cover this
-    // older load as well)
-    if (il.may && threadIdx.x == 0) dma4(&a.split_ready[cs.split], lds_addr(&sm.probe));
-    compute_tile(sm, a, cur, filled, next, nt, t_mid, il);
-    const bool prefetched = next && il.task < 0;
-    // Publish once per split: consumers wait for whole splits, so the tiles
-    // of a split are published together after this workgroup's last tile of
-    // it (an agent-scope release writes back the whole L2; once per tile it
-    // cost ~3.6 us per tile).  Every wave waits until its Y stores are
-    // acknowledged by the L2 (vmcnt counts in issue order, so only the next
-    // tile's stage 1, issued after them, may stay in flight), the barrier
-    // orders those waits before thread 0, whose release fence writes back
-    // the L2 before it stores the flags.
-    const bool last_of_split = !next || g_next / W_comp != g / W_comp;
-    if (last_of_split) {
-      wait_stage(prefetched && nk > 1 ? 1 : 0);
-      __syncthreads();
-      if (threadIdx.x == 0) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        for (int gg = split_first; gg <= g; gg += a.P)
-          __hip_atomic_store(&a.tile_flags[gg], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (defer_inverse && split_first == g_first)   // first publish: also the inverse map
-          __hip_atomic_store(&a.wg_flags[blockIdx.x], a.epoch, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-        // the split's count of published tiles (opened for this launch by
-        // an atomic max, as the per-token counters are); the workgroup that
-        // completes it acquires the others' releases and publishes the
-        // split's readiness flag, which a role-switch workgroup can read
-        // with a single load
-        const int sp = g / W_comp;
-        const int n = (g - split_first) / a.P + 1;
-        u64* cnt = &a.split_cnt[sp];
-        __hip_atomic_fetch_max(cnt, a.cnt_epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const u64 old = __hip_atomic_fetch_add(cnt, (u64)n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if ((long long)epoch_count(old, a.cnt_epoch) + n == W_comp) {
-          __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
-          __hip_atomic_store(&a.split_ready[sp], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-      }
-      // nothing the compiler tracks stays in flight past the publish: else
-      // it would wait for it (and, in order, for the ring loads issued
-      // since) at the next tile's start, on every tile
-      waitcnt_vm<0>();
-      split_first = g_next;
-      in_split = 0;
-    } else {
-      ++in_split;
-    }
-    if (a.trace && threadIdx.x == 0) {
-      store8(&a.trace[4 * g + 0], t_start);
-      store8(&a.trace[4 * g + 1], t_mid[0]);
-      store8(&a.trace[4 * g + 2], t_mid[1]);
-      store8(&a.trace[4 * g + 3], now_100mhz());
-    }
-    if (il.may) {
-      if (il.task == -2) {
-        ++cs.split;   // every task of that split is taken
-      } else if (il.task >= 0) {
-        const u64 t_go = now_100mhz();
-        cs.inv_ok = true;
-        if (il.split > cs.ready) {   // the split's tiles and the inverse map
-          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-          cs.ready = il.split;
-        }
-        cs.meta_t0 = -1;   // the tiles overwrote the task metadata
-        run_task(sm, a, W_comp, il.tps, il.split, il.task, cs, t_go, t_go);
-        waitcnt_vm<0>();   // as after a publish
-        __syncthreads();   // the task is done with the LDS before the next ring fill
-      }
-    }
-    cur = nt;
-    filled = prefetched;
-    g = g_next;
-  }
-  // after its tiles, a workgroup serves consumer tasks
-  if (a.drain) {
-    cs.meta_t0 = -1;
-    consumer_loop(sm, a, W_comp, cs);
-  }
+  consumer_loop(sm, a, W_comp, cs);
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -1246,9 +1132,7 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->max_tiles = (long long)wl->splits * L->ntps * ((L->rows + kBM - 1) / kBM + wl->E);
   size_t off = 0;
   L->status = off;   // word 0: status bits; bytes kZeroBlock..255: zeros, never
-                     // written; 256..383: per-split published-tile counts;
-                     // 384..447: per-split consumer task counters; 448..511:
-                     // per-split readiness flags
+                     // written; 256..319: per-split consumer task counters
   off += 512;
   L->wg_flags = off;
   off += (size_t)kMaxGrid * 4;
@@ -1257,7 +1141,7 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->tok_cnt = off;
   off = round_up(off + (size_t)wl->T * 8, 256);
   L->inv = off;
-  off = round_up(off + (size_t)wl->T * wl->topk * 4, 256);
+  off = round_up(off + (size_t)wl->T * wl->topk * 8, 256);
   L->Y = off;
   off = round_up(off + (size_t)L->rows * (wl->H + kYPad) * 2, 256);
   L->total = off;
@@ -1437,9 +1321,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.inv = reinterpret_cast<int32_t*>(ws + L.inv);
   a.status = reinterpret_cast<uint32_t*>(ws + L.status);
   a.zeros = reinterpret_cast<const uint16_t*>(ws + L.status + kZeroBlock);
-  a.split_cnt = reinterpret_cast<u64*>(ws + L.status + 256);
-  a.task_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 384);
-  a.split_ready = reinterpret_cast<uint32_t*>(ws + L.status + 448);
+  a.task_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 256);
   a.trace = reinterpret_cast<u64*>(trace);
   a.rows = L.rows;
   a.max_tiles = L.max_tiles;
@@ -1464,14 +1346,6 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.cb_per_split = L.cb_per_split;
   a.tasks_per_split = L.tasks_per_split;
   a.mode = mode;
-  // with MOE_GEMM2_INTERLEAVE=1 the role switch takes finished splits'
-  // tasks between tiles; MOE_GEMM2_SPREAD overrides the spread (default:
-  // tiles per split / compute workgroups)
-  a.interleave = 0;
-  a.spread = 0;
-  if (const char* e = std::getenv("MOE_GEMM2_INTERLEAVE"))
-    if (e[0] == '1') a.interleave = drain;
-  if (const char* e = std::getenv("MOE_GEMM2_SPREAD")) a.spread = std::atoi(e) > 0 ? std::atoi(e) : 0;
   uint64_t ep = g_epoch.fetch_add(1) + 1;
   if ((uint32_t)ep == 0) ep = g_epoch.fetch_add(1) + 1;  // flag value 0 is the cleared state
   a.epoch = (uint32_t)ep;

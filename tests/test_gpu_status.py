@@ -212,33 +212,3 @@ def test_scatter_traced_records_every_tile_task(gpu_lib):
         assert (k[:, 1] >= k[:, 0]).all() and (k[:, 2] >= k[:, 1]).all()
         assert (tr[4 * max_tiles + 4 * n_tiles:] == 0).all()
 
-
-@pytest.mark.parametrize("spread", [None, "1", "3"])
-def test_role_switch_interleave_option(gpu_lib, spread):
-    """MOE_GEMM2_INTERLEAVE=1: with C = 0, compute workgroups take consumer
-    tasks of published splits between their tiles.  Same result as the
-    default, to the bar for the scatter mode and bitwise for owner-write."""
-    import gpu_util
-    w = custom(T=3000, H=1024, I=96, E=10, topk=4, L=4, routing=("zipf", 1.0), seed=21)
-    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
-    dev = gpu_util.to_device(w)
-    base, _, ws = gpu_util.run(w, C=0, dev=dev)
-    keys = ("MOE_GEMM2_INTERLEAVE", "MOE_GEMM2_SPREAD")
-    old = {k: os.environ.get(k) for k in keys}
-    os.environ["MOE_GEMM2_INTERLEAVE"] = "1"
-    if spread is not None:
-        os.environ["MOE_GEMM2_SPREAD"] = spread
-    try:
-        for _ in range(3):
-            got, used, ws = gpu_util.run(w, C=0, dev=dev, workspace=ws)
-            assert used == 0
-            assert np.array_equal(got.view(np.uint32), base.view(np.uint32))
-            sc, _, ws = gpu_util.run(w, C=0, dev=dev, workspace=ws, mode=1)
-            _check(sc, ref, f"interleave scatter spread={spread}")
-    finally:
-        for k, v in old.items():
-            if v is None:
-                os.environ.pop(k, None)
-            else:
-                os.environ[k] = v
-    _check(base, ref, "interleave base")
