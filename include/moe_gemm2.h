@@ -172,7 +172,11 @@ int moe_gemm2_workspace_init(void* workspace, size_t workspace_bytes, void* stre
  *   workspace       device memory of at least moe_gemm2_workspace_size(wl)
  *                   bytes, 256-byte aligned, zeroed once by
  *                   moe_gemm2_workspace_init; calls that may overlap in
- *                   time need distinct workspaces
+ *                   time need distinct workspaces.  The workspace keeps a
+ *                   launch epoch that each launch advances on the device,
+ *                   so a call captured in a HIP graph may be replayed
+ *                   (with wl->host_expert_counts NULL the call reads
+ *                   nothing from the device on the host)
  *   stream          hipStream_t the kernel is enqueued on
  * Supported shapes: H % (8 * splits) == 0, I % 8 == 0, 1 <= E <= 1024,
  * 1 <= topk <= 64, splits <= 16 (else MOE_ERR_UNSUPPORTED).

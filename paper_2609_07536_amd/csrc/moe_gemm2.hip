@@ -40,6 +40,7 @@ constexpr int kBM = 256;                // compute tile rows (routed rows)
 constexpr int kBN = 256;                // compute tile columns (hidden)
 constexpr int kBK = 64;                 // reduction step of one LDS stage
 constexpr int kStages = 2;              // LDS ring depth
+constexpr int kEpSlot = kStages / 2;    // first ring slot the epilogue's C-shuffle uses
 constexpr int kResidentPerCu = 1;       // one workgroup (eight waves, 256 registers each) per CU
 constexpr int kCommTM = 64;             // consumer task: tokens
 constexpr int kCommTN = 1024;           // consumer task: columns (at most)
@@ -90,8 +91,8 @@ struct KArgs {
   int comm_tn;                // consumer task width (<= kCommTN)
   int cb_per_split;           // consumer column blocks per split
   int tasks_per_split;
-  uint32_t epoch;             // launch epoch (flags: low 32 bits of the launch counter)
-  u64 cnt_epoch;              // launch counter mod 2^40, << 24 (token counters)
+  u64* epoch_word;            // the workspace's last completed launch epoch
+  uint32_t* done_ctr;         // workgroups of this launch that have finished
   const uint16_t* zeros;      // 16+ zero bytes (operand chunks past the reduction)
   uint32_t* task_ctr;         // [kMaxSplits]: next consumer task of each split (reset by
                               // workgroup 0 each launch)
@@ -124,6 +125,21 @@ __device__ __forceinline__ uint32_t epoch_count(u64 v, u64 cnt_epoch) {
   return (v & ~kCntMask) == cnt_epoch ? (uint32_t)(v & kCntMask) : 0u;
 }
 
+// The launch's epoch: one more than the workspace's last completed launch,
+// whose last workgroup to finish stored it.  Stream order makes that store
+// visible to the next launch, also when both are replays of one captured
+// graph (whose kernel arguments cannot change), and no workgroup of this
+// launch changes it before every workgroup is done.  Readiness flags hold
+// its low 32 bits (never 0, the cleared state); per-token counters hold it
+// mod 2^40 above a 24-bit count.
+__device__ __forceinline__ u64 launch_epoch(const KArgs& a) {
+  return __hip_atomic_load(a.epoch_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
+}
+__device__ __forceinline__ uint32_t flag_epoch(const KArgs& a) { return (uint32_t)launch_epoch(a); }
+__device__ __forceinline__ u64 count_epoch(const KArgs& a) {
+  return (launch_epoch(a) & ((1ull << (64 - kCntBits)) - 1)) << kCntBits;
+}
+
 __device__ __forceinline__ u64 now_100mhz() { return __builtin_amdgcn_s_memrealtime(); }
 
 // threadIdx.x, opaque to the compiler: per-lane addresses derived from it
@@ -145,14 +161,15 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
                            bool acquire = true) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
+    const uint32_t epoch = flag_epoch(a);
     long long i = 0, spins = 0;
     int ok = 1;
     while (i < n) {
       const long long idx = i + lane;
       const uint32_t v = idx < n ? __hip_atomic_load(&flags[idx], __ATOMIC_RELAXED,
                                                       __HIP_MEMORY_SCOPE_AGENT)
-                                 : a.epoch;
-      const u64 ready = __ballot(v == a.epoch);
+                                 : epoch;
+      const u64 ready = __ballot(v == epoch);
       if (ready == ~0ull) {
         i += 64;
         continue;
@@ -237,6 +254,7 @@ __device__ void consumer_prologue(const KArgs& a, long long rows_dev, bool publi
       __builtin_nontemporal_store(z, (f32x4*)a.out + i);
     rows_dev = 0;   // no inverse map
   }
+  const u64 cnt_epoch = count_epoch(a);
   for (long long r = (long long)blockIdx.x * kThreads + threadIdx.x; r < rows_dev; r += stride) {
     const int t = a.token_ids[r];
     if (t < 0 || t >= a.T) {
@@ -247,10 +265,10 @@ __device__ void consumer_prologue(const KArgs& a, long long rows_dev, bool publi
     // smaller epoch in its high word), then take a slot.  The two atomics
     // of a thread on one address are performed in order, so the add always
     // sees this epoch; no compare-and-swap, no dependent round trip.
-    __hip_atomic_fetch_max(&a.tok_cnt[t], a.cnt_epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_max(&a.tok_cnt[t], cnt_epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const u64 old = __hip_atomic_fetch_add(&a.tok_cnt[t], 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t slot =
-        (old & ~kCntMask) == a.cnt_epoch ? (uint32_t)(old & kCntMask) : 0xffffffffu;
+        (old & ~kCntMask) == cnt_epoch ? (uint32_t)(old & kCntMask) : 0xffffffffu;
     if (slot >= (uint32_t)a.topk) {
       __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       continue;
@@ -268,7 +286,7 @@ __device__ void consumer_prologue(const KArgs& a, long long rows_dev, bool publi
   __syncthreads();
   if (threadIdx.x == 0) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    __hip_atomic_store(&a.wg_flags[blockIdx.x], a.epoch, __ATOMIC_RELAXED,
+    __hip_atomic_store(&a.wg_flags[blockIdx.x], flag_epoch(a), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
   }
 }
@@ -609,14 +627,18 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
   block_barrier();
   t_mid[0] = now_100mhz();
 
-  // The next tile's stage 0 goes into ring slot 0 now, ahead of this
-  // tile's Y stores in the load/store queue; slot 1 carries the epilogue,
-  // and the next tile's stage 1 follows the stores.
-  static_assert(kStages == 2, "the epilogue uses the second ring slot");
-  if (next) issue_stage(a, make_ctx(sm, a, nt, wave), 0, wave);
+  // The next tile's first kEpSlot stages go into their ring slots now,
+  // ahead of this tile's Y stores in the load/store queue; the slots from
+  // kEpSlot on carry the epilogue, and the next tile's later stages follow
+  // the stores.
+  if (next) {
+#pragma unroll
+    for (int st = 0; st < kEpSlot; ++st)
+      if (st < nk) issue_stage(a, make_ctx(sm, a, nt, wave), st, wave);
+  }
 
   // epilogue: the wave's kWM x kWN block goes through LDS in two halves of
-  // 64 rows (8 KB per wave, in slot 1) as bf16 rows of 2 kWN bytes, 16-byte
+  // 64 rows (8 KB per wave, from slot kEpSlot on) as bf16 rows of 2 kWN bytes, 16-byte
   // chunk j of row r at chunk j ^ ((r / r1) % c), c = chunks per row,
   // r1 = rows per 256-byte bank line (so 16 consecutive rows hit 16 distinct
   // bank groups), then leaves as whole rows of 2 kWN bytes (full 128-byte
@@ -626,11 +648,12 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
   constexpr int kEpRowsPerLine = 256 / (2 * kWN);
   constexpr int kEpRowsPerStore = 64 / kEpChunks;
   constexpr int kEpRows = 64;                       // rows per half
-  static_assert(kWaves == 8 && kEpRows * kWN * 2 * 4 == kStageElems * 2, "epilogue halves fill slot 1");
+  static_assert(kWaves == 8 && kEpRows * kWN * 4 <= (kStages - kEpSlot) * kStageElems,
+                "the epilogue halves fit in the ring slots from kEpSlot on");
   const int h = lane >> 5;
   __attribute__((address_space(3))) uint16_t* ep =
-      (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(wave < 4 ? lds_addr(&sm.a[1][0])
-                                                                         : lds_addr(&sm.b[1][0])) +
+      (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(wave < 4 ? lds_addr(&sm.a[kEpSlot][0])
+                                                                         : lds_addr(&sm.b[kEpSlot][0])) +
       (wave & 3) * (kEpRows * kWN);
   const int j = lane % kEpChunks;
   const int n = wn0 + 8 * j;
@@ -664,11 +687,13 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
         store16_nt(a.Y + (size_t)(r0 + m) * a.ypitch + n0 + n, __builtin_bit_cast(u32x4, v));
     }
   }
-  if (next && nk > 1) {
+  if (next && nk > kEpSlot) {
     // every wave has read its block back (its stores carry the data), so
-    // slot 1 may take the next tile's stage 1
+    // the slots from kEpSlot on may take the next tile's later stages
     block_barrier();
-    issue_stage(a, make_ctx(sm, a, nt, wave), 1, wave);
+#pragma unroll
+    for (int st = kEpSlot; st < kStages; ++st)
+      if (st < nk) issue_stage(a, make_ctx(sm, a, nt, wave), st, wave);
   }
   t_mid[1] = now_100mhz();
 }
@@ -694,12 +719,13 @@ __device__ TaskMeta& task_meta(Smem& sm) { return *reinterpret_cast<TaskMeta*>(&
 
 __device__ void load_task_meta(TaskMeta& m, const KArgs& a, int t0, int ntok) {
   const int K = a.topk;
+  const u64 cnt_epoch = count_epoch(a);
   for (int i = opaque_tid(); i < ntok * K; i += kThreads) {
     const int t = i / K;
     const int j = i - t * K;
     // the count and the entry are loaded together (one round trip); an
     // entry past the count is stale and ignored
-    const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t0 + t]), a.cnt_epoch);
+    const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t0 + t]), cnt_epoch);
     const int n = (int)(have < (uint32_t)K ? have : (uint32_t)K);
     int r = 0;
     float g = 0.f;
@@ -994,9 +1020,7 @@ __device__ __forceinline__ int compute_index(int b, int C, int N) {
   return c + below(b, xcd) - below(C, xcd);
 }
 
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-moe_gemm2_fused(KArgs a) {
-  __shared__ Smem sm;
+__device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
   load_experts(sm, a);
   const long long rows_dev = a.E > 0 ? (long long)sm.start[a.E - 1] + sm.count[a.E - 1] : 0;
   const int m_tiles = sm.tile_prefix[a.E];
@@ -1051,14 +1075,16 @@ moe_gemm2_fused(KArgs a) {
       // the L2 before it stores the flags.
       const bool last_of_split = !next || g_next / W_comp != g / W_comp;
       if (last_of_split) {
-        wait_stage(next && nk > 1 ? 1 : 0);
+        // (the stages issued after the stores may stay in flight)
+        wait_stage(next ? max(0, min(kStages, nk) - kEpSlot) : 0);
         __syncthreads();
         if (threadIdx.x == 0) {
           __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+          const uint32_t epoch = flag_epoch(a);
           for (int gg = split_first; gg <= g; gg += a.P)
-            __hip_atomic_store(&a.tile_flags[gg], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&a.tile_flags[gg], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           if (defer_inverse && split_first == g_first)   // first publish: also the inverse map
-            __hip_atomic_store(&a.wg_flags[blockIdx.x], a.epoch, __ATOMIC_RELAXED,
+            __hip_atomic_store(&a.wg_flags[blockIdx.x], epoch, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
         }
         // nothing the compiler tracks stays in flight past the publish: else
@@ -1085,6 +1111,25 @@ moe_gemm2_fused(KArgs a) {
   // so that the loop is inlined)
   Consumer cs = {-1, 0, -1, false};
   consumer_loop(sm, a, W_comp, cs);
+}
+
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+moe_gemm2_fused(KArgs a) {
+  __shared__ Smem sm;
+  fused_body(sm, a);
+  // The last workgroup to finish advances the workspace's launch epoch (and
+  // rearms the counter) for the next launch on this workspace.
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t done = __hip_atomic_fetch_add(a.done_ctr, 1u, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+    if (done == gridDim.x - 1) {
+      u64 e = launch_epoch(a);
+      if ((uint32_t)(e + 1) == 0) ++e;   // the next launch's flags must not be 0
+      __hip_atomic_store(a.done_ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.epoch_word, e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -1132,7 +1177,8 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->max_tiles = (long long)wl->splits * L->ntps * ((L->rows + kBM - 1) / kBM + wl->E);
   size_t off = 0;
   L->status = off;   // word 0: status bits; bytes kZeroBlock..255: zeros, never
-                     // written; 256..319: per-split consumer task counters
+                     // written; 256..319: per-split consumer task counters;
+                     // 320: launch epoch (u64); 328: finished workgroups
   off += 512;
   L->wg_flags = off;
   off += (size_t)kMaxGrid * 4;
@@ -1155,7 +1201,6 @@ struct DevInfo {
 };
 std::mutex g_mu;
 DevInfo g_dev[64];
-std::atomic<uint64_t> g_epoch{0};
 
 int device_info(int dev, DevInfo* out) {
   if (dev < 0 || dev >= 64) return MOE_ERR_INVALID_ARG;
@@ -1346,10 +1391,8 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.cb_per_split = L.cb_per_split;
   a.tasks_per_split = L.tasks_per_split;
   a.mode = mode;
-  uint64_t ep = g_epoch.fetch_add(1) + 1;
-  if ((uint32_t)ep == 0) ep = g_epoch.fetch_add(1) + 1;  // flag value 0 is the cleared state
-  a.epoch = (uint32_t)ep;
-  a.cnt_epoch = (ep & ((1ull << (64 - kCntBits)) - 1)) << kCntBits;
+  a.epoch_word = reinterpret_cast<u64*>(ws + L.status + 320);
+  a.done_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 328);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipLaunchKernelGGL(moe_gemm2_fused, dim3(C + P), dim3(kThreads), 0, s, a);

@@ -212,3 +212,51 @@ def test_scatter_traced_records_every_tile_task(gpu_lib):
         assert (k[:, 1] >= k[:, 0]).all() and (k[:, 2] >= k[:, 1]).all()
         assert (tr[4 * max_tiles + 4 * n_tiles:] == 0).all()
 
+
+
+def test_graph_capture_replays(gpu_lib):
+    """The stage captured in a HIP graph (host counts absent, so the selector
+    uses the even-load estimate and needs nothing from the device) and
+    replayed: every replay equals the eager launch bitwise, with eager
+    launches and synchronisations between replays.  Each launch's epoch
+    comes from the workspace, so replays of the same captured arguments
+    never see the previous replay's flags."""
+    import torch
+
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    w = custom(T=1200, H=1024, I=128, E=12, topk=4, L=2, routing=("zipf", 1.0), seed=31)
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+    x, w2, off, tid, g = gpu_util.to_device(w)
+    wl, _ = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L)
+    B.default_params(0)                       # device facts cached before the capture
+    for mode in (0, 1):
+        ws = B.Workspace(B.workspace_size(wl))
+        out = torch.empty((w.T, w.H), dtype=torch.float32, device="cuda")
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):         # warm-up launch on the capture stream
+            B.combine(x, w2, off, tid, g, T=w.T, splits=w.L, topk=w.topk, out=out,
+                      workspace=ws, stream=side, mode=mode)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        eager = out.cpu().numpy().copy()
+        _check(eager, ref, f"graph eager mode={mode}")
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            B.combine(x, w2, off, tid, g, T=w.T, splits=w.L, topk=w.topk, out=out,
+                      workspace=ws, stream=side, mode=mode)
+        for i in range(4):
+            out.fill_(float("nan"))
+            graph.replay()
+            torch.cuda.synchronize()
+            got = out.cpu().numpy()
+            if mode == 0:
+                assert np.array_equal(got.view(np.uint32), eager.view(np.uint32)), i
+            else:
+                _check(got, ref, f"graph replay {i} scatter")
+            # an eager launch on the same workspace between replays
+            B.combine(x, w2, off, tid, g, T=w.T, splits=w.L, topk=w.topk, out=out,
+                      workspace=ws, mode=mode)
+            torch.cuda.synchronize()
+            assert ws.status() == 0
