@@ -202,11 +202,17 @@ def run_sweep(B, torch, samples, c_max=64):
         best_dom = min(Cs[1:], key=lambda c: med[c])
         pick = B.select_partition(dw.wl, params)[0]
         pick_p = B.select_partition(dw.wl, params_paper)[0]
+        # the selector without the routed counts (even-load estimate), as a
+        # launch that reads nothing back from the device would run it
+        wl_est, _ = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, None)
+        pick_e = B.select_partition(wl_est, params)[0]
         rows.append({
             "workload": name, "T": w.T, "r_expert": round(w.r_expert, 3),
             "best_C": best_all, "best_us": round(med[best_all] * 1e3, 1),
             "pick_C": pick, "pick_us": round(med[pick] * 1e3, 1),
             "regret": round((med[pick] - med[best_all]) / med[best_all], 4),
+            "pick_C_estimate": pick_e, "pick_us_estimate": round(med[pick_e] * 1e3, 1),
+            "regret_estimate": round((med[pick_e] - med[best_all]) / med[best_all], 4),
             "best_C_1_64": best_dom, "best_us_1_64": round(med[best_dom] * 1e3, 1),
             "pick_C_paper_set": pick_p, "pick_us_paper_set": round(med[pick_p] * 1e3, 1),
             "regret_paper_set_vs_best_1_64": round((med[pick_p] - med[best_dom]) / med[best_dom], 4),
@@ -222,6 +228,7 @@ def run_sweep(B, torch, samples, c_max=64):
     return {"workloads": len(rows), "samples_per_C": samples, "C_range": [0, c_max],
             "rho_ref": [params.rho_ref_num, params.rho_ref_den],
             "regret": agg("regret"),
+            "regret_estimate": agg("regret_estimate"),
             "regret_paper_set_vs_best_1_64": agg("regret_paper_set_vs_best_1_64"),
             "per_workload": rows}
 

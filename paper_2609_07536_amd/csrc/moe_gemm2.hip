@@ -108,6 +108,7 @@ struct Smem {
   int scan[kThreads];
   int flag;
   int task;                   // consumer task claimed by the workgroup
+  u64 epoch;                  // this launch's epoch, read once at the start
 };
 
 // ---- memory-model helpers ----------------------------------------------------
@@ -132,12 +133,14 @@ __device__ __forceinline__ uint32_t epoch_count(u64 v, u64 cnt_epoch) {
 // launch changes it before every workgroup is done.  Readiness flags hold
 // its low 32 bits (never 0, the cleared state); per-token counters hold it
 // mod 2^40 above a 24-bit count.
+// The epoch is read once per workgroup at the start, into LDS (a global
+// load later would be waited for together with the ring loads in flight).
 __device__ __forceinline__ u64 launch_epoch(const KArgs& a) {
   return __hip_atomic_load(a.epoch_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
 }
-__device__ __forceinline__ uint32_t flag_epoch(const KArgs& a) { return (uint32_t)launch_epoch(a); }
-__device__ __forceinline__ u64 count_epoch(const KArgs& a) {
-  return (launch_epoch(a) & ((1ull << (64 - kCntBits)) - 1)) << kCntBits;
+__device__ __forceinline__ uint32_t flag_epoch(const Smem& sm) { return (uint32_t)sm.epoch; }
+__device__ __forceinline__ u64 count_epoch(const Smem& sm) {
+  return (sm.epoch & ((1ull << (64 - kCntBits)) - 1)) << kCntBits;
 }
 
 __device__ __forceinline__ u64 now_100mhz() { return __builtin_amdgcn_s_memrealtime(); }
@@ -161,7 +164,7 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
                            bool acquire = true) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
-    const uint32_t epoch = flag_epoch(a);
+    const uint32_t epoch = flag_epoch(sm);
     long long i = 0, spins = 0;
     int ok = 1;
     while (i < n) {
@@ -241,7 +244,7 @@ __device__ void load_experts(Smem& sm, const KArgs& a) {
 // `publish`, the workgroup's share is published at once (release + its
 // workgroup flag); otherwise the caller publishes it later, with its first
 // split's tiles (one L2 write-back for both).
-__device__ void consumer_prologue(const KArgs& a, long long rows_dev, bool publish) {
+__device__ void consumer_prologue(const Smem& sm, const KArgs& a, long long rows_dev, bool publish) {
   const long long stride = (long long)gridDim.x * kThreads;
   if (a.mode == 1) {
     // out as 16-byte words, split into one contiguous range per workgroup
@@ -254,7 +257,7 @@ __device__ void consumer_prologue(const KArgs& a, long long rows_dev, bool publi
       __builtin_nontemporal_store(z, (f32x4*)a.out + i);
     rows_dev = 0;   // no inverse map
   }
-  const u64 cnt_epoch = count_epoch(a);
+  const u64 cnt_epoch = count_epoch(sm);
   for (long long r = (long long)blockIdx.x * kThreads + threadIdx.x; r < rows_dev; r += stride) {
     const int t = a.token_ids[r];
     if (t < 0 || t >= a.T) {
@@ -286,7 +289,7 @@ __device__ void consumer_prologue(const KArgs& a, long long rows_dev, bool publi
   __syncthreads();
   if (threadIdx.x == 0) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    __hip_atomic_store(&a.wg_flags[blockIdx.x], flag_epoch(a), __ATOMIC_RELAXED,
+    __hip_atomic_store(&a.wg_flags[blockIdx.x], flag_epoch(sm), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
   }
 }
@@ -717,9 +720,8 @@ static_assert(sizeof(TaskMeta) <= sizeof(Smem::a) + sizeof(Smem::b) &&
               "task metadata overlays the operand ring");
 __device__ TaskMeta& task_meta(Smem& sm) { return *reinterpret_cast<TaskMeta*>(&sm.a[0][0]); }
 
-__device__ void load_task_meta(TaskMeta& m, const KArgs& a, int t0, int ntok) {
+__device__ void load_task_meta(TaskMeta& m, const KArgs& a, u64 cnt_epoch, int t0, int ntok) {
   const int K = a.topk;
-  const u64 cnt_epoch = count_epoch(a);
   for (int i = opaque_tid(); i < ntok * K; i += kThreads) {
     const int t = i / K;
     const int j = i - t * K;
@@ -952,7 +954,7 @@ __device__ void run_task(Smem& sm, const KArgs& a, int W_comp, int tps, int s, i
     TaskMeta& m = task_meta(sm);
     if (t0 != cs.meta_t0) {
       __syncthreads();   // every wave is done with the previous task's metadata
-      load_task_meta(m, a, t0, ntok);
+      load_task_meta(m, a, count_epoch(sm), t0, ntok);
       cs.meta_t0 = t0;
     }
     consume_task(a, m, t0, ntok, col0, ncols);
@@ -1021,6 +1023,7 @@ __device__ __forceinline__ int compute_index(int b, int C, int N) {
 }
 
 __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
+  if (threadIdx.x == 0) sm.epoch = launch_epoch(a);   // load_experts synchronises
   load_experts(sm, a);
   const long long rows_dev = a.E > 0 ? (long long)sm.start[a.E - 1] + sm.count[a.E - 1] : 0;
   const int m_tiles = sm.tile_prefix[a.E];
@@ -1046,7 +1049,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
                    __builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
     filled = true;
   }
-  consumer_prologue(a, rows_dev, !defer_inverse);
+  consumer_prologue(sm, a, rows_dev, !defer_inverse);
 
   if (b >= a.C) {   // compute role
     if (total > a.max_tiles) {  // cannot happen with sanitized offsets; stay in bounds
@@ -1080,7 +1083,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
         __syncthreads();
         if (threadIdx.x == 0) {
           __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-          const uint32_t epoch = flag_epoch(a);
+          const uint32_t epoch = flag_epoch(sm);
           for (int gg = split_first; gg <= g; gg += a.P)
             __hip_atomic_store(&a.tile_flags[gg], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           if (defer_inverse && split_first == g_first)   // first publish: also the inverse map
@@ -1124,7 +1127,7 @@ moe_gemm2_fused(KArgs a) {
     const uint32_t done = __hip_atomic_fetch_add(a.done_ctr, 1u, __ATOMIC_RELAXED,
                                                  __HIP_MEMORY_SCOPE_AGENT);
     if (done == gridDim.x - 1) {
-      u64 e = launch_epoch(a);
+      u64 e = sm.epoch;
       if ((uint32_t)(e + 1) == 0) ++e;   // the next launch's flags must not be 0
       __hip_atomic_store(a.done_ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(a.epoch_word, e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
