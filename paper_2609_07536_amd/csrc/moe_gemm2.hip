@@ -40,7 +40,6 @@ constexpr int kBM = 256;                // compute tile rows (routed rows)
 constexpr int kBN = 256;                // compute tile columns (hidden)
 constexpr int kBK = 64;                 // reduction step of one LDS stage
 constexpr int kStages = 2;              // LDS ring depth
-constexpr int kEpSlot = kStages / 2;    // first ring slot the epilogue's C-shuffle uses
 constexpr int kResidentPerCu = 1;       // one workgroup (eight waves, 256 registers each) per CU
 constexpr int kCommTM = 64;             // consumer task: tokens
 constexpr int kCommTN = 1024;           // consumer task: columns (at most)
@@ -399,12 +398,12 @@ struct TileCtx {
 };
 
 // Issue load q (q < kLoadsPerOperand) of each operand of reduction stage kt
-// into ring slot kt % kStages.  Every load is issued, so each stage adds
-// exactly kLoadsPerStage to vmcnt; lanes whose chunk lies past the
-// reduction (k >= I) load 16 zero bytes from the workspace instead, which
-// zeroes both operands there.
-__device__ __forceinline__ void issue_load(const KArgs& a, const TileCtx& t, int kt, int wave, int q) {
-  const int slot = kt % kStages;
+// into ring slot `slot`.  Every load is issued, so each stage adds exactly
+// kLoadsPerStage to vmcnt; lanes whose chunk lies past the reduction
+// (k >= I) load 16 zero bytes from the workspace instead, which zeroes both
+// operands there.
+__device__ __forceinline__ void issue_load(const KArgs& a, const TileCtx& t, int kt, int slot,
+                                           int wave, int q) {
   const int k0 = kt * kBK;
   const uint32_t blk = (uint32_t)(slot * kStageElems + (kLoadsPerOperand * wave + q) * 512) * 2;
   const int kx = k0 + t.xk[q];
@@ -413,9 +412,10 @@ __device__ __forceinline__ void issue_load(const KArgs& a, const TileCtx& t, int
   dma16(kw < a.I ? t.wgp[q] + (size_t)kw * a.H : a.zeros, t.lds_b + blk);
 }
 
-__device__ __forceinline__ void issue_stage(const KArgs& a, const TileCtx& t, int kt, int wave) {
+__device__ __forceinline__ void issue_stage(const KArgs& a, const TileCtx& t, int kt, int slot,
+                                            int wave) {
 #pragma unroll
-  for (int q = 0; q < kLoadsPerOperand; ++q) issue_load(a, t, kt, wave, q);
+  for (int q = 0; q < kLoadsPerOperand; ++q) issue_load(a, t, kt, slot, wave, q);
 }
 
 typedef const __attribute__((address_space(3))) uint16_t lds_u16;
@@ -453,14 +453,14 @@ __device__ __forceinline__ void mfma_step(f32x16 (&acc)[kNB][kMB], const bf16x8 
 // issue long enough to starve the matrix core.
 __device__ __forceinline__ void mfma_step_loads(f32x16 (&acc)[kNB][kMB], const bf16x8 (&af)[kNB],
                                                 const bf16x8 (&bm)[kMB], const KArgs& a,
-                                                const TileCtx& t, int kt, int wave, int q0,
-                                                bool on) {
+                                                const TileCtx& t, int kt, int slot, int wave,
+                                                int q0, bool on) {
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
 #pragma unroll
     for (int mb = 0; mb < kMB; ++mb)
       acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[nb], bm[mb], acc[nb][mb], 0, 0, 0);
-    if (on) issue_load(a, t, kt, wave, q0 + nb);
+    if (on) issue_load(a, t, kt, slot, wave, q0 + nb);
   }
 }
 
@@ -522,19 +522,48 @@ __device__ __forceinline__ TileCtx make_ctx(Smem& sm, const KArgs& a, const Tile
   return t;
 }
 
-// The loads of a tile's first min(kStages, nk) stages (its ring fill).
-__device__ __forceinline__ void issue_prologue(const KArgs& a, const TileCtx& t, int nk, int wave) {
+// The loads of a tile's first min(kStages, nk) stages (its ring fill), the
+// tile's stage 0 going into ring slot `base`.
+__device__ __forceinline__ void issue_prologue(const KArgs& a, const TileCtx& t, int nk, int base,
+                                               int wave) {
 #pragma unroll
   for (int s = 0; s < kStages; ++s)
-    if (s < nk) issue_stage(a, t, s, wave);
+    if (s < nk) issue_stage(a, t, s, (base + s) % kStages, wave);
 }
 
-// Computes tile `ti` and stores it to Y.  Its ring fill was issued already
-// if `filled`; with `next`, the ring fill of tile `nt` is issued from this
-// tile's epilogue (stage 0 before the Y stores, stage 1 after them), so
-// that its loads fly during the stores and the publish.
+// The K=16 steps of one stage boundary: the last step of stage kt (MFMAs on
+// fragments read before the boundary) and the other steps of stage kt+1
+// (slot s1), with the loads of stage `ls` of the tile `tl` into slot `lslot`
+// spread over the first kLoadSteps steps.
+__device__ __forceinline__ void boundary_steps(f32x16 (&acc)[kNB][kMB], bf16x8 (&af)[2][kNB],
+                                               bf16x8 (&bm)[2][kMB], const KArgs& a,
+                                               lds_u16* As1, lds_u16* Bs1, const int (&offA)[kNB],
+                                               const int (&offB)[kKS], const TileCtx& tl, int ls,
+                                               int lslot, int wave, bool on) {
+  constexpr int kLoadSteps = kLoadsPerOperand / kNB;   // steps that carry a stage's loads
+  load_frags(As1, Bs1, offA, offB, 0, af[0], bm[0]);
+  __builtin_amdgcn_sched_barrier(0);
+  mfma_step_loads(acc, af[(kKS - 1) & 1], bm[(kKS - 1) & 1], a, tl, ls, lslot, wave, 0, on);
+#pragma unroll
+  for (int ks = 0; ks + 1 < kKS; ++ks) {
+    load_frags(As1, Bs1, offA, offB, ks + 1, af[(ks + 1) & 1], bm[(ks + 1) & 1]);
+    __builtin_amdgcn_sched_barrier(0);
+    if (ks + 1 < kLoadSteps)
+      mfma_step_loads(acc, af[ks & 1], bm[ks & 1], a, tl, ls, lslot, wave, (ks + 1) * kNB, on);
+    else
+      mfma_step(acc, af[ks & 1], bm[ks & 1]);
+  }
+}
+
+// Computes tile `ti` and stores it to Y.  The ring continues across tiles:
+// stage kt of this tile sits in slot (base + kt) % kStages, and the next
+// tile's stages follow this tile's last one.  Its ring fill was issued
+// already if `filled`; with `next`, the next tile `nt` gets its stage 0
+// from this tile's last stage boundary (the slot freed there, while this
+// tile's last stage computes) and its stage 1 after this tile's Y stores
+// (the slot of this tile's last stage, which carries the epilogue).
 __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool filled, bool next,
-                             const TileInfo& nt, u64* t_mid) {
+                             const TileInfo& nt, int base, u64* t_mid) {
   // The lane's LDS offsets are recomputed for every tile (a few VALU
   // operations) rather than kept across the tile loop.
   const int lane = opaque_tid() & 63;
@@ -578,18 +607,19 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
 
   // prologue: fill the ring (unless done during the previous tile's
   // publish), then wait for stage 0 (every wave's share)
-  if (!filled) issue_prologue(a, t, nk, wave);
+  if (!filled) issue_prologue(a, t, nk, base, wave);
   wait_stage(min(kStages - 1, nk - 1));
   block_barrier();
 
   // One flat pipeline over the K=16 steps: the fragments of step g+1 are
   // read while the MFMAs of step g run, also across stage boundaries.  The
   // stage boundary (stage kt+1 landed for every wave, every wave done
-  // reading slot kt) is one barrier, after which slot kt is refilled with
-  // stage kt + kStages.
+  // reading the slot of stage kt) is one barrier, after which that slot is
+  // refilled with stage kt + kStages (of the next tile past the last one).
   bf16x8 af[2][kNB], bm[2][kMB];
-  auto slot_a = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_a + (kt % kStages) * kStageElems * 2); };
-  auto slot_b = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_b + (kt % kStages) * kStageElems * 2); };
+  auto slot_of = [&](int kt) { return (base + kt) % kStages; };
+  auto slot_a = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_a + slot_of(kt) * kStageElems * 2); };
+  auto slot_b = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_b + slot_of(kt) * kStageElems * 2); };
   // Steps are grouped so that the loop starts at a stage boundary (which
   // waits for all LDS reads anyway) and every MFMA group follows the reads
   // of the next step in straight-line code: the compiler's LDS waits before
@@ -602,46 +632,34 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
     mfma_step(acc, af[ks & 1], bm[ks & 1]);
   }
   static_assert(kLoadsPerOperand % kNB == 0 && kLoadsPerOperand / kNB <= kKS, "load spread");
-  constexpr int kLoadSteps = kLoadsPerOperand / kNB;   // steps that carry a stage's loads
-  for (int kt = 0; kt + 1 < nk; ++kt) {
-    // last step of stage kt: stage kt+1 landed for every wave and every wave
-    // is done reading slot kt, which is refilled with stage kt + kStages
-    // during the next kLoadSteps steps
-    wait_stage(min(kStages - 2, nk - 2 - kt));
+  static_assert(kStages == 2, "the boundary loop refills one stage ahead");
+  // boundaries whose freed slot takes a stage of this tile
+  for (int kt = 0; kt + kStages < nk; ++kt) {
+    wait_stage(kStages - 2);
     block_barrier();
-    const bool refill = kt + kStages < nk;
-    load_frags(slot_a(kt + 1), slot_b(kt + 1), offA, offB, 0, af[0], bm[0]);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step_loads(acc, af[(kKS - 1) & 1], bm[(kKS - 1) & 1], a, t, kt + kStages, wave, 0, refill);
-    // the other steps of stage kt+1
-#pragma unroll
-    for (int ks = 0; ks + 1 < kKS; ++ks) {
-      load_frags(slot_a(kt + 1), slot_b(kt + 1), offA, offB, ks + 1, af[(ks + 1) & 1],
-                 bm[(ks + 1) & 1]);
-      __builtin_amdgcn_sched_barrier(0);
-      if (ks + 1 < kLoadSteps)
-        mfma_step_loads(acc, af[ks & 1], bm[ks & 1], a, t, kt + kStages, wave, (ks + 1) * kNB, refill);
-      else
-        mfma_step(acc, af[ks & 1], bm[ks & 1]);
-    }
+    boundary_steps(acc, af, bm, a, slot_a(kt + 1), slot_b(kt + 1), offA, offB, t, kt + kStages,
+                   slot_of(kt), wave, true);
+  }
+  // the last boundary: its freed slot takes the next tile's stage 0
+  if (nk >= 2) {
+    wait_stage(0);
+    block_barrier();
+    const TileCtx tn = make_ctx(sm, a, next ? nt : ti, wave);
+    boundary_steps(acc, af, bm, a, slot_a(nk - 1), slot_b(nk - 1), offA, offB, tn, 0,
+                   slot_of(nk), wave, next);
   }
   mfma_step(acc, af[(kKS - 1) & 1], bm[(kKS - 1) & 1]);
-  // every wave is done with the ring before the next tile's prologue
+  // every wave is done with the slot of the last stage, which carries the
+  // epilogue
   block_barrier();
   t_mid[0] = now_100mhz();
-
-  // The next tile's first kEpSlot stages go into their ring slots now,
-  // ahead of this tile's Y stores in the load/store queue; the slots from
-  // kEpSlot on carry the epilogue, and the next tile's later stages follow
-  // the stores.
-  if (next) {
-#pragma unroll
-    for (int st = 0; st < kEpSlot; ++st)
-      if (st < nk) issue_stage(a, make_ctx(sm, a, nt, wave), st, wave);
-  }
+  const int eslot = slot_of(nk - 1);
+  // with a single stage there was no boundary: the next tile's stage 0 goes
+  // into the other slot now, ahead of the Y stores
+  if (next && nk == 1) issue_stage(a, make_ctx(sm, a, nt, wave), 0, slot_of(nk), wave);
 
   // epilogue: the wave's kWM x kWN block goes through LDS in two halves of
-  // 64 rows (8 KB per wave, from slot kEpSlot on) as bf16 rows of 2 kWN bytes, 16-byte
+  // 64 rows (8 KB per wave, in slot eslot) as bf16 rows of 2 kWN bytes, 16-byte
   // chunk j of row r at chunk j ^ ((r / r1) % c), c = chunks per row,
   // r1 = rows per 256-byte bank line (so 16 consecutive rows hit 16 distinct
   // bank groups), then leaves as whole rows of 2 kWN bytes (full 128-byte
@@ -651,12 +669,12 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
   constexpr int kEpRowsPerLine = 256 / (2 * kWN);
   constexpr int kEpRowsPerStore = 64 / kEpChunks;
   constexpr int kEpRows = 64;                       // rows per half
-  static_assert(kWaves == 8 && kEpRows * kWN * 4 <= (kStages - kEpSlot) * kStageElems,
-                "the epilogue halves fit in the ring slots from kEpSlot on");
+  static_assert(kWaves == 8 && kEpRows * kWN * 4 <= kStageElems,
+                "the epilogue halves of four waves fit in one operand's part of a slot");
   const int h = lane >> 5;
   __attribute__((address_space(3))) uint16_t* ep =
-      (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(wave < 4 ? lds_addr(&sm.a[kEpSlot][0])
-                                                                         : lds_addr(&sm.b[kEpSlot][0])) +
+      (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(wave < 4 ? lds_addr(&sm.a[eslot][0])
+                                                                         : lds_addr(&sm.b[eslot][0])) +
       (wave & 3) * (kEpRows * kWN);
   const int j = lane % kEpChunks;
   const int n = wn0 + 8 * j;
@@ -690,13 +708,11 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
         store16_nt(a.Y + (size_t)(r0 + m) * a.ypitch + n0 + n, __builtin_bit_cast(u32x4, v));
     }
   }
-  if (next && nk > kEpSlot) {
+  if (next && nk >= 2) {
     // every wave has read its block back (its stores carry the data), so
-    // the slots from kEpSlot on may take the next tile's later stages
+    // the slot may take the next tile's stage 1
     block_barrier();
-#pragma unroll
-    for (int st = kEpSlot; st < kStages; ++st)
-      if (st < nk) issue_stage(a, make_ctx(sm, a, nt, wave), st, wave);
+    issue_stage(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
   }
   t_mid[1] = now_100mhz();
 }
@@ -1046,7 +1062,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
   if (total <= a.max_tiles && g_first >= 0) {
     cur = decode(g_first);
     issue_prologue(a, make_ctx(sm, a, cur, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)), nk,
-                   __builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
+                   0, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
     filled = true;
   }
   consumer_prologue(sm, a, rows_dev, !defer_inverse);
@@ -1058,6 +1074,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       return;
     }
     int split_first = g_first;   // this workgroup's first tile of the current split
+    int base = 0;                // ring slot of the current tile's stage 0
     // the inverse-map stores are done before the tile loop (once), so that
     // the compiler has nothing in flight to wait for inside it
     waitcnt_vm<0>();
@@ -1067,7 +1084,8 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       const TileInfo nt = next ? decode(g_next) : cur;
       const u64 t_start = now_100mhz();
       u64 t_mid[2];
-      compute_tile(sm, a, cur, filled, next, nt, t_mid);
+      compute_tile(sm, a, cur, filled, next, nt, base, t_mid);
+      base = (base + nk) % kStages;   // the next tile's stages follow this tile's
       // Publish once per split: consumers wait for whole splits, so the tiles
       // of a split are published together after this workgroup's last tile of
       // it (an agent-scope release writes back the whole L2; once per tile it
@@ -1079,7 +1097,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       const bool last_of_split = !next || g_next / W_comp != g / W_comp;
       if (last_of_split) {
         // (the stages issued after the stores may stay in flight)
-        wait_stage(next ? max(0, min(kStages, nk) - kEpSlot) : 0);
+        wait_stage(next && nk >= 2 ? 1 : 0);
         __syncthreads();
         if (threadIdx.x == 0) {
           __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
