@@ -109,7 +109,7 @@ class DevWorkload:
         used = self.run(C, trace=buf, mode=mode)
         torch.cuda.synchronize()
         tr = buf.cpu().numpy().astype(np.int64)
-        part = B.select_partition(self.wl, B.default_params(0))[1]
+        part = B.select_partition(self.wl, B.launch_params(self.wl, mode or 0))[1]
         n_tiles = int(part.W_comp) * w.L
         ntasks = n_tiles if mode == 1 else int(part.W_comm) * w.L
         # tile records first (room for max_tiles), then the task records
@@ -188,14 +188,15 @@ def run_sweep(B, torch, samples, c_max=64):
     The library's candidate set is 0..64 (C = 0: role switch); the paper's
     legal set is 1..C_max, reported separately."""
     from workloads import sweep_workload, sweep_workloads
-    params = B.default_params(0)
-    params_paper = B.default_params(0)
-    params_paper.c_min = 1
+    base_params = B.default_params(0)
     rows = []
     for name, _ in sweep_workloads():
         w = sweep_workload(name, with_tensors=False)
         log(f"sweep {name}: rows={w.Mtot} r_expert={w.r_expert:.2f}")
         dw = DevWorkload(w, B, torch, synth_tensors=True)
+        params = B.launch_params(dw.wl)        # what a launch with C = -1 uses
+        params_paper = B.launch_params(dw.wl)
+        params_paper.c_min = 1
         Cs = list(range(0, c_max + 1))
         med = time_launches(dw, Cs, samples, torch)
         best_all = min(Cs, key=lambda c: med[c])
@@ -205,9 +206,10 @@ def run_sweep(B, torch, samples, c_max=64):
         # the selector without the routed counts (even-load estimate), as a
         # launch that reads nothing back from the device would run it
         wl_est, _ = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, None)
-        pick_e = B.select_partition(wl_est, params)[0]
+        pick_e = B.select_partition(wl_est, B.launch_params(wl_est))[0]
         rows.append({
             "workload": name, "T": w.T, "r_expert": round(w.r_expert, 3),
+            "task_tokens": params.comm_tile_m,
             "best_C": best_all, "best_us": round(med[best_all] * 1e3, 1),
             "pick_C": pick, "pick_us": round(med[pick] * 1e3, 1),
             "regret": round((med[pick] - med[best_all]) / med[best_all], 4),
@@ -226,7 +228,7 @@ def run_sweep(B, torch, samples, c_max=64):
         return {"mean": round(float(np.mean(v)), 4), "max": round(float(np.max(v)), 4)}
 
     return {"workloads": len(rows), "samples_per_C": samples, "C_range": [0, c_max],
-            "rho_ref": [params.rho_ref_num, params.rho_ref_den],
+            "rho_ref_64_token_task": [base_params.rho_ref_num, base_params.rho_ref_den],
             "regret": agg("regret"),
             "regret_estimate": agg("regret_estimate"),
             "regret_paper_set_vs_best_1_64": agg("regret_paper_set_vs_best_1_64"),
@@ -316,7 +318,7 @@ def main():
     assert st == 0, B.strerror(st)
 
     # selector cost on the host (pure C++, no HIP calls)
-    params = B.default_params(0)
+    params = B.launch_params(dw.wl)
     nsel = 20000
     t0 = time.perf_counter()
     for _ in range(nsel):

@@ -124,9 +124,10 @@ int moe_select_partition(const moe_workload_t* wl, const moe_select_params_t* p,
 int moe_select_evaluate(const moe_workload_t* wl, const moe_select_params_t* p,
                         int64_t* T_num_out, int32_t n, int64_t* T_den_out);
 
-/* Parameters for the fused kernel on a HIP device: its tile shapes, its
- * occupancy from hipOccupancyMaxActiveBlocksPerMultiprocessor (capped by its
- * LDS and register budget), the device's CU count, the candidate set
+/* Parameters for the fused kernel on a HIP device: its tile shapes (the
+ * owner-write consumer task at its full size of 64 tokens x 1024 columns),
+ * its occupancy from hipOccupancyMaxActiveBlocksPerMultiprocessor (capped
+ * by its LDS and register budget), the device's CU count, the candidate set
  * C = 0..64 (C = 0 is the role switch, a legal launch of this kernel) and
  * the MI355X calibration of rho_ref.  Device facts are cached
  * on first use (Method, "System Integration and Correctness").  Returns 0 or
@@ -142,6 +143,20 @@ int moe_gemm2_default_params(int device, moe_select_params_t* out);
  * MOE_ERR_HIP / MOE_ERR_INVALID_ARG (also for a mode other than 0 or 1 or
  * topk <= 0). */
 int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk, moe_select_params_t* out);
+
+/* The parameters a launch of this workload hands to the selector (what
+ * num_consumers = -1 uses).  Mode 0: an owner-write task is TM tokens x
+ * min(1024, H/splits) columns, where TM = 64, halved down to 16 while the
+ * launch would have fewer than 512 tasks (splits * ceil(T/TM) *
+ * ceil(H/splits/1024)), so that a small batch's combine still spreads over
+ * every CU; comm_tile_m = TM and rho_ref, calibrated for 64-token tasks, is
+ * scaled by TM/64 (a task's bytes are proportional to its tokens).  Mode 1:
+ * as moe_gemm2_default_params_ex(device, 1, wl->topk).  Returns 0,
+ * MOE_ERR_INVALID_ARG (null pointer, mode other than 0 or 1, invalid
+ * workload), MOE_ERR_UNSUPPORTED (shape outside moe_gemm2_combine's range)
+ * or MOE_ERR_HIP. */
+int moe_gemm2_launch_params(int device, int32_t mode, const moe_workload_t* wl,
+                            moe_select_params_t* out);
 
 /* Bytes of workspace moe_gemm2_combine needs for this workload (flags,
  * counters, the token->rows inverse map and the bf16 staging of Y).
@@ -167,7 +182,8 @@ int moe_gemm2_workspace_init(void* workspace, size_t workspace_bytes, void* stre
  *                   0: no dedicated consumers, every workgroup computes its
  *                   tiles and then takes consumer tasks;
  *                   -1: chosen by moe_select_partition with
- *                   moe_gemm2_default_params, unless the environment sets
+ *                   moe_gemm2_launch_params(device, 0, wl), unless the
+ *                   environment sets
  *                   MOE_GEMM2_SELECTOR=0, which restores a fixed C = 8
  *   workspace       device memory of at least moe_gemm2_workspace_size(wl)
  *                   bytes, 256-byte aligned, zeroed once by
@@ -197,7 +213,10 @@ int moe_gemm2_combine(const void* x_perm, const void* w2, const int32_t* expert_
  * publish for a workgroup's last tile of a split); then, from word
  * 4 * max_tiles (max_tiles = splits * ceil(H/splits/256) *
  * (ceil(rows/256) + E)), for each consumer task j, words 4j..4j+3 = wait
- * start, wait end, finish, workgroup id.  The arithmetic and the result are
+ * start, wait end, finish, workgroup id (task j: split j / tasks_per_split,
+ * token block and column block from j % tasks_per_split, with
+ * tasks_per_split = ceil(T/TM) * ceil(H/splits/1024) and TM the task's
+ * tokens given by moe_gemm2_launch_params).  The arithmetic and the result are
  * identical to the untraced call. */
 int moe_gemm2_combine_traced(const void* x_perm, const void* w2, const int32_t* expert_offsets,
                              const int32_t* token_ids, const float* gate_w, float* out,
@@ -222,7 +241,7 @@ int moe_gemm2_combine_traced(const void* x_perm, const void* w2, const int32_t* 
  * trace: NULL, or a buffer as for moe_gemm2_combine_traced (in mode 1 the
  * consumer-task words hold one record per compute tile of the global
  * sequence).  With num_consumers = -1 the selector runs with
- * moe_gemm2_default_params_ex(device, mode, topk).  Everything else is as
+ * moe_gemm2_launch_params(device, mode, wl).  Everything else is as
  * for moe_gemm2_combine; MOE_ERR_INVALID_ARG for a mode other than 0 or 1. */
 int moe_gemm2_combine_ex(const void* x_perm, const void* w2, const int32_t* expert_offsets,
                          const int32_t* token_ids, const float* gate_w, float* out,
@@ -232,8 +251,8 @@ int moe_gemm2_combine_ex(const void* x_perm, const void* w2, const int32_t* expe
 
 /* Bytes the trace buffer needs for this workload (0 for an invalid one):
  * 4 * max_tiles words for the compute tiles, then 4 words for each of
- * max(splits * ceil(T/64) * ceil(H/splits/1024), max_tiles) consumer
- * tasks. */
+ * max(splits * tasks_per_split, max_tiles) consumer tasks (tasks_per_split
+ * as for moe_gemm2_combine_traced). */
 size_t moe_gemm2_trace_size(const moe_workload_t* wl);
 
 /* Synchronises stream, then reports the device-side status of the last
@@ -244,7 +263,7 @@ int moe_gemm2_status(void* workspace, void* stream, int clear);
 /* Static description of an error code. */
 const char* moe_strerror(int status);
 
-/* ABI version of this header (major * 100 + minor). */
+/* ABI version of this header (major * 100 + minor): 102. */
 int moe_gemm2_abi_version(void);
 
 #ifdef __cplusplus

@@ -31,7 +31,7 @@ EXPORTED = (
     "moe_gemm2_workspace_size", "moe_gemm2_workspace_init", "moe_gemm2_combine",
     "moe_gemm2_combine_traced", "moe_gemm2_trace_size", "moe_gemm2_status",
     "moe_strerror", "moe_gemm2_abi_version", "moe_gemm2_default_params_ex",
-    "moe_gemm2_combine_ex",
+    "moe_gemm2_combine_ex", "moe_gemm2_launch_params",
 )
 
 MODE_OWNER_WRITE = 0
@@ -103,6 +103,9 @@ def lib() -> ctypes.CDLL:
             L.moe_gemm2_default_params_ex.argtypes = [ctypes.c_int, i32, i32,
                                                       ctypes.POINTER(SelectParams)]
             L.moe_gemm2_default_params_ex.restype = ctypes.c_int
+            L.moe_gemm2_launch_params.argtypes = [ctypes.c_int, i32, ctypes.POINTER(Workload),
+                                                  ctypes.POINTER(SelectParams)]
+            L.moe_gemm2_launch_params.restype = ctypes.c_int
             L.moe_gemm2_workspace_size.argtypes = [ctypes.POINTER(Workload)]
             L.moe_gemm2_workspace_size.restype = sz
             L.moe_gemm2_trace_size.argtypes = [ctypes.POINTER(Workload)]
@@ -170,6 +173,16 @@ def default_params(device: int = 0, mode: Optional[int] = None, topk: int = 1) -
         r = lib().moe_gemm2_default_params_ex(device, int(mode), int(topk), ctypes.byref(p))
     if r < 0:
         raise MoeError(r, "moe_gemm2_default_params")
+    return p
+
+
+def launch_params(wl: Workload, mode: int = 0, device: int = 0) -> SelectParams:
+    """moe_gemm2_launch_params: the selector parameters a launch of this
+    workload uses (its consumer task size and the matching rho_ref)."""
+    p = SelectParams()
+    r = lib().moe_gemm2_launch_params(device, int(mode), ctypes.byref(wl), ctypes.byref(p))
+    if r < 0:
+        raise MoeError(r, "moe_gemm2_launch_params")
     return p
 
 

@@ -41,7 +41,9 @@ constexpr int kBN = 256;                // compute tile columns (hidden)
 constexpr int kBK = 64;                 // reduction step of one LDS stage
 constexpr int kStages = 2;              // LDS ring depth
 constexpr int kResidentPerCu = 1;       // one workgroup (eight waves, 256 registers each) per CU
-constexpr int kCommTM = 64;             // consumer task: tokens
+constexpr int kCommTM = 64;             // consumer task: tokens (at most; fewer for small batches)
+constexpr int kCommTMMin = 16;          // consumer task: tokens (at least)
+constexpr int kTaskTarget = 512;        // owner-write tasks wanted per launch (two per CU)
 constexpr int kCommTN = 1024;           // consumer task: columns (at most)
 constexpr int kMaxE = 1024;
 constexpr int kMaxSplits = 16;
@@ -87,6 +89,7 @@ struct KArgs {
   int ntps;                   // compute n-tiles per split
   int C, P;                   // consumer and compute workgroups
   int drain;                  // compute workgroups also take consumer tasks
+  int comm_tm;                // consumer task tokens (<= kCommTM)
   int comm_tn;                // consumer task width (<= kCommTN)
   int cb_per_split;           // consumer column blocks per split
   int tasks_per_split;
@@ -963,8 +966,8 @@ __device__ void run_task(Smem& sm, const KArgs& a, int W_comp, int tps, int s, i
   } else {
     const int tb = idx / a.cb_per_split;
     const int cb = idx - tb * a.cb_per_split;
-    const int t0 = tb * kCommTM;
-    const int ntok = min(kCommTM, a.T - t0);
+    const int t0 = tb * a.comm_tm;
+    const int ntok = min(a.comm_tm, a.T - t0);
     const int col0 = s * a.nsplit + cb * a.comm_tn;
     const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
     TaskMeta& m = task_meta(sm);
@@ -1003,7 +1006,7 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
     if (!wait_flags(sm, a.wg_flags, gridDim.x, a, W_comp == 0)) return;
     cs.inv_ok = true;
   }
-  // owner-write: tasks of kCommTM tokens x comm_tn columns; atomic scatter:
+  // owner-write: tasks of comm_tm tokens x comm_tn columns; atomic scatter:
   // one task per compute tile
   const int tps = a.mode == 1 ? (int)W_comp : a.tasks_per_split;
   for (; cs.split < a.L; ++cs.split) {
@@ -1164,7 +1167,7 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
 struct Layout {
   size_t status, wg_flags, flags, tok_cnt, inv, Y, total;
   long long rows, max_tiles;
-  int nsplit, ntps, comm_tn, cb_per_split, tasks_per_split;
+  int nsplit, ntps, comm_tm, comm_tn, cb_per_split, tasks_per_split;
 };
 
 inline size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -1194,7 +1197,16 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->ntps = (L->nsplit + kBN - 1) / kBN;
   L->comm_tn = L->nsplit < kCommTN ? L->nsplit : kCommTN;
   L->cb_per_split = (L->nsplit + L->comm_tn - 1) / L->comm_tn;
-  L->tasks_per_split = ((wl->T + kCommTM - 1) / kCommTM) * L->cb_per_split;
+  // Owner-write tasks of kCommTM tokens, halved (down to kCommTMMin) while
+  // the launch would have fewer than kTaskTarget of them: a small batch's
+  // combine then still spreads over every CU, and the last tasks of the
+  // launch are short.
+  L->comm_tm = kCommTM;
+  while (L->comm_tm > kCommTMMin &&
+         (long long)wl->splits * ((wl->T + L->comm_tm - 1) / L->comm_tm) * L->cb_per_split <
+             kTaskTarget)
+    L->comm_tm /= 2;
+  L->tasks_per_split = ((wl->T + L->comm_tm - 1) / L->comm_tm) * L->cb_per_split;
   L->max_tiles = (long long)wl->splits * L->ntps * ((L->rows + kBM - 1) / kBM + wl->E);
   size_t off = 0;
   L->status = off;   // word 0: status bits; bytes kZeroBlock..255: zeros, never
@@ -1271,10 +1283,13 @@ constexpr int64_t kRhoScatterNum = 109;
 constexpr int64_t kRhoScatterDen = 100;
 constexpr int kDefaultFixedC = 8;
 
-void fill_params(const DevInfo& d, int mode, int topk, moe_select_params_t* p) {
+// Selector parameters of a launch.  comm_tm is the owner-write task's token
+// count; rho_ref, calibrated for kCommTM-token tasks, scales with it (a
+// task's bytes are proportional to its tokens).
+void fill_params(const DevInfo& d, int mode, int topk, int comm_tm, moe_select_params_t* p) {
   p->tile_m = kBM;
   p->tile_n = kBN;
-  p->comm_tile_m = kCommTM;
+  p->comm_tile_m = comm_tm;
   p->comm_tile_n = kCommTN;
   if (mode == 1) {
     // a scatter task is one compute tile: kBM routed rows, i.e. about
@@ -1298,6 +1313,10 @@ void fill_params(const DevInfo& d, int mode, int topk, moe_select_params_t* p) {
       p->rho_ref_num = n;
       p->rho_ref_den = q;
     }
+  }
+  if (mode == 0 && comm_tm != kCommTM) {
+    p->rho_ref_num *= comm_tm;
+    p->rho_ref_den *= kCommTM;
   }
   p->k_ref = 704;
   p->tile_m_ref = kBM;
@@ -1351,7 +1370,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
       C = kDefaultFixedC;
     } else {
       moe_select_params_t p;
-      fill_params(d, mode, wl->topk, &p);
+      fill_params(d, mode, wl->topk, L.comm_tm, &p);
       moe_workload_t w = *wl;
       if (w.ranks <= 0) w.ranks = 1;
       moe_partition_t part;
@@ -1408,6 +1427,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.C = C;
   a.P = P;
   a.drain = drain;
+  a.comm_tm = L.comm_tm;
   a.comm_tn = L.comm_tn;
   a.cb_per_split = L.cb_per_split;
   a.tasks_per_split = L.tasks_per_split;
@@ -1452,7 +1472,7 @@ extern "C" int moe_gemm2_default_params(int device, moe_select_params_t* out) {
   DevInfo d;
   const int st = device_info(device, &d);
   if (st != MOE_OK) return st;
-  fill_params(d, 0, 0, out);
+  fill_params(d, 0, 0, kCommTM, out);
   return MOE_OK;
 }
 
@@ -1462,7 +1482,20 @@ extern "C" int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t top
   DevInfo d;
   const int st = device_info(device, &d);
   if (st != MOE_OK) return st;
-  fill_params(d, mode, topk, out);
+  fill_params(d, mode, topk, kCommTM, out);
+  return MOE_OK;
+}
+
+extern "C" int moe_gemm2_launch_params(int device, int32_t mode, const moe_workload_t* wl,
+                                       moe_select_params_t* out) {
+  if (!out || (mode != 0 && mode != 1)) return MOE_ERR_INVALID_ARG;
+  Layout L;
+  if (!make_layout(wl, &L)) return check_shape(wl) == MOE_ERR_UNSUPPORTED ? MOE_ERR_UNSUPPORTED
+                                                                          : MOE_ERR_INVALID_ARG;
+  DevInfo d;
+  const int st = device_info(device, &d);
+  if (st != MOE_OK) return st;
+  fill_params(d, mode, wl->topk, L.comm_tm, out);
   return MOE_OK;
 }
 

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(B.EXPORTED)
-    assert L.moe_gemm2_abi_version() == 101
+    assert L.moe_gemm2_abi_version() == 102
 
 
 def _params(**kw):
@@ -194,8 +194,42 @@ def test_combine_host_validation_without_gpu():
         assert call_ex(mode, out=A + 4) == B.MOE_ERR_ALIGNMENT
         assert call_ex(mode, C=-2) == B.MOE_ERR_INVALID_ARG
     assert L.moe_gemm2_default_params_ex(0, 2, 1, None) == B.MOE_ERR_INVALID_ARG
+    p = B.SelectParams()
+    assert L.moe_gemm2_launch_params(0, 0, ctypes.byref(wl), None) == B.MOE_ERR_INVALID_ARG
+    for mode in (-1, 2):
+        assert L.moe_gemm2_launch_params(0, mode, ctypes.byref(wl),
+                                         ctypes.byref(p)) == B.MOE_ERR_INVALID_ARG
+    bad, kb = B.make_workload(T=256, H=1020, I=512, E=8, topk=2, splits=1)
+    assert L.moe_gemm2_launch_params(0, 0, ctypes.byref(bad),
+                                     ctypes.byref(p)) == B.MOE_ERR_UNSUPPORTED
     assert L.moe_gemm2_workspace_init(None, 0, None) == B.MOE_ERR_INVALID_ARG
     assert L.moe_gemm2_status(None, None, 0) == B.MOE_ERR_INVALID_ARG
+
+
+def _task_tokens(T, H, L):
+    """The documented owner-write task size: 64 tokens, halved down to 16
+    while the launch would have fewer than 512 tasks."""
+    cb = -(-(H // L) // min(1024, H // L))
+    tm = 64
+    while tm > 16 and L * -(-T // tm) * cb < 512:
+        tm //= 2
+    return tm
+
+
+@pytest.mark.parametrize("T,H,L,tm", [(16384, 2048, 2, 64), (8192, 2048, 2, 32),
+                                      (4096, 1024, 1, 16), (4096, 2048, 2, 16),
+                                      (32768, 2048, 2, 64), (256, 1024, 1, 16),
+                                      (20000, 1024, 1, 32), (1, 64, 1, 16)])
+def test_trace_size_counts_the_adaptive_consumer_tasks(T, H, L, tm):
+    """trace_size holds one record per owner-write task, and the task size
+    follows the documented rule (checked without a device)."""
+    assert _task_tokens(T, H, L) == tm
+    E, k, I = 8, 2, 64
+    wl, _ = B.make_workload(T=T, H=H, I=I, E=E, topk=k, splits=L)
+    rows = T * k
+    max_tiles = L * -(-(H // L) // 256) * (-(-rows // 256) + E)
+    tasks = L * -(-T // tm) * -(-(H // L) // 1024)
+    assert B.trace_size(wl) == 8 * (4 * max_tiles + 4 * max(tasks, max_tiles))
 
 
 def test_workspace_size_grows_with_rows():

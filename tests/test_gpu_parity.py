@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 from oracle import combine as oc
-from workloads import CONFIGS, config, custom, explicit
+from workloads import CONFIGS, config, custom, explicit, sweep_workload, sweep_workloads
 
 pytestmark = pytest.mark.gpu
 
@@ -42,6 +42,24 @@ def test_parity_configs(gpu_lib, name):
     # independent brute force on sampled tokens
     rng = np.random.default_rng(0)
     toks = rng.choice(w.T, size=min(w.T, 48), replace=False)
+    bf = oc.combine_tokens(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T, toks)
+    _check(got[toks], bf, f"{name} sampled")
+
+
+@pytest.mark.parametrize("name", [n for n, _ in sweep_workloads()])
+def test_parity_sweep_workloads(gpu_lib, name):
+    """The selector-sweep configuration (DeepSeek-V2-Lite-like shapes at
+    T = 4096..32768, uniform and Zipf 0.8 / 1.2 loads) at full size, in the
+    launch the benchmark times (the selector's pick), against the full
+    oracle and a brute force on sampled tokens."""
+    import gpu_util
+    w = sweep_workload(name)
+    print(f"sweep {name}: T={w.T} rows={w.Mtot} r_expert={w.r_expert:.2f}", flush=True)
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+    got, C, _ = gpu_util.run(w)
+    _check(got, ref, f"{name} C={C}")
+    rng = np.random.default_rng(1)
+    toks = rng.choice(w.T, size=48, replace=False)
     bf = oc.combine_tokens(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T, toks)
     _check(got[toks], bf, f"{name} sampled")
 

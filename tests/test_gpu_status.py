@@ -43,13 +43,14 @@ def test_traced_matches_untraced(gpu_lib):
         assert used2 == used
         assert np.array_equal(traced.view(np.uint32), plain.view(np.uint32))
         tr = trace.cpu().numpy().astype(np.int64)
-        p = B.default_params(0)
+        p = B.launch_params(wl)
         r, part = B.select_partition(wl, p)
         n_tiles = int(part.W_comp) * w.L
         t = tr[:4 * n_tiles].reshape(-1, 4)
         assert (t[:, 3] > 0).all(), "every tile publishes"
         assert (np.diff(t, axis=1) >= 0).all(), "tile timestamps ordered"
-        n_tasks = w.L * ((w.T + 63) // 64) * ((w.H // w.L + 1023) // 1024)
+        tm = p.comm_tile_m
+        n_tasks = w.L * ((w.T + tm - 1) // tm) * ((w.H // w.L + 1023) // 1024)
         rows = w.x_perm.shape[0]
         max_tiles = w.L * (-(-(w.H // w.L) // 256)) * (-(-rows // 256) + w.E)
         k = tr[4 * max_tiles:4 * max_tiles + 4 * n_tasks].reshape(-1, 4)
@@ -203,7 +204,8 @@ def test_scatter_traced_records_every_tile_task(gpu_lib):
         tr = trace.cpu().numpy().astype(np.int64)
         rows = w.x_perm.shape[0]
         max_tiles = w.L * (-(-(w.H // w.L) // 256)) * (-(-rows // 256) + w.E)
-        owner_tasks = w.L * (-(-w.T // 64)) * (-(-(w.H // w.L) // 1024))
+        tm = B.launch_params(wl).comm_tile_m
+        owner_tasks = w.L * (-(-w.T // tm)) * (-(-(w.H // w.L) // 1024))
         assert len(tr) == 4 * max_tiles + 4 * max(owner_tasks, max_tiles)
         t = tr[:4 * n_tiles].reshape(-1, 4)
         assert (t[:, 3] > 0).all()
