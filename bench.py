@@ -273,6 +273,9 @@ def main():
                     help="print the rho_ref calibration at C=32 (both consumer modes) and exit")
     ap.add_argument("--no-scatter", action="store_true",
                     help="skip the comparison with the atomic-scatter consumer mode")
+    ap.add_argument("--timed-only", action="store_true",
+                    help="only the warm-up and the timed steps (for profiler runs): no cold-cache "
+                         "samples, trace, scatter comparison, sweep or CPU baseline")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 3 device copies of MIB MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -344,6 +347,13 @@ def main():
     tflops = flops / (ms_per_step / 1e3) / 1e12
     achieved = flops / ker_avg_s / 1e12
 
+    if args.timed_only:
+        print(json.dumps({"metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s",
+                          "ms_per_step": round(ms_per_step, 4),
+                          "avg_launch_us": round(ker_avg_s * 1e6, 2),
+                          "us_per_layer": round(float(np.median(ker_ms)) * 1e3, 2),
+                          "kernel_sha": kernel_sha()}), flush=True)
+        return
     # cold-cache latency: 512 MiB scratch write between samples (untimed)
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     cold = []
