@@ -235,6 +235,18 @@ def run_sweep(B, torch, samples, c_max=64):
             "per_workload": rows}
 
 
+def spread(samples_us, reps=2000, seed=0):
+    """Median, p10/p90 and a bootstrap 95% confidence interval of the median."""
+    v = np.asarray(samples_us, dtype=np.float64)
+    rng = np.random.default_rng(seed)
+    meds = np.median(v[rng.integers(0, len(v), size=(reps, len(v)))], axis=1)
+    return {"median": round(float(np.median(v)), 2), "p10": round(float(np.percentile(v, 10)), 2),
+            "p90": round(float(np.percentile(v, 90)), 2),
+            "ci95_median": [round(float(np.percentile(meds, 2.5)), 2),
+                            round(float(np.percentile(meds, 97.5)), 2)],
+            "samples": int(len(v))}
+
+
 def cpu_baseline(w, budget_s=12.0):
     """The oracle as it stands, timed on the host cores on this workload."""
     import threadpoolctl
@@ -409,6 +421,8 @@ def main():
                    "parallelism": "single GPU"},
         "us_per_layer": round(float(np.median(ker_ms)) * 1e3, 2),
         "us_per_layer_cold": round(float(np.median(cold)) * 1e3, 2),
+        "us_per_layer_stats": spread(ker_ms * 1e3),
+        "us_per_layer_cold_stats": spread(np.asarray(cold) * 1e3),
         "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "consumers": C_used,
         "selector_us": round(sel_us, 3),
