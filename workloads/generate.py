@@ -31,7 +31,11 @@ Draw recipe (fixed, so every consumer sees the same bits for a seed):
   * gate weights: the chosen experts' softmax probabilities, renormalised to
     sum to one per token, stored as fp32;
   * rows grouped by expert (expert-major), ascending token id inside an
-    expert; expert_offsets is the exclusive prefix sum of the counts.
+    expert; expert_offsets is the exclusive prefix sum of the counts;
+  * for the whole post-router layer (``layer_inputs``): hidden states
+    ~ N(0, 1) [T, H] and the up-projection weights ~ N(0, 1/H) [E, H, 2I]
+    (columns 0..I-1 the gate projection, I..2I-1 the up projection), each
+    from its own stream, rounded to bf16 the same way.
 """
 from __future__ import annotations
 
@@ -42,6 +46,7 @@ import numpy as np
 
 # Stream ids for default_rng([seed, cfg_id, stream]).
 _S_X, _S_W2, _S_LOGITS, _S_ROUTE = 1, 2, 3, 4
+_S_HIDDEN, _S_W1 = 5, 6
 
 
 @dataclasses.dataclass
@@ -305,3 +310,24 @@ def explicit(T: int, H: int, I: int, E: int, sel: np.ndarray,
                     expert_offsets=offsets,
                     token_ids=tok[order].astype(np.int32),
                     gate_w=gw[order], counts=counts)
+
+
+def layer_inputs(w: Workload):
+    """Hidden states bf16 [T, H] and up-projection weights bf16 [E, H, 2I]
+    (gate columns, then up columns) for workload w, as uint16 bit patterns."""
+    h = _rng(w.seed, _cfg_of(w), _S_HIDDEN).standard_normal((w.T, w.H), dtype=np.float32)
+    hidden = f32_to_bf16_bits(h)
+    del h
+    g = _rng(w.seed, _cfg_of(w), _S_W1).standard_normal((w.E, w.H, 2 * w.I), dtype=np.float32)
+    g *= np.float32(1.0 / np.sqrt(w.H))
+    w1 = f32_to_bf16_bits(g)
+    del g
+    return hidden, w1
+
+
+def _cfg_of(w: Workload) -> int:
+    """The stream id of a workload's configuration (a hash of its name for
+    workloads outside the named configurations)."""
+    if w.name in CONFIGS:
+        return CONFIGS[w.name]["cfg_id"]
+    return 1000 + sum(ord(c) for c in w.name) % 1000
