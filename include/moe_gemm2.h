@@ -255,6 +255,75 @@ int moe_gemm2_combine_ex(const void* x_perm, const void* w2, const int32_t* expe
  * as for moe_gemm2_combine_traced). */
 size_t moe_gemm2_trace_size(const moe_workload_t* wl);
 
+/* ---- The rest of the post-router layer on one GPU: the up-projection.
+ * Paper: Background, "Distributed MoE Execution" (the grouped GEMM1 with
+ * the gate and up projections and the gated activation that feed GEMM2).
+ * It is not what the paper's method changes; it is here so that the whole
+ * layer after the router runs on the device and the down-projection stage's
+ * share of it can be measured.
+ *
+ *   h_r          = hidden[token_ids[r], :]                  (the dispatch gather)
+ *   x_perm[r, c] = silu(h_r . Wg[e(r)][:, c]) * (h_r . Wu[e(r)][:, c]),
+ *   silu(z)      = z / (1 + exp(-z)),   c < I,
+ *
+ * products in bf16 with fp32 accumulation, the activation in fp32, x_perm
+ * rounded once to bf16 (round to nearest even). */
+
+/* Repacks the up-projection weights for moe_gemm1_swiglu:
+ *   w_gate_up   device bf16 [E, H, 2I]: columns 0..I-1 the gate projection
+ *               Wg[e], columns I..2I-1 the up projection Wu[e] (each row k
+ *               of length 2I is the k-th input feature's weights)
+ *   w1_packed   device bf16 [E, H, 2I], a different buffer: column 32b + j
+ *               holds gate column 16b + j and column 32b + 16 + j up column
+ *               16b + j (j < 16), so each 32-column block carries the gate
+ *               and up weights of 16 outputs
+ * Enqueued on stream.  I % 16 == 0 (else MOE_ERR_UNSUPPORTED); E, H, I > 0
+ * and distinct non-null buffers (else MOE_ERR_INVALID_ARG); 2-byte aligned
+ * (else MOE_ERR_ALIGNMENT).  Returns 0 or MOE_ERR_HIP. */
+int moe_gemm1_pack_weights(const void* w_gate_up, void* w1_packed, int32_t E, int32_t H,
+                           int32_t I, void* stream);
+
+/* The up-projection: x_perm from hidden, as above, for the rows grouped by
+ * expert exactly as for moe_gemm2_combine.
+ *   hidden          device bf16 [T, H] (16-byte aligned)
+ *   w1              device bf16 [E, H, 2I], packed by moe_gemm1_pack_weights
+ *                   (16-byte aligned)
+ *   expert_offsets  device int32 [E+1], as for moe_gemm2_combine
+ *   token_ids       device int32 [rows]: the token of each permuted row; an id
+ *                   outside [0, T) is replaced by 0 and flagged
+ *                   (MOE_ERR_BAD_ROUTING from moe_gemm2_status)
+ *   x_perm          device bf16 [rows, I] (16-byte aligned), fully written for
+ *                   every row inside the expert ranges
+ *   wl              T, H, I, E, topk, rows as for moe_gemm2_combine (splits,
+ *                   ranks and host counts are not used, except that host
+ *                   counts, when given, must sum to rows)
+ *   workspace       a moe_gemm2 workspace (at least 512 bytes, 256-byte
+ *                   aligned, zeroed once by moe_gemm2_workspace_init): only
+ *                   its status word and zero block are used
+ * One persistent launch, every workgroup computing 256 x 256 tiles of the
+ * packed columns.  Supported: H % 8 == 0, I % 16 == 0, 1 <= E <= 1024,
+ * 1 <= topk <= 64 (else MOE_ERR_UNSUPPORTED).  Returns 0 or a negative
+ * status (host-side validation and launch errors). */
+int moe_gemm1_swiglu(const void* hidden, const void* w1, const int32_t* expert_offsets,
+                     const int32_t* token_ids, void* x_perm, const moe_workload_t* wl,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace moe_layer_forward needs: a moe_gemm2 workspace followed
+ * by x_perm.  0 for an invalid or unsupported workload. */
+size_t moe_layer_workspace_size(const moe_workload_t* wl);
+
+/* The post-router layer: moe_gemm1_swiglu into the workspace's x_perm, then
+ * moe_gemm2_combine on it (same stream, two launches).  Arguments as for
+ * those two functions; workspace of at least moe_layer_workspace_size(wl)
+ * bytes, 256-byte aligned, zeroed once by moe_gemm2_workspace_init.  Shapes
+ * must satisfy both functions' limits.  Returns the number of consumer
+ * workgroups of the second launch (>= 0) or a negative status. */
+int moe_layer_forward(const void* hidden, const void* w1, const void* w2,
+                      const int32_t* expert_offsets, const int32_t* token_ids,
+                      const float* gate_w, float* out, const moe_workload_t* wl,
+                      int32_t num_consumers, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
 /* Synchronises stream, then reports the device-side status of the last
  * launches that used this workspace: 0, MOE_ERR_TIMEOUT or
  * MOE_ERR_BAD_ROUTING (or MOE_ERR_HIP).  clear != 0 resets it. */
@@ -263,7 +332,7 @@ int moe_gemm2_status(void* workspace, void* stream, int clear);
 /* Static description of an error code. */
 const char* moe_strerror(int status);
 
-/* ABI version of this header (major * 100 + minor): 102. */
+/* ABI version of this header (major * 100 + minor): 103. */
 int moe_gemm2_abi_version(void);
 
 #ifdef __cplusplus

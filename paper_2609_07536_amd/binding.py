@@ -31,7 +31,8 @@ EXPORTED = (
     "moe_gemm2_workspace_size", "moe_gemm2_workspace_init", "moe_gemm2_combine",
     "moe_gemm2_combine_traced", "moe_gemm2_trace_size", "moe_gemm2_status",
     "moe_strerror", "moe_gemm2_abi_version", "moe_gemm2_default_params_ex",
-    "moe_gemm2_combine_ex", "moe_gemm2_launch_params",
+    "moe_gemm2_combine_ex", "moe_gemm2_launch_params", "moe_gemm1_pack_weights",
+    "moe_gemm1_swiglu", "moe_layer_workspace_size", "moe_layer_forward",
 )
 
 MODE_OWNER_WRITE = 0
@@ -123,6 +124,15 @@ def lib() -> ctypes.CDLL:
                                                ctypes.POINTER(Workload), i32, i32, vp, sz,
                                                vp, vp, sz]
             L.moe_gemm2_combine_ex.restype = ctypes.c_int
+            L.moe_gemm1_pack_weights.argtypes = [vp, vp, i32, i32, i32, vp]
+            L.moe_gemm1_pack_weights.restype = ctypes.c_int
+            L.moe_gemm1_swiglu.argtypes = [vp, vp, vp, vp, vp, ctypes.POINTER(Workload), vp, sz, vp]
+            L.moe_gemm1_swiglu.restype = ctypes.c_int
+            L.moe_layer_workspace_size.argtypes = [ctypes.POINTER(Workload)]
+            L.moe_layer_workspace_size.restype = sz
+            L.moe_layer_forward.argtypes = [vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(Workload),
+                                            i32, vp, sz, vp]
+            L.moe_layer_forward.restype = ctypes.c_int
             L.moe_gemm2_status.argtypes = [vp, vp, ctypes.c_int]
             L.moe_gemm2_status.restype = ctypes.c_int
             L.moe_strerror.argtypes = [ctypes.c_int]
@@ -265,4 +275,89 @@ def combine(x_perm, w2, expert_offsets, token_ids, gate_w, T: int, splits: int =
     del keep
     if r < 0:
         raise MoeError(r, "moe_gemm2_combine")
+    return out, r
+
+
+# ---- the up-projection and the whole post-router layer -----------------------------
+
+def _check_tensor(t, dt, what):
+    if t.dtype != dt or not t.is_contiguous() or not t.is_cuda:
+        raise TypeError(f"{what}: expected a contiguous CUDA {dt} tensor, got {t.dtype}")
+
+
+def pack_w1(w_gate_up, stream=None):
+    """moe_gemm1_pack_weights: [E, H, 2I] (gate columns, then up columns) to
+    the packed layout the up-projection reads; returns a new tensor."""
+    import torch
+    _check_tensor(w_gate_up, torch.bfloat16, "w_gate_up")
+    E, H, N = (int(d) for d in w_gate_up.shape)
+    out = torch.empty_like(w_gate_up)
+    r = lib().moe_gemm1_pack_weights(ctypes.c_void_p(w_gate_up.data_ptr()),
+                                     ctypes.c_void_p(out.data_ptr()), E, H, N // 2, _stream(stream))
+    if r < 0:
+        raise MoeError(r, "moe_gemm1_pack_weights")
+    return out
+
+
+def layer_workspace_size(wl: Workload) -> int:
+    return int(lib().moe_layer_workspace_size(ctypes.byref(wl)))
+
+
+def gemm1_swiglu(hidden, w1_packed, expert_offsets, token_ids, topk: int, rows: int,
+                 counts=None, out=None, workspace: Optional[Workspace] = None, stream=None):
+    """moe_gemm1_swiglu on torch device tensors: hidden bf16 [T, H], w1_packed
+    bf16 [E, H, 2I]; returns x_perm bf16 [rows, I]."""
+    import torch
+    _check_tensor(hidden, torch.bfloat16, "hidden")
+    _check_tensor(w1_packed, torch.bfloat16, "w1")
+    _check_tensor(expert_offsets, torch.int32, "expert_offsets")
+    _check_tensor(token_ids, torch.int32, "token_ids")
+    T, H = int(hidden.shape[0]), int(hidden.shape[1])
+    E, I = int(w1_packed.shape[0]), int(w1_packed.shape[2]) // 2
+    wl, keep = make_workload(T, H, I, E, topk, 1, counts, rows=rows)
+    if out is None:
+        out = torch.empty((max(rows, 1), I), dtype=torch.bfloat16, device=hidden.device)
+    if workspace is None:
+        workspace = Workspace(512, device=hidden.device, stream=stream)
+    vp = ctypes.c_void_p
+    r = lib().moe_gemm1_swiglu(vp(hidden.data_ptr()), vp(w1_packed.data_ptr()),
+                               vp(expert_offsets.data_ptr()), vp(token_ids.data_ptr()),
+                               vp(out.data_ptr()), ctypes.byref(wl), vp(workspace.ptr),
+                               ctypes.c_size_t(workspace.nbytes), _stream(stream))
+    del keep
+    if r < 0:
+        raise MoeError(r, "moe_gemm1_swiglu")
+    return out
+
+
+def layer_forward(hidden, w1_packed, w2, expert_offsets, token_ids, gate_w, topk: int,
+                  splits: int = 1, counts=None, num_consumers: int = -1, out=None,
+                  workspace: Optional[Workspace] = None, stream=None):
+    """moe_layer_forward: the up-projection then the down-projection with the
+    combine; returns (out fp32 [T, H], C of the second launch)."""
+    import torch
+    for t, dt, what in ((hidden, torch.bfloat16, "hidden"), (w1_packed, torch.bfloat16, "w1"),
+                        (w2, torch.bfloat16, "w2"), (expert_offsets, torch.int32, "offsets"),
+                        (token_ids, torch.int32, "token_ids"), (gate_w, torch.float32, "gate_w")):
+        _check_tensor(t, dt, what)
+    T, H = int(hidden.shape[0]), int(hidden.shape[1])
+    E, I = int(w2.shape[0]), int(w2.shape[1])
+    rows = int(token_ids.shape[0])
+    wl, keep = make_workload(T, H, I, E, topk, splits, counts, rows=rows)
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.float32, device=hidden.device)
+    need = layer_workspace_size(wl)
+    if need == 0:
+        raise MoeError(MOE_ERR_UNSUPPORTED, "moe_layer_workspace_size")
+    if workspace is None or workspace.nbytes < need:
+        workspace = Workspace(need, device=hidden.device, stream=stream)
+    vp = ctypes.c_void_p
+    r = lib().moe_layer_forward(vp(hidden.data_ptr()), vp(w1_packed.data_ptr()), vp(w2.data_ptr()),
+                                vp(expert_offsets.data_ptr()), vp(token_ids.data_ptr()),
+                                vp(gate_w.data_ptr()), vp(out.data_ptr()), ctypes.byref(wl),
+                                int(num_consumers), vp(workspace.ptr),
+                                ctypes.c_size_t(workspace.nbytes), _stream(stream))
+    del keep
+    if r < 0:
+        raise MoeError(r, "moe_layer_forward")
     return out, r

@@ -101,6 +101,48 @@ struct KArgs {
   int mode;                   // 0 owner-write, 1 fp32 atomic scatter
 };
 
+// Arguments of the up-projection stage (grouped GEMM1 with the SwiGLU
+// activation): x_perm[r, c] = silu(h_r . Wg[e(r)][:, c]) * (h_r . Wu[e(r)][:, c])
+// with h_r = hidden[token_ids[r]], the tokens gathered by the loads.
+struct G1Args {
+  const uint16_t* hidden;     // [T, H] bf16
+  const uint16_t* w1;         // [E, H, 2I] bf16, gate and up interleaved in 16-column blocks
+  const int32_t* offsets;     // [E+1]
+  const int32_t* token_ids;   // [rows]
+  uint16_t* xout;             // [rows, I] bf16
+  uint32_t* status;           // [1]
+  const uint16_t* zeros;      // 16+ zero bytes
+  long long rows;             // capacity of token_ids / xout
+  int T, H, I, E;
+  int ntps;                   // n-tiles of the packed 2I columns
+  int nsplit;                 // = 2I (one split)
+};
+
+// The grouped GEMM core below serves two stages through these accessors:
+// its reduction length, the row length of its B operand, B of expert e, the
+// A row of a routed row, and the zero block for chunks past the reduction.
+__device__ __forceinline__ int gemm_k(const KArgs& a) { return a.I; }
+__device__ __forceinline__ int gemm_ldb(const KArgs& a) { return a.H; }
+__device__ __forceinline__ const uint16_t* gemm_b(const KArgs& a, int e) {
+  return a.w2 + (size_t)e * a.I * a.H;
+}
+__device__ __forceinline__ const uint16_t* gemm_a_row(const int* rowtok, const KArgs& a, long long r0,
+                                                     int row) {
+  return a.x + (size_t)(r0 + row) * a.I;
+}
+__device__ __forceinline__ int gemm_k(const G1Args& a) { return a.H; }
+__device__ __forceinline__ int gemm_ldb(const G1Args& a) { return 2 * a.I; }
+__device__ __forceinline__ const uint16_t* gemm_b(const G1Args& a, int e) {
+  return a.w1 + (size_t)e * a.H * (2 * a.I);
+}
+// the gathered token of the tile's row `row`, staged in LDS
+__device__ __forceinline__ const uint16_t* gemm_a_row(const int* rowtok, const G1Args& a, long long r0,
+                                                     int row) {
+  return a.hidden + (size_t)rowtok[row] * a.H;
+}
+template <class Args> struct RowGather { static constexpr bool on = false; };
+template <> struct RowGather<G1Args> { static constexpr bool on = true; };
+
 struct Smem {
   uint16_t a[kStages][kBM * kBK];  // x tile: row m = kBK/8 chunks of 8 k (swizzled)
   uint16_t b[kStages][kBK * kBN];  // W2 tile: row k = 32 chunks of 8 n (swizzled)
@@ -108,6 +150,7 @@ struct Smem {
   int count[kMaxE];           // sanitized row count of each expert
   int tile_prefix[kMaxE + 1]; // exclusive prefix of ceil(count/kBM)
   int scan[kThreads];
+  int rowtok[kBM];            // gathering stages: token of each row of the staged tile
   int flag;
   int task;                   // consumer task claimed by the workgroup
   u64 epoch;                  // this launch's epoch, read once at the start
@@ -203,7 +246,8 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
 // flagged); overlapping ranges from bad input compute some rows twice (with
 // meaningless values), and a tile count past the workspace's capacity makes
 // the compute workgroups stop (flagged) instead of indexing past it.
-__device__ void load_experts(Smem& sm, const KArgs& a) {
+template <class Args>
+__device__ void load_experts(Smem& sm, const Args& a) {
   const int tid = threadIdx.x;
   bool bad = false;
   for (int e = tid; e < a.E; e += kThreads) {
@@ -405,17 +449,19 @@ struct TileCtx {
 // kLoadsPerStage to vmcnt; lanes whose chunk lies past the reduction
 // (k >= I) load 16 zero bytes from the workspace instead, which zeroes both
 // operands there.
-__device__ __forceinline__ void issue_load(const KArgs& a, const TileCtx& t, int kt, int slot,
+template <class Args>
+__device__ __forceinline__ void issue_load(const Args& a, const TileCtx& t, int kt, int slot,
                                            int wave, int q) {
   const int k0 = kt * kBK;
   const uint32_t blk = (uint32_t)(slot * kStageElems + (kLoadsPerOperand * wave + q) * 512) * 2;
   const int kx = k0 + t.xk[q];
-  dma16(kx < a.I ? t.xg[q] + kx : a.zeros, t.lds_a + blk);
+  dma16(kx < gemm_k(a) ? t.xg[q] + kx : a.zeros, t.lds_a + blk);
   const int kw = k0 + t.wk[q];
-  dma16(kw < a.I ? t.wgp[q] + (size_t)kw * a.H : a.zeros, t.lds_b + blk);
+  dma16(kw < gemm_k(a) ? t.wgp[q] + (size_t)kw * gemm_ldb(a) : a.zeros, t.lds_b + blk);
 }
 
-__device__ __forceinline__ void issue_stage(const KArgs& a, const TileCtx& t, int kt, int slot,
+template <class Args>
+__device__ __forceinline__ void issue_stage(const Args& a, const TileCtx& t, int kt, int slot,
                                             int wave) {
 #pragma unroll
   for (int q = 0; q < kLoadsPerOperand; ++q) issue_load(a, t, kt, slot, wave, q);
@@ -454,8 +500,9 @@ __device__ __forceinline__ void mfma_step(f32x16 (&acc)[kNB][kMB], const bf16x8 
 // mfma_step with loads q0 .. q0+kNB-1 of stage kt issued one after each
 // n-block of MFMAs: spread out, the loads never hold the wave's in-order
 // issue long enough to starve the matrix core.
+template <class Args>
 __device__ __forceinline__ void mfma_step_loads(f32x16 (&acc)[kNB][kMB], const bf16x8 (&af)[kNB],
-                                                const bf16x8 (&bm)[kMB], const KArgs& a,
+                                                const bf16x8 (&bm)[kMB], const Args& a,
                                                 const TileCtx& t, int kt, int slot, int wave,
                                                 int q0, bool on) {
 #pragma unroll
@@ -473,10 +520,32 @@ struct TileInfo {
   int e, r0, rows_valid, n0, cols_valid;
 };
 
+// Gathering stages: the token of tile row threadIdx.x (rows past the
+// expert repeat its last row), loaded from token_ids.  The id is checked
+// only when it is staged (gather_commit, after a wait that covers the load
+// anyway): an id outside [0, T) is flagged and replaced by 0, so that every
+// load of the hidden rows stays in bounds.
+__device__ __forceinline__ int gather_load(const G1Args& a, const TileInfo& ti) {
+  const int i = threadIdx.x;
+  if (i >= kBM) return 0;
+  const long long r = (long long)ti.r0 + (i < ti.rows_valid ? i : ti.rows_valid - 1);
+  return a.token_ids[r];
+}
+__device__ __forceinline__ void gather_commit(Smem& sm, const G1Args& a, int t) {
+  if (threadIdx.x < kBM) {
+    if (t < 0 || t >= a.T) {
+      __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      t = 0;
+    }
+    sm.rowtok[threadIdx.x] = t;
+  }
+}
+
 // Tile g of the global sequence (split-major, then expert, m-tile, n-tile).
 // Every tile count fits in 32 bits (checked on the host for the worst case
 // of overlapping expert ranges).
-__device__ TileInfo decode_tile(const Smem& sm, const KArgs& a, int W_comp, int g) {
+template <class Args>
+__device__ TileInfo decode_tile(const Smem& sm, const Args& a, int W_comp, int g) {
   const int s = g / W_comp;
   const int idx = g - s * W_comp;
   const int mt = idx / a.ntps;
@@ -497,14 +566,15 @@ __device__ TileInfo decode_tile(const Smem& sm, const KArgs& a, int W_comp, int 
 }
 
 // This lane's global addresses for its loads of a tile's stages.
-__device__ __forceinline__ TileCtx make_ctx(Smem& sm, const KArgs& a, const TileInfo& ti, int wave) {
+template <class Args>
+__device__ __forceinline__ TileCtx make_ctx(Smem& sm, const Args& a, const TileInfo& ti, int wave) {
   const int lane = threadIdx.x & 63;
   const int e = ti.e, r0 = ti.r0, rows_valid = ti.rows_valid, n0 = ti.n0, cols_valid = ti.cols_valid;
   TileCtx t;
   t.lds_a = lds_addr(&sm.a[0][0]);
   t.lds_b = lds_addr(&sm.b[0][0]);
   {
-    const uint16_t* w2e = a.w2 + (size_t)e * a.I * a.H + n0;
+    const uint16_t* w2e = gemm_b(a, e) + n0;
 #pragma unroll
     for (int q = 0; q < kLoadsPerOperand; ++q) {
       const int i = kLoadsPerOperand * wave + q;   // 1 KB block of the stage
@@ -512,7 +582,7 @@ __device__ __forceinline__ TileCtx make_ctx(Smem& sm, const KArgs& a, const Tile
       const int row = kXRowsPerLoad * i + lane / kXChunks;
       const int lc = (lane % kXChunks) ^ ((row / kXRowsPerLine) % kXChunks);
       const int grow = row < rows_valid ? row : rows_valid - 1;   // rows past the expert: unused
-      t.xg[q] = a.x + (size_t)(r0 + grow) * a.I;
+      t.xg[q] = gemm_a_row(sm.rowtok, a, r0, grow);
       t.xk[q] = 8 * lc;
       // W2: rows 2i + L/32, physical chunk L%32
       const int krow = 2 * i + (lane >> 5);
@@ -527,7 +597,8 @@ __device__ __forceinline__ TileCtx make_ctx(Smem& sm, const KArgs& a, const Tile
 
 // The loads of a tile's first min(kStages, nk) stages (its ring fill), the
 // tile's stage 0 going into ring slot `base`.
-__device__ __forceinline__ void issue_prologue(const KArgs& a, const TileCtx& t, int nk, int base,
+template <class Args>
+__device__ __forceinline__ void issue_prologue(const Args& a, const TileCtx& t, int nk, int base,
                                                int wave) {
 #pragma unroll
   for (int s = 0; s < kStages; ++s)
@@ -538,8 +609,9 @@ __device__ __forceinline__ void issue_prologue(const KArgs& a, const TileCtx& t,
 // fragments read before the boundary) and the other steps of stage kt+1
 // (slot s1), with the loads of stage `ls` of the tile `tl` into slot `lslot`
 // spread over the first kLoadSteps steps.
+template <class Args>
 __device__ __forceinline__ void boundary_steps(f32x16 (&acc)[kNB][kMB], bf16x8 (&af)[2][kNB],
-                                               bf16x8 (&bm)[2][kMB], const KArgs& a,
+                                               bf16x8 (&bm)[2][kMB], const Args& a,
                                                lds_u16* As1, lds_u16* Bs1, const int (&offA)[kNB],
                                                const int (&offB)[kKS], const TileCtx& tl, int ls,
                                                int lslot, int wave, bool on) {
@@ -558,110 +630,12 @@ __device__ __forceinline__ void boundary_steps(f32x16 (&acc)[kNB][kMB], bf16x8 (
   }
 }
 
-// Computes tile `ti` and stores it to Y.  The ring continues across tiles:
-// stage kt of this tile sits in slot (base + kt) % kStages, and the next
-// tile's stages follow this tile's last one.  Its ring fill was issued
-// already if `filled`; with `next`, the next tile `nt` gets its stage 0
-// from this tile's last stage boundary (the slot freed there, while this
-// tile's last stage computes) and its stage 1 after this tile's Y stores
-// (the slot of this tile's last stage, which carries the epilogue).
-__device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool filled, bool next,
-                             const TileInfo& nt, int base, u64* t_mid) {
-  // The lane's LDS offsets are recomputed for every tile (a few VALU
-  // operations) rather than kept across the tile loop.
-  const int lane = opaque_tid() & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nk = (a.I + kBK - 1) / kBK;
+// The tile's Y rows: bf16 through the LDS slot `eslot` to whole-line stores.
+__device__ __forceinline__ void epilogue_store(Smem& sm, const KArgs& a, f32x16 (&acc)[kNB][kMB],
+                                               int eslot, int lane, int wave, int wn0, int wm0,
+                                               const TileInfo& ti) {
   const int rows_valid = ti.rows_valid, cols_valid = ti.cols_valid, r0 = ti.r0, n0 = ti.n0;
-  const TileCtx t = make_ctx(sm, a, ti, wave);
-
-  // per-lane LDS element offsets of the MFMA fragments (stage 0, step 0)
-  const int wn0 = (wave % kWavesN) * kWN;
-  const int wm0 = (wave / kWavesN) * kWM;
-  int offA[kNB];
-  {
-    const int j = lane & 15;
-    const int krow = 8 * (lane >> 5) + (j >> 2);
-    const int u = j & 3;
-    const int rg = (lane >> 4) & 1;
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
-      const int col = wn0 + 32 * nb + 16 * rg + 8 * (u & 1) + 4 * (u >> 1);
-      offA[nb] = krow * kBN + (((col >> 3) ^ (4 * (krow & 3))) << 3) + (col & 7);
-    }
-  }
-  int offB[kKS];
-  {
-    const int m = wm0 + (lane & 31);
-#pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) {
-      const int c = 2 * ks + (lane >> 5);
-      offB[ks] = m * kBK + ((c ^ ((m / kXRowsPerLine) % kXChunks)) << 3);
-    }
-  }
-
-  f32x16 acc[kNB][kMB];
-#pragma unroll
-  for (int i = 0; i < kNB; ++i)
-#pragma unroll
-    for (int j = 0; j < kMB; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-  // prologue: fill the ring (unless done during the previous tile's
-  // publish), then wait for stage 0 (every wave's share)
-  if (!filled) issue_prologue(a, t, nk, base, wave);
-  wait_stage(min(kStages - 1, nk - 1));
-  block_barrier();
-
-  // One flat pipeline over the K=16 steps: the fragments of step g+1 are
-  // read while the MFMAs of step g run, also across stage boundaries.  The
-  // stage boundary (stage kt+1 landed for every wave, every wave done
-  // reading the slot of stage kt) is one barrier, after which that slot is
-  // refilled with stage kt + kStages (of the next tile past the last one).
-  bf16x8 af[2][kNB], bm[2][kMB];
-  auto slot_of = [&](int kt) { return (base + kt) % kStages; };
-  auto slot_a = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_a + slot_of(kt) * kStageElems * 2); };
-  auto slot_b = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_b + slot_of(kt) * kStageElems * 2); };
-  // Steps are grouped so that the loop starts at a stage boundary (which
-  // waits for all LDS reads anyway) and every MFMA group follows the reads
-  // of the next step in straight-line code: the compiler's LDS waits before
-  // each group then cover only that group's own fragments.
-  load_frags(slot_a(0), slot_b(0), offA, offB, 0, af[0], bm[0]);
-#pragma unroll
-  for (int ks = 0; ks + 1 < kKS; ++ks) {
-    load_frags(slot_a(0), slot_b(0), offA, offB, ks + 1, af[(ks + 1) & 1], bm[(ks + 1) & 1]);
-    __builtin_amdgcn_sched_barrier(0);   // keep the next step's reads ahead of these MFMAs
-    mfma_step(acc, af[ks & 1], bm[ks & 1]);
-  }
-  static_assert(kLoadsPerOperand % kNB == 0 && kLoadsPerOperand / kNB <= kKS, "load spread");
-  static_assert(kStages == 2, "the boundary loop refills one stage ahead");
-  // boundaries whose freed slot takes a stage of this tile
-  for (int kt = 0; kt + kStages < nk; ++kt) {
-    wait_stage(kStages - 2);
-    block_barrier();
-    boundary_steps(acc, af, bm, a, slot_a(kt + 1), slot_b(kt + 1), offA, offB, t, kt + kStages,
-                   slot_of(kt), wave, true);
-  }
-  // the last boundary: its freed slot takes the next tile's stage 0
-  if (nk >= 2) {
-    wait_stage(0);
-    block_barrier();
-    const TileCtx tn = make_ctx(sm, a, next ? nt : ti, wave);
-    boundary_steps(acc, af, bm, a, slot_a(nk - 1), slot_b(nk - 1), offA, offB, tn, 0,
-                   slot_of(nk), wave, next);
-  }
-  mfma_step(acc, af[(kKS - 1) & 1], bm[(kKS - 1) & 1]);
-  // every wave is done with the slot of the last stage, which carries the
-  // epilogue
-  block_barrier();
-  t_mid[0] = now_100mhz();
-  const int eslot = slot_of(nk - 1);
-  // with a single stage there was no boundary: the next tile's stage 0 goes
-  // into the other slot now, ahead of the Y stores
-  if (next && nk == 1) issue_stage(a, make_ctx(sm, a, nt, wave), 0, slot_of(nk), wave);
-
-  // epilogue: the wave's kWM x kWN block goes through LDS in two halves of
+  // The wave's kWM x kWN block goes through LDS in two halves of
   // 64 rows (8 KB per wave, in slot eslot) as bf16 rows of 2 kWN bytes, 16-byte
   // chunk j of row r at chunk j ^ ((r / r1) % c), c = chunks per row,
   // r1 = rows per 256-byte bank line (so 16 consecutive rows hit 16 distinct
@@ -711,6 +685,179 @@ __device__ void compute_tile(Smem& sm, const KArgs& a, const TileInfo& ti, bool 
         store16_nt(a.Y + (size_t)(r0 + m) * a.ypitch + n0 + n, __builtin_bit_cast(u32x4, v));
     }
   }
+}
+
+// The up-projection tile's outputs.  In the packed W1 a 32-column block is
+// 16 gate columns followed by the up columns of the same 16 outputs, and the
+// MFMA row remap gives lane half h the accumulators 8c..8c+7 = 8 consecutive
+// columns 32nb + 16c + 8h.., so a lane holds the gate (c = 0) and the up
+// (c = 1) values of the same 8 outputs: act = silu(gate) * up in fp32,
+// rounded once to bf16.  The workgroup's 256 x 128 outputs go through the
+// LDS slot eslot (rows 0..127 in its x part, 128..255 in its W part; 16-byte
+// chunk c of row r at c ^ (r % 16), so 16 rows' chunks hit 16 distinct bank
+// groups) and leave as whole 256-byte row pieces of x_perm.
+__device__ __forceinline__ void epilogue_store(Smem& sm, const G1Args& a, f32x16 (&acc)[kNB][kMB],
+                                               int eslot, int lane, int wave, int wn0, int wm0,
+                                               const TileInfo& ti) {
+  constexpr int kOut = kBN / 2;           // output columns per tile
+  constexpr int kChunks = kOut / 8;       // 16-byte chunks per output row
+  static_assert(kChunks == 16 && (kBM / 2) * kOut <= kStageElems, "activation epilogue layout");
+  const int h = lane >> 5;
+  auto row_ptr = [&](int row) {
+    return (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(
+               row < kBM / 2 ? lds_addr(&sm.a[eslot][0]) : lds_addr(&sm.b[eslot][0])) +
+           (row & (kBM / 2 - 1)) * kOut;
+  };
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < kMB; ++mb) {
+      const int row = wm0 + 32 * mb + (lane & 31);
+      const int chunk = wn0 / 16 + 2 * nb + h;
+      bf16x8 v;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float g = acc[nb][mb][i];
+        const float u = acc[nb][mb][8 + i];
+        v[i] = (__bf16)(g / (1.f + __expf(-g)) * u);
+      }
+      *(__attribute__((address_space(3))) bf16x8*)(row_ptr(row) + ((chunk ^ (row & 15)) << 3)) = v;
+    }
+  block_barrier();   // every wave's outputs are in the slot
+  const int c0 = ti.n0 / 2, cvalid = ti.cols_valid / 2;
+  for (int idx = threadIdx.x; idx < kBM * kChunks; idx += kThreads) {
+    const int row = idx / kChunks, ch = idx % kChunks;
+    const bf16x8 v =
+        *(const __attribute__((address_space(3))) bf16x8*)(row_ptr(row) + ((ch ^ (row & 15)) << 3));
+    if (row < ti.rows_valid && 8 * ch < cvalid)
+      store16_nt(a.xout + (size_t)(ti.r0 + row) * a.I + c0 + 8 * ch, __builtin_bit_cast(u32x4, v));
+  }
+}
+
+// Computes tile `ti` and stores it to Y.  The ring continues across tiles:
+// stage kt of this tile sits in slot (base + kt) % kStages, and the next
+// tile's stages follow this tile's last one.  Its ring fill was issued
+// already if `filled`; with `next`, the next tile `nt` gets its stage 0
+// from this tile's last stage boundary (the slot freed there, while this
+// tile's last stage computes) and its stage 1 after this tile's Y stores
+// (the slot of this tile's last stage, which carries the epilogue).
+template <class Args>
+__device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool filled, bool next,
+                             const TileInfo& nt, int base, u64* t_mid) {
+  // The lane's LDS offsets are recomputed for every tile (a few VALU
+  // operations) rather than kept across the tile loop.
+  const int lane = opaque_tid() & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nk = (gemm_k(a) + kBK - 1) / kBK;
+  if constexpr (RowGather<Args>::on) {
+    // the tile's gathered rows: staged by the previous tile when it loaded
+    // this tile's first stage, else now
+    if (!filled) {
+      gather_commit(sm, a, gather_load(a, ti));
+      block_barrier();
+    }
+  }
+  const TileCtx t = make_ctx(sm, a, ti, wave);
+
+  // per-lane LDS element offsets of the MFMA fragments (stage 0, step 0)
+  const int wn0 = (wave % kWavesN) * kWN;
+  const int wm0 = (wave / kWavesN) * kWM;
+  int offA[kNB];
+  {
+    const int j = lane & 15;
+    const int krow = 8 * (lane >> 5) + (j >> 2);
+    const int u = j & 3;
+    const int rg = (lane >> 4) & 1;
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) {
+      const int col = wn0 + 32 * nb + 16 * rg + 8 * (u & 1) + 4 * (u >> 1);
+      offA[nb] = krow * kBN + (((col >> 3) ^ (4 * (krow & 3))) << 3) + (col & 7);
+    }
+  }
+  int offB[kKS];
+  {
+    const int m = wm0 + (lane & 31);
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) {
+      const int c = 2 * ks + (lane >> 5);
+      offB[ks] = m * kBK + ((c ^ ((m / kXRowsPerLine) % kXChunks)) << 3);
+    }
+  }
+
+  f32x16 acc[kNB][kMB];
+#pragma unroll
+  for (int i = 0; i < kNB; ++i)
+#pragma unroll
+    for (int j = 0; j < kMB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  // prologue: fill the ring (unless done during the previous tile's
+  // publish), then wait for stage 0 (every wave's share)
+  if (!filled) issue_prologue(a, t, nk, base, wave);
+  wait_stage(min(kStages - 1, nk - 1));
+  block_barrier();
+  // gathering stages: the next tile's tokens load now and are staged at the
+  // last stage boundary (after its wait, so waiting for them costs nothing)
+  int next_tok = 0;
+  if constexpr (RowGather<Args>::on) {
+    if (next) next_tok = gather_load(a, nt);
+  }
+
+  // One flat pipeline over the K=16 steps: the fragments of step g+1 are
+  // read while the MFMAs of step g run, also across stage boundaries.  The
+  // stage boundary (stage kt+1 landed for every wave, every wave done
+  // reading the slot of stage kt) is one barrier, after which that slot is
+  // refilled with stage kt + kStages (of the next tile past the last one).
+  bf16x8 af[2][kNB], bm[2][kMB];
+  auto slot_of = [&](int kt) { return (base + kt) % kStages; };
+  auto slot_a = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_a + slot_of(kt) * kStageElems * 2); };
+  auto slot_b = [&](int kt) { return (lds_u16*)(uintptr_t)(t.lds_b + slot_of(kt) * kStageElems * 2); };
+  // Steps are grouped so that the loop starts at a stage boundary (which
+  // waits for all LDS reads anyway) and every MFMA group follows the reads
+  // of the next step in straight-line code: the compiler's LDS waits before
+  // each group then cover only that group's own fragments.
+  load_frags(slot_a(0), slot_b(0), offA, offB, 0, af[0], bm[0]);
+#pragma unroll
+  for (int ks = 0; ks + 1 < kKS; ++ks) {
+    load_frags(slot_a(0), slot_b(0), offA, offB, ks + 1, af[(ks + 1) & 1], bm[(ks + 1) & 1]);
+    __builtin_amdgcn_sched_barrier(0);   // keep the next step's reads ahead of these MFMAs
+    mfma_step(acc, af[ks & 1], bm[ks & 1]);
+  }
+  static_assert(kLoadsPerOperand % kNB == 0 && kLoadsPerOperand / kNB <= kKS, "load spread");
+  static_assert(kStages == 2, "the boundary loop refills one stage ahead");
+  // boundaries whose freed slot takes a stage of this tile
+  for (int kt = 0; kt + kStages < nk; ++kt) {
+    wait_stage(kStages - 2);
+    block_barrier();
+    boundary_steps(acc, af, bm, a, slot_a(kt + 1), slot_b(kt + 1), offA, offB, t, kt + kStages,
+                   slot_of(kt), wave, true);
+  }
+  // the last boundary: its freed slot takes the next tile's stage 0
+  if (nk >= 2) {
+    wait_stage(0);
+    if constexpr (RowGather<Args>::on) {
+      if (next) gather_commit(sm, a, next_tok);   // this tile's rows are in t already
+    }
+    block_barrier();
+    const TileCtx tn = make_ctx(sm, a, nt, wave);   // nt is a valid tile (== ti) without a next one
+    boundary_steps(acc, af, bm, a, slot_a(nk - 1), slot_b(nk - 1), offA, offB, tn, 0,
+                   slot_of(nk), wave, next);
+  }
+  mfma_step(acc, af[(kKS - 1) & 1], bm[(kKS - 1) & 1]);
+  if constexpr (RowGather<Args>::on) {
+    if (next && nk == 1) gather_commit(sm, a, next_tok);
+  }
+  // every wave is done with the slot of the last stage, which carries the
+  // epilogue
+  block_barrier();
+  t_mid[0] = now_100mhz();
+  const int eslot = slot_of(nk - 1);
+  // with a single stage there was no boundary: the next tile's stage 0 goes
+  // into the other slot now, ahead of the Y stores
+  if (next && nk == 1) issue_stage(a, make_ctx(sm, a, nt, wave), 0, slot_of(nk), wave);
+
+  epilogue_store(sm, a, acc, eslot, lane, wave, wn0, wm0, ti);
   if (next && nk >= 2) {
     // every wave has read its block back (its stores carry the data), so
     // the slot may take the next tile's stage 1
@@ -1156,6 +1303,47 @@ moe_gemm2_fused(KArgs a) {
   }
 }
 
+// ---- the up-projection stage: grouped GEMM1 + SwiGLU -----------------------------
+// Every workgroup computes: tiles expert -> m-tile -> n-tile of the packed
+// 2I columns, workgroup c (XCD-aware index) taking tiles c, c+P, ...
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+moe_gemm1_swiglu_kernel(G1Args a) {
+  __shared__ Smem sm;
+  load_experts(sm, a);
+  const int m_tiles = sm.tile_prefix[a.E];
+  const int total = m_tiles * a.ntps;
+  const int P = (int)gridDim.x;
+  const int c = compute_index((int)blockIdx.x, 0, P);
+  if (c >= total) return;
+  const int nk = (a.H + kBK - 1) / kBK;
+  bool filled = false;
+  int base = 0;
+  for (int g = c; g < total; g += P) {
+    const bool next = g + P < total;
+    const TileInfo cur = decode_tile(sm, a, total, g);
+    const TileInfo nt = decode_tile(sm, a, total, next ? g + P : g);
+    u64 t_mid[2];
+    compute_tile(sm, a, cur, filled, next, nt, base, t_mid);
+    base = (base + nk) % kStages;
+    filled = next;
+  }
+}
+
+// W1 from [E, H, 2I] (gate columns 0..I-1, up columns I..2I-1) to the
+// packed layout: column 32b + j holds gate column 16b + j and column
+// 32b + 16 + j up column 16b + j (j < 16).
+__global__ void pack_w1_kernel(const uint16_t* src, uint16_t* dst, long long n, int I) {
+  const int N = 2 * I;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < n;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const long long row = idx / N;
+    const int p = (int)(idx - row * N);
+    const int b = p >> 5, j = p & 31;
+    const int col = j < 16 ? 16 * b + j : I + 16 * b + (j - 16);
+    dst[idx] = src[row * N + col];
+  }
+}
+
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (size_t)gridDim.x * blockDim.x)
@@ -1542,4 +1730,124 @@ extern "C" int moe_gemm2_status(void* workspace, void* stream, int clear) {
   if (v & kStTimeout) return MOE_ERR_TIMEOUT;
   if (v & kStBadRouting) return MOE_ERR_BAD_ROUTING;
   return MOE_OK;
+}
+
+// ---- the up-projection stage and the whole post-router layer ----------------------
+namespace {
+
+int check_gemm1_shape(const moe_workload_t* wl) {
+  if (!wl) return MOE_ERR_INVALID_ARG;
+  if (wl->T < 0 || wl->H <= 0 || wl->I <= 0 || wl->E <= 0 || wl->topk <= 0 || wl->rows < 0)
+    return MOE_ERR_INVALID_ARG;
+  if (wl->E > kMaxE || wl->topk > kMaxTopk) return MOE_ERR_UNSUPPORTED;
+  if (wl->H % 8 != 0 || wl->I % 16 != 0) return MOE_ERR_UNSUPPORTED;
+  const long long rows = wl->rows > 0 ? wl->rows : (long long)wl->T * wl->topk;
+  if (rows > (long long)INT32_MAX || (long long)wl->T * wl->H > (long long)INT64_MAX / 4)
+    return MOE_ERR_UNSUPPORTED;
+  const long long ntps = (2LL * wl->I + kBN - 1) / kBN;
+  if ((long long)wl->E * ((rows + kBM - 1) / kBM + 1) * ntps > (long long)INT32_MAX / 2)
+    return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+int launch_gemm1(const void* hidden, const void* w1, const int32_t* expert_offsets,
+                 const int32_t* token_ids, void* x_perm, const moe_workload_t* wl, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  const int st = check_gemm1_shape(wl);
+  if (st != MOE_OK) return st;
+  const long long rows = wl->rows > 0 ? wl->rows : (long long)wl->T * wl->topk;
+  if (!hidden || !w1 || !expert_offsets || (rows > 0 && (!token_ids || !x_perm)))
+    return MOE_ERR_INVALID_ARG;
+  if (!aligned(hidden, 16) || !aligned(w1, 16) || !aligned(x_perm, 16) ||
+      !aligned(expert_offsets, 4) || !aligned(token_ids, 4))
+    return MOE_ERR_ALIGNMENT;
+  if (!workspace) return MOE_ERR_WORKSPACE;
+  if (!aligned(workspace, 256)) return MOE_ERR_ALIGNMENT;
+  if (workspace_bytes < 512) return MOE_ERR_WORKSPACE;
+  if (wl->host_expert_counts) {
+    long long sum = 0;
+    for (int e = 0; e < wl->E; ++e) {
+      if (wl->host_expert_counts[e] < 0) return MOE_ERR_INVALID_ARG;
+      sum += wl->host_expert_counts[e];
+    }
+    if (sum != rows) return MOE_ERR_INVALID_ARG;
+  }
+  if (rows == 0 || wl->T == 0) return MOE_OK;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOE_ERR_HIP;
+  DevInfo d;
+  const int r = device_info(dev, &d);
+  if (r != MOE_OK) return r;
+  char* ws = static_cast<char*>(workspace);
+  G1Args a;
+  a.hidden = static_cast<const uint16_t*>(hidden);
+  a.w1 = static_cast<const uint16_t*>(w1);
+  a.offsets = expert_offsets;
+  a.token_ids = token_ids;
+  a.xout = static_cast<uint16_t*>(x_perm);
+  a.status = reinterpret_cast<uint32_t*>(ws);
+  a.zeros = reinterpret_cast<const uint16_t*>(ws + kZeroBlock);
+  a.rows = rows;
+  a.T = wl->T;
+  a.H = wl->H;
+  a.I = wl->I;
+  a.E = wl->E;
+  a.ntps = (2 * wl->I + kBN - 1) / kBN;
+  a.nsplit = 2 * wl->I;
+  const int grid = d.occ * d.cus;
+  hipLaunchKernelGGL(moe_gemm1_swiglu_kernel, dim3(grid), dim3(kThreads), 0,
+                     static_cast<hipStream_t>(stream), a);
+  return hipGetLastError() == hipSuccess ? MOE_OK : MOE_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" int moe_gemm1_swiglu(const void* hidden, const void* w1, const int32_t* expert_offsets,
+                                const int32_t* token_ids, void* x_perm, const moe_workload_t* wl,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+  return launch_gemm1(hidden, w1, expert_offsets, token_ids, x_perm, wl, workspace,
+                      workspace_bytes, stream);
+}
+
+extern "C" int moe_gemm1_pack_weights(const void* w_gate_up, void* w1_packed, int32_t E,
+                                      int32_t H, int32_t I, void* stream) {
+  if (!w_gate_up || !w1_packed || w_gate_up == w1_packed || E <= 0 || H <= 0 || I <= 0)
+    return MOE_ERR_INVALID_ARG;
+  if (I % 16 != 0) return MOE_ERR_UNSUPPORTED;
+  if (!aligned(w_gate_up, 2) || !aligned(w1_packed, 2)) return MOE_ERR_ALIGNMENT;
+  const long long n = (long long)E * H * 2 * I;
+  const long long blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(pack_w1_kernel, dim3((unsigned)(blocks < 8192 ? blocks : 8192)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), static_cast<const uint16_t*>(w_gate_up),
+                     static_cast<uint16_t*>(w1_packed), n, (int)I);
+  return hipGetLastError() == hipSuccess ? MOE_OK : MOE_ERR_HIP;
+}
+
+extern "C" size_t moe_layer_workspace_size(const moe_workload_t* wl) {
+  Layout L;
+  if (check_gemm1_shape(wl) != MOE_OK || !make_layout(wl, &L)) return 0;
+  return round_up(L.total, 256) + round_up((size_t)L.rows * wl->I * 2, 256);
+}
+
+extern "C" int moe_layer_forward(const void* hidden, const void* w1, const void* w2,
+                                 const int32_t* expert_offsets, const int32_t* token_ids,
+                                 const float* gate_w, float* out, const moe_workload_t* wl,
+                                 int32_t num_consumers, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  int st = check_gemm1_shape(wl);
+  if (st != MOE_OK) return st;
+  st = check_shape(wl);
+  if (st != MOE_OK) return st;
+  Layout L;
+  if (!make_layout(wl, &L)) return MOE_ERR_INVALID_ARG;
+  if (!workspace) return MOE_ERR_WORKSPACE;
+  if (!aligned(workspace, 256)) return MOE_ERR_ALIGNMENT;
+  const size_t gemm2_bytes = round_up(L.total, 256);
+  if (workspace_bytes < moe_layer_workspace_size(wl)) return MOE_ERR_WORKSPACE;
+  void* x_perm = static_cast<char*>(workspace) + gemm2_bytes;
+  st = launch_gemm1(hidden, w1, expert_offsets, token_ids, x_perm, wl, workspace, gemm2_bytes,
+                    stream);
+  if (st != MOE_OK) return st;
+  return launch(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl, num_consumers, 0,
+                workspace, gemm2_bytes, stream, nullptr, 0);
 }
