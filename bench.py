@@ -235,6 +235,65 @@ def run_sweep(B, torch, samples, c_max=64):
             "per_workload": rows}
 
 
+def layer_measure(dw, B, torch, samples=20):
+    """The whole post-router layer on the same routing: the up-projection
+    (grouped GEMM1 + SwiGLU, moe_gemm1_swiglu), the layer (moe_layer_forward)
+    and this stage alone, launch for launch interleaved; the stage's share of
+    the layer is the quantity the paper reports for its baseline."""
+    w = dw.w
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1)
+    hidden = torch.randn((w.T, w.H), generator=g, device="cuda").to(torch.bfloat16)
+    w1 = (torch.randn((w.E, w.H, 2 * w.I), generator=g, device="cuda")
+          * (1.0 / np.sqrt(w.H))).to(torch.bfloat16)
+    w1p = B.pack_w1(w1)
+    del w1
+    xbuf = torch.empty((w.Mtot, w.I), dtype=torch.bfloat16, device="cuda")
+    out = torch.empty((w.T, w.H), dtype=torch.float32, device="cuda")
+    wl, _keep = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, w.counts, rows=w.Mtot)
+    lws = B.Workspace(B.layer_workspace_size(wl))
+
+    def gemm1():
+        B.gemm1_swiglu(hidden, w1p, dw.off, dw.tid, topk=w.topk, rows=w.Mtot, counts=w.counts,
+                       out=xbuf, workspace=dw.ws)
+
+    def layer():
+        B.layer_forward(hidden, w1p, dw.w2, dw.off, dw.tid, dw.g, topk=w.topk, splits=w.L,
+                        counts=w.counts, out=out, workspace=lws)
+
+    fns = {"gemm1": gemm1, "layer": layer, "stage": lambda: dw.run(-1)}
+    for f in fns.values():
+        f()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    times = {k: [] for k in fns}
+    keys = list(fns)
+    for s in range(samples):
+        order = keys if s % 2 == 0 else keys[::-1]
+        evs = []
+        for k in order:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fns[k]()
+            b.record(stream)
+            evs.append((k, a, b))
+        torch.cuda.synchronize()
+        for k, a, b in evs:
+            times[k].append(a.elapsed_time(b) * 1e3)
+    assert dw.ws.status() == 0 and lws.status() == 0
+    med = {k: float(np.median(v)) for k, v in times.items()}
+    f1 = 2 * w.Mtot * w.H * 2 * w.I
+    f2 = 2 * w.Mtot * w.I * w.H
+    return {"us_gemm1_swiglu": round(med["gemm1"], 1),
+            "gemm1_tflops": round(f1 / med["gemm1"] / 1e6, 1),
+            "us_layer": round(med["layer"], 1),
+            "layer_tflops": round((f1 + f2) / med["layer"] / 1e6, 1),
+            "us_gemm2_combine": round(med["stage"], 1),
+            "gemm2_combine_share_of_layer": round(med["stage"] / med["layer"], 4),
+            "samples": samples,
+            "inputs": "hidden N(0,1) and W1 N(0,1/H) drawn on the GPU, the stage's routing"}
+
+
 def spread(samples_us, reps=2000, seed=0):
     """Median, p10/p90 and a bootstrap 95% confidence interval of the median."""
     v = np.asarray(samples_us, dtype=np.float64)
@@ -283,6 +342,8 @@ def main():
     ap.add_argument("--sweep-samples", type=int, default=7)
     ap.add_argument("--calibrate", action="store_true",
                     help="print the rho_ref calibration at C=32 (both consumer modes) and exit")
+    ap.add_argument("--no-layer", action="store_true",
+                    help="skip the whole-layer measurement (up-projection + this stage)")
     ap.add_argument("--no-scatter", action="store_true",
                     help="skip the comparison with the atomic-scatter consumer mode")
     ap.add_argument("--timed-only", action="store_true",
@@ -402,6 +463,11 @@ def main():
                    "gemm_portion": {k: round(v, 3) for k, v in gp_sc.items()},
                    "combine": {k: round(v, 3) for k, v in comb_sc.items()} if comb_sc else None}
 
+    layer_res = None
+    if not args.no_layer:
+        log("post-router layer")
+        layer_res = layer_measure(dw, B, torch)
+
     res = {
         "metric": METRIC,
         "value": round(tflops, 2),
@@ -429,6 +495,7 @@ def main():
         "gemm_portion": {k: round(v, 3) for k, v in gemm_portion.items()},
         "combine": {k: round(v, 3) for k, v in combine.items()} if combine else None,
         "scatter_mode": scatter,
+        "layer": layer_res,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
