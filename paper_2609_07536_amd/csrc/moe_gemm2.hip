@@ -235,7 +235,12 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
   }
   __syncthreads();
   const bool ok = sm.flag != 0;
-  if (acquire) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  // One agent-scope acquire per workgroup, by the wave that saw the flags:
+  // it invalidates the CU's L1 and the XCD's L2, which every wave of the
+  // workgroup shares, and the barrier orders the other waves' reads after
+  // it.  (An acquire in every wave made eight L2 invalidates per workgroup;
+  // with all workgroups acquiring at once they queued for microseconds.)
+  if (acquire && threadIdx.x < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();  // sm.flag may be rewritten by the next wait
   return ok;
 }
