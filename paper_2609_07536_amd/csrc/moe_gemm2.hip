@@ -748,7 +748,7 @@ __device__ __forceinline__ void epilogue_store(Smem& sm, const G1Args& a, f32x16
 // (the slot of this tile's last stage, which carries the epilogue).
 template <class Args>
 __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool filled, bool next,
-                             const TileInfo& nt, int base, u64* t_mid) {
+                             const TileInfo& nt, int base, u64* t_mid, bool defer_stage1 = false) {
   // The lane's LDS offsets are recomputed for every tile (a few VALU
   // operations) rather than kept across the tile loop.
   const int lane = opaque_tid() & 63;
@@ -863,13 +863,21 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
   if (next && nk == 1) issue_stage(a, make_ctx(sm, a, nt, wave), 0, slot_of(nk), wave);
 
   epilogue_store(sm, a, acc, eslot, lane, wave, wn0, wm0, ti);
-  if (next && nk >= 2) {
+  if (next && nk >= 2 && !defer_stage1) {
     // every wave has read its block back (its stores carry the data), so
     // the slot may take the next tile's stage 1
     block_barrier();
     issue_stage(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
   }
   t_mid[1] = now_100mhz();
+}
+
+// The next tile's stage 1 into its slot, when the tile before deferred it
+// (after every wave has read its epilogue block back).
+template <class Args>
+__device__ __forceinline__ void issue_stage1(Smem& sm, const Args& a, const TileInfo& nt, int base) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  issue_stage(a, make_ctx(sm, a, nt, wave), 1, (base + 1) % kStages, wave);
 }
 
 // ---- consumer role: one task --------------------------------------------------
@@ -1239,7 +1247,10 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       const TileInfo nt = next ? decode(g_next) : cur;
       const u64 t_start = now_100mhz();
       u64 t_mid[2];
-      compute_tile(sm, a, cur, filled, next, nt, base, t_mid);
+      const bool last_of_split = !next || g_next / W_comp != g / W_comp;
+      // A split's last tile holds its next tile's stage 1 back until the
+      // publish, so that the publish's waits cover the Y stores only.
+      compute_tile(sm, a, cur, filled, next, nt, base, t_mid, last_of_split);
       base = (base + nk) % kStages;   // the next tile's stages follow this tile's
       // Publish once per split: consumers wait for whole splits, so the tiles
       // of a split are published together after this workgroup's last tile of
@@ -1249,10 +1260,9 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       // tile's stage 1, issued after them, may stay in flight), the barrier
       // orders those waits before thread 0, whose release fence writes back
       // the L2 before it stores the flags.
-      const bool last_of_split = !next || g_next / W_comp != g / W_comp;
       if (last_of_split) {
-        // (the stages issued after the stores may stay in flight)
-        wait_stage(next && nk >= 2 ? 1 : 0);
+        // only the next tile's stage 0 (older) and the Y stores are in flight
+        waitcnt_vm<0>();
         __syncthreads();
         if (threadIdx.x == 0) {
           __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -1268,6 +1278,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
         // since) at the next tile's start, on every tile
         waitcnt_vm<0>();
         split_first = g_next;
+        if (next && nk >= 2) issue_stage1(sm, a, nt, base);
       }
       if (a.trace && threadIdx.x == 0) {
         store8(&a.trace[4 * g + 0], t_start);
