@@ -1114,8 +1114,19 @@ struct Consumer {
   int ready;     // splits [0, ready] were acquired by this workgroup
   int split;     // the first split that may still have unclaimed tasks
   int meta_t0;   // token block whose metadata is in LDS (-1: none)
-  bool inv_ok;   // every workgroup's inverse-map share is published and acquired
+  bool inv_ok;   // every workgroup's inverse-map share is published
+  bool inv_acq;  // ... and acquired by this workgroup
 };
+
+// The owner-write task idx's metadata in LDS (unless it is there already).
+__device__ void ensure_task_meta(Smem& sm, const KArgs& a, int idx, Consumer& cs) {
+  const int t0 = (idx / a.cb_per_split) * a.comm_tm;
+  if (t0 != cs.meta_t0) {
+    __syncthreads();   // every wave is done with the previous task's metadata
+    load_task_meta(task_meta(sm), a, count_epoch(sm), t0, min(a.comm_tm, a.T - t0));
+    cs.meta_t0 = t0;
+  }
+}
 
 // Task idx of split s (owner-write: token block idx / cb_per_split, column
 // block idx % cb_per_split; atomic scatter: compute tile idx of the split).
@@ -1130,13 +1141,8 @@ __device__ void run_task(Smem& sm, const KArgs& a, int W_comp, int tps, int s, i
     const int ntok = min(a.comm_tm, a.T - t0);
     const int col0 = s * a.nsplit + cb * a.comm_tn;
     const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
-    TaskMeta& m = task_meta(sm);
-    if (t0 != cs.meta_t0) {
-      __syncthreads();   // every wave is done with the previous task's metadata
-      load_task_meta(m, a, count_epoch(sm), t0, ntok);
-      cs.meta_t0 = t0;
-    }
-    consume_task(a, m, t0, ntok, col0, ncols);
+    ensure_task_meta(sm, a, idx, cs);
+    consume_task(a, task_meta(sm), t0, ntok, col0, ncols);
   }
   if (a.trace) {
     __syncthreads();
@@ -1165,6 +1171,7 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
   if (!cs.inv_ok) {
     if (!wait_flags(sm, a.wg_flags, gridDim.x, a, W_comp == 0)) return;
     cs.inv_ok = true;
+    cs.inv_acq = W_comp == 0;
   }
   // owner-write: tasks of comm_tm tokens x comm_tn columns; atomic scatter:
   // one task per compute tile
@@ -1182,8 +1189,12 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
       __syncthreads();   // sm.task is rewritten by the next claim
       if (idx >= tps) break;
       if (s > cs.ready) {
+        // a task's metadata needs the inverse map only: once that is
+        // acquired, it loads while the task's split is still computing
+        if (a.mode == 0 && cs.inv_acq) ensure_task_meta(sm, a, idx, cs);
         if (W_comp > 0 && !wait_flags(sm, a.tile_flags + (long long)s * W_comp, W_comp, a)) return;
         cs.ready = s;
+        cs.inv_acq = true;   // that acquire covered the inverse map as well
       }
       run_task(sm, a, W_comp, tps, s, idx, cs, t_wait, now_100mhz());
     }
@@ -1296,7 +1307,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
   }
   // consumers, and role-switch workgroups after their tiles (one call site,
   // so that the loop is inlined)
-  Consumer cs = {-1, 0, -1, false};
+  Consumer cs = {-1, 0, -1, false, false};
   consumer_loop(sm, a, W_comp, cs);
 }
 
