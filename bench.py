@@ -20,6 +20,7 @@ Also measured, in the same run:
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -393,13 +394,22 @@ def main():
     st = dw.ws.status()
     assert st == 0, B.strerror(st)
 
-    # selector cost on the host (pure C++, no HIP calls)
+    # selector cost on the host (pure C++, no HIP calls), 10^5 calls through
+    # ctypes; the same loop around a call that does nothing (the ABI version)
+    # gives the ctypes overhead, which the net figure leaves out
     params = B.launch_params(dw.wl)
-    nsel = 20000
+    L_ = B.lib()
+    nsel = 100000
+    sel_fn, nop_fn = L_.moe_select_partition, L_.moe_gemm2_abi_version
+    wl_ref, p_ref = ctypes.byref(dw.wl), ctypes.byref(params)
     t0 = time.perf_counter()
     for _ in range(nsel):
-        B.lib().moe_select_partition(dw.wl, params, None)
+        sel_fn(wl_ref, p_ref, None)
     sel_us = (time.perf_counter() - t0) / nsel * 1e6
+    t0 = time.perf_counter()
+    for _ in range(nsel):
+        nop_fn()
+    nop_us = (time.perf_counter() - t0) / nsel * 1e6
 
     log(f"timing {args.steps} steps, C={C_used}")
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -492,6 +502,7 @@ def main():
         "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "consumers": C_used,
         "selector_us": round(sel_us, 3),
+        "selector_us_net_of_ctypes": round(max(sel_us - nop_us, 0.0), 3),
         "gemm_portion": {k: round(v, 3) for k, v in gemm_portion.items()},
         "combine": {k: round(v, 3) for k, v in combine.items()} if combine else None,
         "scatter_mode": scatter,
