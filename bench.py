@@ -120,10 +120,19 @@ class DevWorkload:
         return used, tiles, tasks
 
 
-def breakdown(dw, C, mode=None):
+def breakdown(dw, C, mode=None, reps=5):
+    """GEMM portion and combine from traced launches: the launch with the
+    median GEMM span out of `reps` (each after a short pause, so that one
+    launch's clock state does not decide the figure)."""
     w = dw.w
     flops, gemm_bytes, combine_bytes, _ = algorithmic(w)
-    used, tiles, tasks = dw.trace(C, mode)
+    runs = []
+    for _ in range(reps):
+        time.sleep(0.05)
+        used, tiles, tasks = dw.trace(C, mode)
+        runs.append((tiles[:, 3].max() - tiles[:, 0].min(), used, tiles, tasks))
+    runs.sort(key=lambda r: r[0])
+    _, used, tiles, tasks = runs[len(runs) // 2]
     if mode == 1:   # Y read, ids and gates, one fp32 atomic per routed element, zeroing
         combine_bytes = w.Mtot * w.H * 2 + w.Mtot * 8 + w.Mtot * w.H * 4 + w.T * w.H * 4
     gemm_span = (tiles[:, 3].max() - tiles[:, 0].min()) * TICK_S
