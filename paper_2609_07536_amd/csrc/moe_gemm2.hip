@@ -149,7 +149,7 @@ struct Smem {
   int start[kMaxE];           // sanitized first row of each expert
   int count[kMaxE];           // sanitized row count of each expert
   int tile_prefix[kMaxE + 1]; // exclusive prefix of ceil(count/kBM)
-  int scan[kThreads];
+  int scan[kThreads / 64];   // per-wave totals of the expert scan
   int rowtok[kBM];            // gathering stages: token of each row of the staged tile
   int flag;
   int task;                   // consumer task claimed by the workgroup
@@ -254,8 +254,14 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
 template <class Args>
 __device__ void load_experts(Smem& sm, const Args& a) {
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  // each thread takes a contiguous chunk of experts for both passes
+  const int chunk = (a.E + kThreads - 1) / kThreads;
+  const int lo = min(a.E, tid * chunk), hi = min(a.E, lo + chunk);
   bool bad = false;
-  for (int e = tid; e < a.E; e += kThreads) {
+  int local = 0;   // m-tiles of the chunk
+  for (int e = lo; e < hi; ++e) {
     long long s = a.offsets[e], en = a.offsets[e + 1];
     if (e == 0 && s != 0) bad = true;
     if (en < s || en > a.rows) bad = true;
@@ -263,29 +269,28 @@ __device__ void load_experts(Smem& sm, const Args& a) {
     en = en < s ? s : (en > a.rows ? a.rows : en);
     sm.start[e] = (int)s;
     sm.count[e] = (int)(en - s);
+    local += (int)((en - s + kBM - 1) / kBM);
   }
   if (bad && a.status)
     __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  // exclusive scan of ceil(count/kBM): each thread scans a contiguous chunk
-  const int chunk = (a.E + kThreads - 1) / kThreads;
-  const int lo = tid * chunk, hi = min(a.E, lo + chunk);
-  int local = 0;
-  for (int e = lo; e < hi; ++e) local += (sm.count[e] + kBM - 1) / kBM;
-  sm.scan[tid] = local;
-  __syncthreads();
-  for (int d = 1; d < kThreads; d <<= 1) {
-    const int v = tid >= d ? sm.scan[tid - d] : 0;
-    __syncthreads();
-    sm.scan[tid] += v;
-    __syncthreads();
+  // exclusive scan of the chunks' m-tiles: inclusive within each wave by
+  // shuffles, then the totals of the waves before (two barriers in all)
+  int v = local;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int u = __shfl_up(v, d);
+    if (lane >= d) v += u;
   }
-  int run = sm.scan[tid] - local;
+  if (lane == 63) sm.scan[wave] = v;
+  __syncthreads();
+  int before = 0;
+  for (int w = 0; w < wave; ++w) before += sm.scan[w];
+  int run = before + v - local;
   for (int e = lo; e < hi; ++e) {
     sm.tile_prefix[e] = run;
     run += (sm.count[e] + kBM - 1) / kBM;
   }
-  if (tid == kThreads - 1) sm.tile_prefix[a.E] = sm.scan[kThreads - 1];
+  if (tid == kThreads - 1) sm.tile_prefix[a.E] = before + v;
   __syncthreads();
 }
 
