@@ -195,7 +195,8 @@ int moe_gemm2_workspace_init(void* workspace, size_t workspace_bytes, void* stre
  *                   nothing from the device on the host)
  *   stream          hipStream_t the kernel is enqueued on
  * Supported shapes: H % (8 * splits) == 0, I % 8 == 0, 1 <= E <= 1024,
- * 1 <= topk <= 64, splits <= 16 (else MOE_ERR_UNSUPPORTED).
+ * 1 <= topk <= 64, splits <= 16, 2 I H < 2^31 (one expert's W2 slice
+ * within 2 GiB) (else MOE_ERR_UNSUPPORTED).
  * Values inside device arrays are checked by the kernel, which skips bad
  * entries and records MOE_ERR_BAD_ROUTING for moe_gemm2_status.
  * Returns the number of consumer workgroups launched (>= 0) or a negative
@@ -299,10 +300,11 @@ int moe_gemm1_pack_weights(const void* w_gate_up, void* w1_packed, int32_t E, in
  *                   counts, when given, must sum to rows)
  *   workspace       a moe_gemm2 workspace (at least 512 bytes, 256-byte
  *                   aligned, zeroed once by moe_gemm2_workspace_init): only
- *                   its status word and zero block are used
+ *                   its status word is used
  * One persistent launch, every workgroup computing 256 x 256 tiles of the
  * packed columns.  Supported: H % 8 == 0, I % 16 == 0, 1 <= E <= 1024,
- * 1 <= topk <= 64 (else MOE_ERR_UNSUPPORTED).  Returns 0 or a negative
+ * 1 <= topk <= 64, 2 T H < 2^31 and 4 H I < 2^31 (hidden and one expert's
+ * W1 slice within 2 GiB) (else MOE_ERR_UNSUPPORTED).  Returns 0 or a negative
  * status (host-side validation and launch errors). */
 int moe_gemm1_swiglu(const void* hidden, const void* w1, const int32_t* expert_offsets,
                      const int32_t* token_ids, void* x_perm, const moe_workload_t* wl,

@@ -50,11 +50,10 @@ constexpr int kMaxSplits = 16;
 constexpr int kMaxTopk = 64;
 constexpr int kMaxGrid = 4096;
 
-constexpr size_t kZeroBlock = 128;
 // Y rows are padded by 128 bytes: with a power-of-two pitch (H = 2048: 4 KB)
 // the rows of a tile fall on few memory channels, which cost ~18% of the
 // write bandwidth of row-strided stores in a microbenchmark.
-constexpr int kYPad = 64;     // offset of the zero block in the status region
+constexpr int kYPad = 64;     // Y row padding, elements
 constexpr uint32_t kStBadRouting = 1u;
 constexpr uint32_t kStTimeout = 2u;
 
@@ -95,7 +94,6 @@ struct KArgs {
   int tasks_per_split;
   u64* epoch_word;            // the workspace's last completed launch epoch
   uint32_t* done_ctr;         // workgroups of this launch that have finished
-  const uint16_t* zeros;      // 16+ zero bytes (operand chunks past the reduction)
   uint32_t* task_ctr;         // [kMaxSplits]: next consumer task of each split (reset by
                               // workgroup 0 each launch)
   int mode;                   // 0 owner-write, 1 fp32 atomic scatter
@@ -111,7 +109,6 @@ struct G1Args {
   const int32_t* token_ids;   // [rows]
   uint16_t* xout;             // [rows, I] bf16
   uint32_t* status;           // [1]
-  const uint16_t* zeros;      // 16+ zero bytes
   long long rows;             // capacity of token_ids / xout
   int T, H, I, E;
   int ntps;                   // n-tiles of the packed 2I columns
@@ -119,26 +116,37 @@ struct G1Args {
 };
 
 // The grouped GEMM core below serves two stages through these accessors:
-// its reduction length, the row length of its B operand, B of expert e, the
-// A row of a routed row, and the zero block for chunks past the reduction.
+// its reduction length, the row length of its B operand, B of expert e, and
+// where the A rows of a tile live: the base its loads address, the bytes
+// readable from there, and the byte offset of the tile's row `row`.
 __device__ __forceinline__ int gemm_k(const KArgs& a) { return a.I; }
 __device__ __forceinline__ int gemm_ldb(const KArgs& a) { return a.H; }
 __device__ __forceinline__ const uint16_t* gemm_b(const KArgs& a, int e) {
   return a.w2 + (size_t)e * a.I * a.H;
 }
-__device__ __forceinline__ const uint16_t* gemm_a_row(const int* rowtok, const KArgs& a, long long r0,
-                                                     int row) {
-  return a.x + (size_t)(r0 + row) * a.I;
+__device__ __forceinline__ const uint16_t* gemm_a_base(const KArgs& a, long long r0) {
+  return a.x + (size_t)r0 * a.I;
+}
+__device__ __forceinline__ long long gemm_a_bytes(const KArgs& a, long long r0) {
+  return (a.rows - r0) * a.I * 2;
+}
+__device__ __forceinline__ uint32_t gemm_a_off(const int* rowtok, const KArgs& a, int row) {
+  return (uint32_t)row * (uint32_t)a.I * 2u;
 }
 __device__ __forceinline__ int gemm_k(const G1Args& a) { return a.H; }
 __device__ __forceinline__ int gemm_ldb(const G1Args& a) { return 2 * a.I; }
 __device__ __forceinline__ const uint16_t* gemm_b(const G1Args& a, int e) {
   return a.w1 + (size_t)e * a.H * (2 * a.I);
 }
-// the gathered token of the tile's row `row`, staged in LDS
-__device__ __forceinline__ const uint16_t* gemm_a_row(const int* rowtok, const G1Args& a, long long r0,
-                                                     int row) {
-  return a.hidden + (size_t)rowtok[row] * a.H;
+// the A rows are gathered: row `row` is hidden[token], the token staged in LDS
+__device__ __forceinline__ const uint16_t* gemm_a_base(const G1Args& a, long long r0) {
+  return a.hidden;
+}
+__device__ __forceinline__ long long gemm_a_bytes(const G1Args& a, long long r0) {
+  return (long long)a.T * a.H * 2;
+}
+__device__ __forceinline__ uint32_t gemm_a_off(const int* rowtok, const G1Args& a, int row) {
+  return (uint32_t)rowtok[row] * (uint32_t)a.H * 2u;
 }
 template <class Args> struct RowGather { static constexpr bool on = false; };
 template <> struct RowGather<G1Args> { static constexpr bool on = true; };
@@ -400,14 +408,35 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-// One 16-byte-per-lane global -> LDS load: lane L's 16 bytes land at
-// lds_base + 16 L.  Issued as asm so the compiler does not serialise later
-// LDS reads behind it; completion is tracked with explicit vmcnt waits.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+// One 16-byte-per-lane buffer -> LDS load: lane L's 16 bytes, at byte
+// offset voff of the buffer rsrc describes, land at lds_base + 16 L; an
+// offset at or past the buffer's extent reads zeros.  Issued as asm so the
+// compiler does not serialise later LDS reads behind it; completion is
+// tracked with explicit vmcnt waits.  (Buffer addressing, a 32-bit offset
+// per lane against a base in scalar registers, keeps the texture
+// addresser's work per load lower than 64-bit global addresses: measured,
+// the same ring with global_load_lds_dwordx4 spends up to a third more
+// time per stage.)
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void dma16(i32x4 rsrc, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
-               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(g)
+               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc)
                : "memory", "m0");
+}
+
+// A raw buffer resource: base address, no stride, `bytes` readable (at most
+// 2^31 - 1, so that kOutOfRange is always past it), wave-uniform.
+constexpr uint32_t kOutOfRange = 0x80000000u;
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, long long bytes) {
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  const long long n = bytes < 0 ? 0 : (bytes > 0x7fffffffLL ? 0x7fffffffLL : bytes);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+  r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)((b >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)n);
+  r[3] = 0x00020000;   // raw 32-bit data format (gfx9 family)
+  return r;
 }
 
 // Stores issued as asm, like the ring loads: the compiler then does not
@@ -447,8 +476,9 @@ __device__ __forceinline__ void block_barrier() {
 }
 
 struct TileCtx {
-  const uint16_t* xg[kLoadsPerOperand];   // this lane's x row for its loads (k offset 0)
-  const uint16_t* wgp[kLoadsPerOperand];  // this lane's W2 column for its loads (k offset 0)
+  i32x4 ra, rb;                           // buffers of the tile's A rows and B columns
+  uint32_t xo[kLoadsPerOperand];          // this lane's A chunk for its loads (bytes, k offset 0)
+  uint32_t wo[kLoadsPerOperand];          // this lane's B chunk for its loads (bytes, k offset 0)
   int xk[kLoadsPerOperand];               // k offset of the chunk each x load fetches
   int wk[kLoadsPerOperand];               // k row (within a stage) each W2 load fetches
   uint32_t lds_a, lds_b;                  // LDS addresses of stage 0
@@ -457,7 +487,7 @@ struct TileCtx {
 // Issue load q (q < kLoadsPerOperand) of each operand of reduction stage kt
 // into ring slot `slot`.  Every load is issued, so each stage adds exactly
 // kLoadsPerStage to vmcnt; lanes whose chunk lies past the reduction
-// (k >= I) load 16 zero bytes from the workspace instead, which zeroes both
+// (k >= I) read past the buffer's extent, which loads zeros into both
 // operands there.
 template <class Args>
 __device__ __forceinline__ void issue_load(const Args& a, const TileCtx& t, int kt, int slot,
@@ -465,9 +495,10 @@ __device__ __forceinline__ void issue_load(const Args& a, const TileCtx& t, int 
   const int k0 = kt * kBK;
   const uint32_t blk = (uint32_t)(slot * kStageElems + (kLoadsPerOperand * wave + q) * 512) * 2;
   const int kx = k0 + t.xk[q];
-  dma16(kx < gemm_k(a) ? t.xg[q] + kx : a.zeros, t.lds_a + blk);
+  dma16(t.ra, kx < gemm_k(a) ? t.xo[q] + 2u * (uint32_t)k0 : kOutOfRange, t.lds_a + blk);
   const int kw = k0 + t.wk[q];
-  dma16(kw < gemm_k(a) ? t.wgp[q] + (size_t)kw * gemm_ldb(a) : a.zeros, t.lds_b + blk);
+  dma16(t.rb, kw < gemm_k(a) ? t.wo[q] + 2u * (uint32_t)k0 * (uint32_t)gemm_ldb(a) : kOutOfRange,
+        t.lds_b + blk);
 }
 
 template <class Args>
@@ -584,7 +615,9 @@ __device__ __forceinline__ TileCtx make_ctx(Smem& sm, const Args& a, const TileI
   t.lds_a = lds_addr(&sm.a[0][0]);
   t.lds_b = lds_addr(&sm.b[0][0]);
   {
-    const uint16_t* w2e = gemm_b(a, e) + n0;
+    const int ldb = gemm_ldb(a);
+    t.ra = buffer_rsrc(gemm_a_base(a, r0), gemm_a_bytes(a, r0));
+    t.rb = buffer_rsrc(gemm_b(a, e) + n0, ((long long)gemm_k(a) * ldb - n0) * 2);
 #pragma unroll
     for (int q = 0; q < kLoadsPerOperand; ++q) {
       const int i = kLoadsPerOperand * wave + q;   // 1 KB block of the stage
@@ -592,14 +625,14 @@ __device__ __forceinline__ TileCtx make_ctx(Smem& sm, const Args& a, const TileI
       const int row = kXRowsPerLoad * i + lane / kXChunks;
       const int lc = (lane % kXChunks) ^ ((row / kXRowsPerLine) % kXChunks);
       const int grow = row < rows_valid ? row : rows_valid - 1;   // rows past the expert: unused
-      t.xg[q] = gemm_a_row(sm.rowtok, a, r0, grow);
       t.xk[q] = 8 * lc;
+      t.xo[q] = gemm_a_off(sm.rowtok, a, grow) + 2u * (uint32_t)t.xk[q];
       // W2: rows 2i + L/32, physical chunk L%32
       const int krow = 2 * i + (lane >> 5);
       const int wc = (lane & 31) ^ (4 * (krow & 3));
       const int n = 8 * wc < cols_valid ? 8 * wc : 0;               // columns past the tile: unused
-      t.wgp[q] = w2e + n;
       t.wk[q] = krow;
+      t.wo[q] = 2u * (uint32_t)n + 2u * (uint32_t)krow * (uint32_t)ldb;
     }
   }
   return t;
@@ -1399,6 +1432,8 @@ int check_shape(const moe_workload_t* wl) {
     return MOE_ERR_INVALID_ARG;
   if (wl->E > kMaxE || wl->topk > kMaxTopk || wl->splits > kMaxSplits) return MOE_ERR_UNSUPPORTED;
   if (wl->I % 8 != 0 || wl->H % (8 * wl->splits) != 0) return MOE_ERR_UNSUPPORTED;
+  // an expert's W2 slice is addressed with 32-bit byte offsets
+  if ((long long)wl->I * wl->H * 2 > 0x7fffffffLL) return MOE_ERR_UNSUPPORTED;
   const long long rows = wl->rows > 0 ? wl->rows : (long long)wl->T * wl->topk;
   if (rows > (long long)INT32_MAX || (long long)wl->T * wl->topk > (long long)INT32_MAX)
     return MOE_ERR_UNSUPPORTED;
@@ -1429,8 +1464,8 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->tasks_per_split = ((wl->T + L->comm_tm - 1) / L->comm_tm) * L->cb_per_split;
   L->max_tiles = (long long)wl->splits * L->ntps * ((L->rows + kBM - 1) / kBM + wl->E);
   size_t off = 0;
-  L->status = off;   // word 0: status bits; bytes kZeroBlock..255: zeros, never
-                     // written; 256..319: per-split consumer task counters;
+  L->status = off;   // word 0: status bits; bytes 4..255: reserved;
+                     // 256..319: per-split consumer task counters;
                      // 320: launch epoch (u64); 328: finished workgroups
   off += 512;
   L->wg_flags = off;
@@ -1625,7 +1660,6 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.tok_cnt = reinterpret_cast<u64*>(ws + L.tok_cnt);
   a.inv = reinterpret_cast<int32_t*>(ws + L.inv);
   a.status = reinterpret_cast<uint32_t*>(ws + L.status);
-  a.zeros = reinterpret_cast<const uint16_t*>(ws + L.status + kZeroBlock);
   a.task_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 256);
   a.trace = reinterpret_cast<u64*>(trace);
   a.rows = L.rows;
@@ -1774,7 +1808,9 @@ int check_gemm1_shape(const moe_workload_t* wl) {
   if (wl->E > kMaxE || wl->topk > kMaxTopk) return MOE_ERR_UNSUPPORTED;
   if (wl->H % 8 != 0 || wl->I % 16 != 0) return MOE_ERR_UNSUPPORTED;
   const long long rows = wl->rows > 0 ? wl->rows : (long long)wl->T * wl->topk;
-  if (rows > (long long)INT32_MAX || (long long)wl->T * wl->H > (long long)INT64_MAX / 4)
+  if (rows > (long long)INT32_MAX) return MOE_ERR_UNSUPPORTED;
+  // hidden and an expert's W1 slice are addressed with 32-bit byte offsets
+  if ((long long)wl->T * wl->H * 2 > 0x7fffffffLL || (long long)wl->H * wl->I * 4 > 0x7fffffffLL)
     return MOE_ERR_UNSUPPORTED;
   const long long ntps = (2LL * wl->I + kBN - 1) / kBN;
   if ((long long)wl->E * ((rows + kBM - 1) / kBM + 1) * ntps > (long long)INT32_MAX / 2)
@@ -1818,7 +1854,6 @@ int launch_gemm1(const void* hidden, const void* w1, const int32_t* expert_offse
   a.token_ids = token_ids;
   a.xout = static_cast<uint16_t*>(x_perm);
   a.status = reinterpret_cast<uint32_t*>(ws);
-  a.zeros = reinterpret_cast<const uint16_t*>(ws + kZeroBlock);
   a.rows = rows;
   a.T = wl->T;
   a.H = wl->H;
