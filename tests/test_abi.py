@@ -232,6 +232,25 @@ def test_trace_size_counts_the_adaptive_consumer_tasks(T, H, L, tm):
     assert B.trace_size(wl) == 8 * (4 * max_tiles + 4 * max(tasks, max_tiles))
 
 
+def test_32bit_offset_limits():
+    """The ring loads address one expert's weight slice (and, in the
+    up-projection, hidden) with 32-bit byte offsets, so shapes past 2 GiB
+    there are refused on the host, and the largest ones below are taken."""
+    over, _ = B.make_workload(T=256, H=16384, I=65536, E=2, topk=1, splits=1)   # 2 I H = 2^31
+    assert B.workspace_size(over) == 0
+    assert B.layer_workspace_size(over) == 0
+    edge, _ = B.make_workload(T=256, H=16384, I=65528, E=2, topk=1, splits=1)   # 2^31 - 2^18
+    assert B.workspace_size(edge) > 0
+    hid, _ = B.make_workload(T=65536, H=16384, I=64, E=2, topk=1, splits=1)     # 2 T H = 2^31
+    assert B.workspace_size(hid) > 0          # the down-projection stage does not read hidden
+    assert B.layer_workspace_size(hid) == 0
+    w1, _ = B.make_workload(T=256, H=16384, I=32768, E=2, topk=1, splits=1)     # 4 H I = 2^31
+    assert B.workspace_size(w1) > 0
+    assert B.layer_workspace_size(w1) == 0
+    ok, _ = B.make_workload(T=256, H=16384, I=32752, E=2, topk=1, splits=1)
+    assert B.layer_workspace_size(ok) > 0
+
+
 def test_workspace_size_grows_with_rows():
     a, _ = B.make_workload(T=1024, H=2048, I=704, E=32, topk=6, splits=2)
     b, _ = B.make_workload(T=2048, H=2048, I=704, E=32, topk=6, splits=2)
