@@ -624,15 +624,18 @@ __device__ __forceinline__ TileCtx make_ctx(Smem& sm, const Args& a, const TileI
       // x: rows kXRowsPerLoad i + L / kXChunks, physical chunk L % kXChunks
       const int row = kXRowsPerLoad * i + lane / kXChunks;
       const int lc = (lane % kXChunks) ^ ((row / kXRowsPerLine) % kXChunks);
-      const int grow = row < rows_valid ? row : rows_valid - 1;   // rows past the expert: unused
+      // rows past the expert and columns past the tile are never stored:
+      // their loads take an offset past the buffer (zeros, no memory request)
+      const int grow = row < rows_valid ? row : rows_valid - 1;
       t.xk[q] = 8 * lc;
-      t.xo[q] = gemm_a_off(sm.rowtok, a, grow) + 2u * (uint32_t)t.xk[q];
+      t.xo[q] = row < rows_valid ? gemm_a_off(sm.rowtok, a, grow) + 2u * (uint32_t)t.xk[q]
+                                 : kOutOfRange;
       // W2: rows 2i + L/32, physical chunk L%32
       const int krow = 2 * i + (lane >> 5);
       const int wc = (lane & 31) ^ (4 * (krow & 3));
-      const int n = 8 * wc < cols_valid ? 8 * wc : 0;               // columns past the tile: unused
       t.wk[q] = krow;
-      t.wo[q] = 2u * (uint32_t)n + 2u * (uint32_t)krow * (uint32_t)ldb;
+      t.wo[q] = 8 * wc < cols_valid ? 16u * (uint32_t)wc + 2u * (uint32_t)krow * (uint32_t)ldb
+                                    : kOutOfRange;
     }
   }
   return t;
