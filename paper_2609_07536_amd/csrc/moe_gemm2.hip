@@ -366,7 +366,7 @@ __device__ void consumer_prologue(const Smem& sm, const KArgs& a, long long rows
 // while the other waits for its LDS fragments, and the wave tile keeps the
 // costly transposing reads (W2) at one 16 KB pass per K=16 step per CU.
 //
-// Operands reach LDS by direct global->LDS loads (no registers) through a
+// Operands reach LDS by direct buffer->LDS loads (no registers) through a
 // ring of kStages stages of kBK reduction steps, kStages - 1 stages ahead of
 // the MFMAs:
 //  * x stage: 256 rows of 2 kBK bytes (kBK/8 chunks of 8 k); chunk c of row
