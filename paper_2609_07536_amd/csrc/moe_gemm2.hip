@@ -508,6 +508,31 @@ __device__ __forceinline__ void issue_stage(const Args& a, const TileCtx& t, int
   for (int q = 0; q < kLoadsPerOperand; ++q) issue_load(a, t, kt, slot, wave, q);
 }
 
+// One operand's half of a stage: the B (W2) loads, or the A (x) loads.
+template <class Args>
+__device__ __forceinline__ void issue_stage_b(const Args& a, const TileCtx& t, int kt, int slot,
+                                              int wave) {
+  const int k0 = kt * kBK;
+#pragma unroll
+  for (int q = 0; q < kLoadsPerOperand; ++q) {
+    const uint32_t blk = (uint32_t)(slot * kStageElems + (kLoadsPerOperand * wave + q) * 512) * 2;
+    const int kw = k0 + t.wk[q];
+    dma16(t.rb, kw < gemm_k(a) ? t.wo[q] + 2u * (uint32_t)k0 * (uint32_t)gemm_ldb(a) : kOutOfRange,
+          t.lds_b + blk);
+  }
+}
+template <class Args>
+__device__ __forceinline__ void issue_stage_a(const Args& a, const TileCtx& t, int kt, int slot,
+                                              int wave) {
+  const int k0 = kt * kBK;
+#pragma unroll
+  for (int q = 0; q < kLoadsPerOperand; ++q) {
+    const uint32_t blk = (uint32_t)(slot * kStageElems + (kLoadsPerOperand * wave + q) * 512) * 2;
+    const int kx = k0 + t.xk[q];
+    dma16(t.ra, kx < gemm_k(a) ? t.xo[q] + 2u * (uint32_t)k0 : kOutOfRange, t.lds_a + blk);
+  }
+}
+
 typedef const __attribute__((address_space(3))) uint16_t lds_u16;
 
 // MFMA operands of K=16 step ks of a ring slot: W2^T blocks by two
@@ -681,33 +706,31 @@ __device__ __forceinline__ void epilogue_store(Smem& sm, const KArgs& a, f32x16 
                                                int eslot, int lane, int wave, int wn0, int wm0,
                                                const TileInfo& ti) {
   const int rows_valid = ti.rows_valid, cols_valid = ti.cols_valid, r0 = ti.r0, n0 = ti.n0;
-  // The wave's kWM x kWN block goes through LDS in two halves of
-  // 64 rows (8 KB per wave, in slot eslot) as bf16 rows of 2 kWN bytes, 16-byte
-  // chunk j of row r at chunk j ^ ((r / r1) % c), c = chunks per row,
-  // r1 = rows per 256-byte bank line (so 16 consecutive rows hit 16 distinct
-  // bank groups), then leaves as whole rows of 2 kWN bytes (full 128-byte
-  // lines).  A wave's LDS operations run in order, so the second half may
-  // overwrite the first once its reads were issued.
+  // The wave's kWM x kWN block goes through LDS one 32-row m-block at a
+  // time (4 KB per wave, all eight in the x part of slot eslot, so that its
+  // W2 part can take the next tile's stage already) as bf16 rows of 2 kWN
+  // bytes, 16-byte chunk j of row r at chunk j ^ ((r / r1) % c), c = chunks
+  // per row, r1 = rows per 256-byte bank line (so 16 consecutive rows hit
+  // 16 distinct bank groups), then leaves as whole rows of 2 kWN bytes (full
+  // 128-byte lines).  A wave's LDS operations run in order, so each pass may
+  // overwrite the previous one once its reads were issued.
   constexpr int kEpChunks = kWN / 8;
   constexpr int kEpRowsPerLine = 256 / (2 * kWN);
   constexpr int kEpRowsPerStore = 64 / kEpChunks;
-  constexpr int kEpRows = 64;                       // rows per half
-  static_assert(kWaves == 8 && kEpRows * kWN * 4 <= kStageElems,
-                "the epilogue halves of four waves fit in one operand's part of a slot");
+  constexpr int kEpRows = 32;                       // rows per pass: one m-block
+  static_assert(kWaves * kEpRows * kWN <= kStageElems,
+                "one pass of every wave fits in the x part of a slot");
   const int h = lane >> 5;
   __attribute__((address_space(3))) uint16_t* ep =
-      (__attribute__((address_space(3))) uint16_t*)(uintptr_t)(wave < 4 ? lds_addr(&sm.a[eslot][0])
-                                                                         : lds_addr(&sm.b[eslot][0])) +
-      (wave & 3) * (kEpRows * kWN);
+      (__attribute__((address_space(3))) uint16_t*)(uintptr_t)lds_addr(&sm.a[eslot][0]) +
+      wave * (kEpRows * kWN);
   const int j = lane % kEpChunks;
   const int n = wn0 + 8 * j;
   const bool n_ok = n < cols_valid;
 #pragma unroll
-  for (int half = 0; half < kMB / 2; ++half) {
-#pragma unroll
-    for (int mh = 0; mh < 2; ++mh) {
-      const int mb = 2 * half + mh;
-      const int row = 32 * mh + (lane & 31);
+  for (int mb = 0; mb < kMB; ++mb) {
+    {
+      const int row = lane & 31;
       const int sw = (row / kEpRowsPerLine) % kEpChunks;
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb)
@@ -720,10 +743,10 @@ __device__ __forceinline__ void epilogue_store(Smem& sm, const KArgs& a, f32x16 
           *(__attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((chunk ^ sw) << 3)) = v;
         }
     }
-#pragma unroll 4
+#pragma unroll
     for (int it = 0; it < kEpRows / kEpRowsPerStore; ++it) {
       const int row = kEpRowsPerStore * it + lane / kEpChunks;
-      const int m = wm0 + kEpRows * half + row;
+      const int m = wm0 + kEpRows * mb + row;
       const int sw = (row / kEpRowsPerLine) % kEpChunks;
       const bf16x8 v =
           *(const __attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((j ^ sw) << 3));
@@ -903,12 +926,20 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
   // into the other slot now, ahead of the Y stores
   if (next && nk == 1) issue_stage(a, make_ctx(sm, a, nt, wave), 0, slot_of(nk), wave);
 
+  // The down-projection's epilogue uses only the x part of the slot, so the
+  // W2 half of the next tile's stage 1 loads during it.
+  constexpr bool kEarlyB = !RowGather<Args>::on;
+  const bool stage1_now = next && nk >= 2 && !defer_stage1;
+  if (kEarlyB && stage1_now) issue_stage_b(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
   epilogue_store(sm, a, acc, eslot, lane, wave, wn0, wm0, ti);
-  if (next && nk >= 2 && !defer_stage1) {
+  if (stage1_now) {
     // every wave has read its block back (its stores carry the data), so
-    // the slot may take the next tile's stage 1
+    // the slot may take the rest of the next tile's stage 1
     block_barrier();
-    issue_stage(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
+    if (kEarlyB)
+      issue_stage_a(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
+    else
+      issue_stage(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
   }
   t_mid[1] = now_100mhz();
 }
