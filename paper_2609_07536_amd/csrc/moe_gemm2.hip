@@ -1241,9 +1241,13 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
   // still running there), so there is one per split: the inverse map's
   // flags are acquired together with the first split's, before any read.
   if (!cs.inv_ok) {
-    if (!wait_flags(sm, a.wg_flags, gridDim.x, a, W_comp == 0)) return;
+    // (acquired here when the split's own acquire would come too late for
+    // the metadata: no tiles, or a single split, whose inverse map is
+    // published at the start)
+    const bool acq = W_comp == 0 || a.L == 1;
+    if (!wait_flags(sm, a.wg_flags, gridDim.x, a, acq)) return;
     cs.inv_ok = true;
-    cs.inv_acq = W_comp == 0;
+    cs.inv_acq = acq;
   }
   // owner-write: tasks of comm_tm tokens x comm_tn columns; atomic scatter:
   // one task per compute tile
@@ -1298,7 +1302,11 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
   const int g_first = b >= a.C && c < total ? c : -1;
   // A compute workgroup with a tile in split 0 publishes its share of the
   // inverse map with that split (consumers read it only after a split).
-  const bool defer_inverse = g_first >= 0 && g_first < W_comp && total <= a.max_tiles;
+  // With a single split that publish comes only at the end of the tiles, so
+  // the share is published at once instead: the consumers then stage their
+  // first task's metadata while the split is still computing.
+  const bool defer_inverse =
+      a.L > 1 && g_first >= 0 && g_first < W_comp && total <= a.max_tiles;
   auto decode = [&](int g) { return decode_tile(sm, a, W_comp, g); };
   const int nk = (a.I + kBK - 1) / kBK;
   // A compute workgroup issues its first tile's ring fill before building
