@@ -929,8 +929,10 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
   // The down-projection's epilogue uses only the x part of the slot, so the
   // W2 half of the next tile's stage 1 loads during it.
   constexpr bool kEarlyB = !RowGather<Args>::on;
+  // (Also before a split's publish: those loads are older than the Y
+  // stores, so the publish's wait for the stores covers them at no cost.)
   const bool stage1_now = next && nk >= 2 && !defer_stage1;
-  if (kEarlyB && stage1_now) issue_stage_b(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
+  if (kEarlyB && next && nk >= 2) issue_stage_b(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
   epilogue_store(sm, a, acc, eslot, lane, wave, wn0, wm0, ti);
   if (stage1_now) {
     // every wave has read its block back (its stores carry the data), so
@@ -944,12 +946,12 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
   t_mid[1] = now_100mhz();
 }
 
-// The next tile's stage 1 into its slot, when the tile before deferred it
-// (after every wave has read its epilogue block back).
-template <class Args>
-__device__ __forceinline__ void issue_stage1(Smem& sm, const Args& a, const TileInfo& nt, int base) {
+// The x half of the next tile's stage 1 into its slot, when the tile
+// before deferred it past its split's publish (after every wave has read
+// its epilogue block back); the W2 half went in before the epilogue.
+__device__ __forceinline__ void issue_stage1_a(Smem& sm, const KArgs& a, const TileInfo& nt, int base) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  issue_stage(a, make_ctx(sm, a, nt, wave), 1, (base + 1) % kStages, wave);
+  issue_stage_a(a, make_ctx(sm, a, nt, wave), 1, (base + 1) % kStages, wave);
 }
 
 // ---- consumer role: one task --------------------------------------------------
@@ -1339,8 +1341,9 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       const u64 t_start = now_100mhz();
       u64 t_mid[2];
       const bool last_of_split = !next || g_next / W_comp != g / W_comp;
-      // A split's last tile holds its next tile's stage 1 back until the
-      // publish, so that the publish's waits cover the Y stores only.
+      // A split's last tile holds the x half of its next tile's stage 1
+      // back until the publish, so that the publish's waits cover nothing
+      // issued after the Y stores.
       compute_tile(sm, a, cur, filled, next, nt, base, t_mid, last_of_split);
       base = (base + nk) % kStages;   // the next tile's stages follow this tile's
       // Publish once per split: consumers wait for whole splits, so the tiles
@@ -1352,7 +1355,8 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       // orders those waits before thread 0, whose release fence writes back
       // the L2 before it stores the flags.
       if (last_of_split) {
-        // only the next tile's stage 0 (older) and the Y stores are in flight
+        // only the next tile's stage 0 and stage-1 W2 half (older) and the
+        // Y stores are in flight
         waitcnt_vm<0>();
         __syncthreads();
         if (threadIdx.x == 0) {
@@ -1369,7 +1373,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
         // since) at the next tile's start, on every tile
         waitcnt_vm<0>();
         split_first = g_next;
-        if (next && nk >= 2) issue_stage1(sm, a, nt, base);
+        if (next && nk >= 2) issue_stage1_a(sm, a, nt, base);
       }
       if (a.trace && threadIdx.x == 0) {
         store8(&a.trace[4 * g + 0], t_start);
