@@ -115,6 +115,39 @@ def test_edge_shapes(gpu_lib, case):
         _check(got, ref, f"{name} C={used}")
 
 
+def _random_cases(n=16, seed=2026):
+    """Seeded random shapes across the supported range: ragged rows, a
+    reduction that is not a multiple of the 64-deep stage, column counts
+    that are not a multiple of the 256-wide tile, 1..4 splits."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        L = int(rng.choice([1, 2, 4]))
+        H = 8 * L * int(rng.integers(1, 1 + 1024 // (8 * L)))
+        I = 8 * int(rng.integers(1, 41))
+        E = int(rng.integers(1, 41))
+        k = int(rng.integers(1, min(E, 8) + 1))
+        T = int(rng.integers(1, 700))
+        routing = ("uniform",) if i % 2 == 0 else ("zipf", float(rng.choice([0.8, 1.2])))
+        cases.append((f"r{i}_T{T}_H{H}_I{I}_E{E}_k{k}_L{L}", T, H, I, E, k, L, routing))
+    return cases
+
+
+RANDOM = _random_cases()
+
+
+@pytest.mark.parametrize("case", RANDOM, ids=[c[0] for c in RANDOM])
+def test_random_shapes(gpu_lib, case):
+    """The selector's pick and the role switch on seeded random shapes."""
+    import gpu_util
+    name, T, H, I, E, k, L, routing = case
+    w = custom(T=T, H=H, I=I, E=E, topk=k, L=L, routing=routing, seed=5)
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+    for C in (-1, 0, 3):
+        got, used, _ = gpu_util.run(w, C=C)
+        _check(got, ref, f"{name} C={used}")
+
+
 def test_dropped_slots_and_empty_experts(gpu_lib):
     import gpu_util
     rng = np.random.default_rng(3)
