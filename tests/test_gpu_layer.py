@@ -147,6 +147,31 @@ def test_layer_edge_shapes(gpu_lib, case):
         _check_bar(out.cpu().numpy(), ref, f"{name} layer C={used}")
 
 
+def _random_layer_cases(n=8, seed=7):
+    """Seeded random shapes for the up-projection: H a multiple of 8, I of
+    16, ragged rows, reductions that are not a multiple of 64 and packed
+    widths 2I that are not a multiple of 256."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        H = 8 * int(rng.integers(1, 65))
+        I = 16 * int(rng.integers(1, 21))
+        E = int(rng.integers(1, 25))
+        k = int(rng.integers(1, min(E, 6) + 1))
+        T = int(rng.integers(1, 400))
+        routing = ("uniform",) if i % 2 == 0 else ("zipf", 1.0)
+        out.append((f"r{i}_T{T}_H{H}_I{I}_E{E}_k{k}", T, H, I, E, k, routing))
+    return out
+
+
+RANDOM = _random_layer_cases()
+
+
+@pytest.mark.parametrize("case", RANDOM, ids=[c[0] for c in RANDOM])
+def test_layer_random_shapes(gpu_lib, case):
+    test_layer_edge_shapes(gpu_lib, case)
+
+
 def test_layer_dropped_slots_and_bad_token_ids(gpu_lib):
     import torch
     from paper_2609_07536_amd import binding as B
