@@ -364,7 +364,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this stage runs on one GPU; multi-GPU runs are not "
-                          "part of this build (use --gpus 1)"}))
+                          "supported (use --gpus 1)"}))
         sys.exit(2)
 
     import torch
