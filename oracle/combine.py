@@ -17,7 +17,10 @@ oracle is the plain definition written out.  Arithmetic is fp32 with bf16
 inputs widened exactly; the k contributions of a token are summed in
 ascending permuted-row order.  Pins (tests/test_oracle_pins.py) tie it to a
 dense fp64 formula, to gate and permutation invariants and to a plain
-matrix product in the special cases that reduce to one.
+matrix product in the special cases that reduce to one; the bf16 widening
+and the two acceptance measures (rel_l2, max_abs_ratio) are pinned on their
+own (tests/test_oracle_numeric_pins.py: every bf16 pattern against torch's
+conversion, hand-decoded values, hand-worked arrays, planted mistakes).
 """
 from __future__ import annotations
 
