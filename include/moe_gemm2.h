@@ -192,13 +192,29 @@ int moe_gemm2_workspace_init(void* workspace, size_t workspace_bytes, void* stre
  *                   launch epoch that each launch advances on the device,
  *                   so a call captured in a HIP graph may be replayed
  *                   (with wl->host_expert_counts NULL the call reads
- *                   nothing from the device on the host)
+ *                   nothing from the device on the host).  A workspace may
+ *                   serve workloads of different dimensions in turn: the
+ *                   library remembers the layout each workspace address was
+ *                   last launched with and, when it changes, zeroes the
+ *                   workspace's metadata (the bytes before the Y staging)
+ *                   with a small kernel on stream before the launch (also
+ *                   inside a captured graph, where it then runs on every
+ *                   replay)
  *   stream          hipStream_t the kernel is enqueued on
  * Supported shapes: H % (8 * splits) == 0, I % 8 == 0, 1 <= E <= 1024,
  * 1 <= topk <= 64, splits <= 16, 2 I H < 2^31 (one expert's W2 slice
  * within 2 GiB) (else MOE_ERR_UNSUPPORTED).
  * Values inside device arrays are checked by the kernel, which skips bad
  * entries and records MOE_ERR_BAD_ROUTING for moe_gemm2_status.
+ * Launches on other streams may share the GPU: compute workgroups never
+ * wait while they hold tiles, with C = 0 a workgroup waits on other
+ * workgroups' tiles only once its whole grid has started, and dedicated
+ * consumers (C >= 1) wait only on compute workgroups, which never wait; so
+ * concurrent launches drain as long as their dedicated consumers together
+ * leave a CU free.  Every wait is bounded (MOE_GEMM2_SPIN_LIMIT polls, then
+ * MOE_ERR_TIMEOUT).  Debugging aid: MOE_GEMM2_DEBUG_PUBLISH_DELAY="m:t"
+ * makes the compute workgroups whose index is a multiple of m hold each
+ * split publish back by t ticks of the 100 MHz clock (t <= 10^6).
  * Returns the number of consumer workgroups launched (>= 0) or a negative
  * status (host-side validation and launch errors only). */
 int moe_gemm2_combine(const void* x_perm, const void* w2, const int32_t* expert_offsets,

@@ -229,6 +229,22 @@ class Workspace:
         return lib().moe_gemm2_status(ctypes.c_void_p(self.ptr), _stream(stream), int(clear))
 
 
+def _call_workspace(nbytes: int, device, stream) -> "Workspace":
+    """A workspace for one call that was given none.
+
+    It is allocated (and zeroed) on the launch's own stream: torch's caching
+    allocator then reuses its memory only for later work on that stream,
+    which runs after the launch, never while the kernel may still write
+    its flags, inverse map and Y staging.  This path allocates on every
+    call; pass a Workspace to avoid that."""
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    with torch.cuda.stream(s):
+        ws = Workspace(nbytes, device=device, stream=s)
+    ws.tensor.record_stream(s)
+    return ws
+
+
 def combine(x_perm, w2, expert_offsets, token_ids, gate_w, T: int, splits: int = 1,
             topk: Optional[int] = None, counts: Optional[Sequence[int]] = None,
             num_consumers: int = -1, out=None, workspace: Optional[Workspace] = None,
@@ -239,6 +255,8 @@ def combine(x_perm, w2, expert_offsets, token_ids, gate_w, T: int, splits: int =
 
     x_perm bf16 [rows, I], w2 bf16 [E, I, H], expert_offsets int32 [E+1],
     token_ids int32 [rows], gate_w fp32 [rows]; returns (out [T, H] fp32, C).
+    Without a (large enough) workspace, one is allocated for this call on
+    the launch's stream.
     """
     import torch
     rows, I = int(x_perm.shape[0]), int(x_perm.shape[1])
@@ -257,7 +275,7 @@ def combine(x_perm, w2, expert_offsets, token_ids, gate_w, T: int, splits: int =
     if need == 0:
         raise MoeError(MOE_ERR_UNSUPPORTED, "moe_gemm2_workspace_size")
     if workspace is None or workspace.nbytes < need:
-        workspace = Workspace(need, device=x_perm.device, stream=stream)
+        workspace = _call_workspace(need, x_perm.device, stream)
     vp = ctypes.c_void_p
     args = [vp(x_perm.data_ptr()), vp(w2.data_ptr()), vp(expert_offsets.data_ptr()),
             vp(token_ids.data_ptr()), vp(gate_w.data_ptr()), vp(out.data_ptr()),
@@ -318,7 +336,7 @@ def gemm1_swiglu(hidden, w1_packed, expert_offsets, token_ids, topk: int, rows: 
     if out is None:
         out = torch.empty((max(rows, 1), I), dtype=torch.bfloat16, device=hidden.device)
     if workspace is None:
-        workspace = Workspace(512, device=hidden.device, stream=stream)
+        workspace = _call_workspace(512, hidden.device, stream)
     vp = ctypes.c_void_p
     r = lib().moe_gemm1_swiglu(vp(hidden.data_ptr()), vp(w1_packed.data_ptr()),
                                vp(expert_offsets.data_ptr()), vp(token_ids.data_ptr()),
@@ -350,7 +368,7 @@ def layer_forward(hidden, w1_packed, w2, expert_offsets, token_ids, gate_w, topk
     if need == 0:
         raise MoeError(MOE_ERR_UNSUPPORTED, "moe_layer_workspace_size")
     if workspace is None or workspace.nbytes < need:
-        workspace = Workspace(need, device=hidden.device, stream=stream)
+        workspace = _call_workspace(need, hidden.device, stream)
     vp = ctypes.c_void_p
     r = lib().moe_layer_forward(vp(hidden.data_ptr()), vp(w1_packed.data_ptr()), vp(w2.data_ptr()),
                                 vp(expert_offsets.data_ptr()), vp(token_ids.data_ptr()),

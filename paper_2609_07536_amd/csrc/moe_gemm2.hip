@@ -19,8 +19,12 @@
 // Every workgroup first adds its share of rows to the token->rows inverse
 // map.  Flags and counters carry the launch's epoch, so nothing has to be
 // cleared between launches and a stale value can never satisfy a wait.
-// Compute workgroups never wait, so the grid drains even if consumers are
-// not all resident; every consumer wait is bounded.
+// Compute workgroups never wait while they hold tiles.  With C = 0 they
+// serve consumer tasks afterwards, and then wait on other workgroups' tiles:
+// they do so only once every workgroup of the grid has started (a started
+// counter), else they leave the tasks to the workgroups started later, so a
+// launch that shares the GPU with another never waits on workgroups that
+// cannot get a CU.  Every consumer wait is bounded.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -30,6 +34,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
+#include <unordered_map>
 
 #include "moe_gemm2.h"
 
@@ -94,6 +99,9 @@ struct KArgs {
   int tasks_per_split;
   u64* epoch_word;            // the workspace's last completed launch epoch
   uint32_t* done_ctr;         // workgroups of this launch that have finished
+  uint32_t* start_ctr;        // workgroups of this launch that have started
+  int delay_mod;              // debug: compute workgroups c % delay_mod == 0 delay
+  long long delay_ticks;      //   each split publish by delay_ticks (100 MHz), else 0
   uint32_t* task_ctr;         // [kMaxSplits]: next consumer task of each split (reset by
                               // workgroup 0 each launch)
   int mode;                   // 0 owner-write, 1 fp32 atomic scatter
@@ -1291,7 +1299,10 @@ __device__ __forceinline__ int compute_index(int b, int C, int N) {
 }
 
 __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
-  if (threadIdx.x == 0) sm.epoch = launch_epoch(a);   // load_experts synchronises
+  if (threadIdx.x == 0) {
+    sm.epoch = launch_epoch(a);   // load_experts synchronises
+    __hip_atomic_fetch_add(a.start_ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   load_experts(sm, a);
   const long long rows_dev = a.E > 0 ? (long long)sm.start[a.E - 1] + sm.count[a.E - 1] : 0;
   const int m_tiles = sm.tile_prefix[a.E];
@@ -1358,6 +1369,12 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
         // only the next tile's stage 0 and stage-1 W2 half (older) and the
         // Y stores are in flight
         waitcnt_vm<0>();
+        if (a.delay_ticks > 0 && threadIdx.x == 0 && c % a.delay_mod == 0) {
+          // debug: hold this publish back for a bounded time, so that
+          // consumers reach the split's flags long before they are set
+          const u64 until = now_100mhz() + (u64)a.delay_ticks;
+          while (now_100mhz() < until) __builtin_amdgcn_s_sleep(16);
+        }
         __syncthreads();
         if (threadIdx.x == 0) {
           __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -1386,8 +1403,19 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       g = g_next;
     }
     // after its tiles, a compute workgroup serves consumer tasks only with
-    // C = 0 (the role switch)
+    // C = 0 (the role switch), and only if every workgroup of the grid has
+    // started: the tasks wait on tiles of other workgroups, and waiting on
+    // one that has not started yet could hold a CU it needs (another launch
+    // may share the GPU).  Workgroups started later serve the tasks instead;
+    // the last one to start always sees the whole grid started.
     if (!a.drain) return;
+    if (threadIdx.x == 0)
+      sm.flag = __hip_atomic_load(a.start_ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >=
+                gridDim.x;
+    __syncthreads();
+    const bool all_started = sm.flag != 0;
+    __syncthreads();   // sm.flag is rewritten by the consumers' waits
+    if (!all_started) return;
   }
   // consumers, and role-switch workgroups after their tiles (one call site,
   // so that the loop is inlined)
@@ -1409,6 +1437,7 @@ moe_gemm2_fused(KArgs a) {
       u64 e = sm.epoch;
       if ((uint32_t)(e + 1) == 0) ++e;   // the next launch's flags must not be 0
       __hip_atomic_store(a.done_ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.start_ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(a.epoch_word, e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
@@ -1512,7 +1541,8 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   size_t off = 0;
   L->status = off;   // word 0: status bits; bytes 4..255: reserved;
                      // 256..319: per-split consumer task counters;
-                     // 320: launch epoch (u64); 328: finished workgroups
+                     // 320: launch epoch (u64); 328: finished workgroups;
+                     // 332: started workgroups
   off += 512;
   L->wg_flags = off;
   off += (size_t)kMaxGrid * 4;
@@ -1627,6 +1657,63 @@ void fill_params(const DevInfo& d, int mode, int topk, int comm_tm, moe_select_p
 
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+// A workspace's metadata regions (flags, per-token counters, inverse map)
+// sit at offsets that depend on the workload's dimensions.  Their epoch
+// tags make stale values harmless only within one layout: after a launch
+// with another layout, a region may hold what another region left (a large
+// flag word read as a per-token counter would never reopen).  So the
+// library remembers the layout each workspace was last launched with, and
+// zeroes the metadata (everything before the Y staging, a few hundred KB)
+// on the launch's stream when the layout changes.  A workspace that
+// moe_gemm2_workspace_init zeroed accepts any layout.
+constexpr uint64_t kWsZeroed = 0;
+std::mutex g_ws_mu;
+std::unordered_map<uintptr_t, uint64_t> g_ws_layout;
+
+uint64_t layout_signature(const moe_workload_t* wl, const Layout& L) {
+  uint64_t h = 1469598103934665603ull;   // FNV-1a over the fields that place or index regions
+  const long long f[] = {(long long)L.flags, (long long)L.tok_cnt, (long long)L.inv,
+                         (long long)L.Y,     wl->T,                  wl->topk,
+                         L.rows,             L.max_tiles,            wl->H};
+  for (long long v : f)
+    for (int i = 0; i < 8; ++i) {
+      h ^= (uint64_t)((v >> (8 * i)) & 0xff);
+      h *= 1099511628211ull;
+    }
+  return h | 1;   // never kWsZeroed
+}
+
+void note_workspace_zeroed(const void* ws) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  if (g_ws_layout.size() > 4096) g_ws_layout.clear();
+  g_ws_layout[(uintptr_t)ws] = kWsZeroed;
+}
+
+// True when the metadata regions must be zeroed before a launch with
+// layout `sig` (a workspace not seen before, or last used with another
+// layout); records `sig` as the workspace's layout.
+bool workspace_needs_clear(const void* ws, uint64_t sig) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  auto it = g_ws_layout.find((uintptr_t)ws);
+  if (it != g_ws_layout.end() && (it->second == sig || it->second == kWsZeroed)) {
+    it->second = sig;
+    return false;
+  }
+  if (g_ws_layout.size() > 4096) g_ws_layout.clear();
+  g_ws_layout[(uintptr_t)ws] = sig;
+  return true;
+}
+
+// Zeroes `bytes` (a multiple of 4) at p on stream with a fill kernel (no
+// memset node, so that a captured graph replays it correctly).
+hipError_t zero_async(void* p, size_t bytes, hipStream_t stream) {
+  const size_t words = bytes / 4;
+  const unsigned blocks = (unsigned)((words + 255) / 256 < 4096 ? (words + 255) / 256 : 4096);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks ? blocks : 1), dim3(256), 0, stream,
+                     static_cast<uint32_t*>(p), words);
+  return hipGetLastError();
+}
+
 int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
            const int32_t* token_ids, const float* gate_w, float* out, const moe_workload_t* wl,
            int32_t num_consumers, int32_t mode, void* workspace, size_t workspace_bytes,
@@ -1734,8 +1821,23 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.mode = mode;
   a.epoch_word = reinterpret_cast<u64*>(ws + L.status + 320);
   a.done_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 328);
+  a.start_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 332);
+  a.delay_mod = 1;
+  a.delay_ticks = 0;
+  if (const char* s = std::getenv("MOE_GEMM2_DEBUG_PUBLISH_DELAY")) {
+    // "mod:ticks": compute workgroups c with c % mod == 0 hold every split
+    // publish back by ticks of the 100 MHz clock (at most 10^6 = 10 ms)
+    long long m = 0, t = 0;
+    if (std::sscanf(s, "%lld:%lld", &m, &t) == 2 && m >= 1 && t > 0) {
+      a.delay_mod = (int)(m < 4096 ? m : 4096);
+      a.delay_ticks = t < 1000000 ? t : 1000000;
+    }
+  }
 
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (workspace_needs_clear(workspace, layout_signature(wl, L)) &&
+      zero_async(workspace, L.Y, s) != hipSuccess)
+    return MOE_ERR_HIP;
   hipLaunchKernelGGL(moe_gemm2_fused, dim3(C + P), dim3(kThreads), 0, s, a);
   if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
   return C;
@@ -1760,11 +1862,10 @@ extern "C" size_t moe_gemm2_trace_size(const moe_workload_t* wl) {
 extern "C" int moe_gemm2_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
   if (!workspace || workspace_bytes == 0) return MOE_ERR_INVALID_ARG;
   if (!aligned(workspace, 256)) return MOE_ERR_ALIGNMENT;
-  const size_t words = workspace_bytes / 4;
-  const unsigned blocks = (unsigned)((words + 255) / 256 < 4096 ? (words + 255) / 256 : 4096);
-  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks ? blocks : 1), dim3(256), 0,
-                     static_cast<hipStream_t>(stream), static_cast<uint32_t*>(workspace), words);
-  return hipGetLastError() == hipSuccess ? MOE_OK : MOE_ERR_HIP;
+  if (zero_async(workspace, workspace_bytes, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return MOE_ERR_HIP;
+  note_workspace_zeroed(workspace);
+  return MOE_OK;
 }
 
 extern "C" int moe_gemm2_default_params(int device, moe_select_params_t* out) {

@@ -138,10 +138,11 @@ def test_watchdog_expires_and_next_launch_is_clean(gpu_lib):
 
 def test_two_streams_at_once(gpu_lib):
     """Two launches in flight together on two streams with two workspaces
-    (each with its own consumers or the role switch) both come out right:
-    launches share nothing but the library's launch counter, and a
-    persistent grid that cannot be fully resident still drains because
-    compute workgroups never wait."""
+    (each with its own consumers or the role switch) both come out right.
+    The launches share no device state, and a grid that is not fully
+    resident still drains: compute workgroups never wait while they hold
+    tiles, and with C = 0 a workgroup serves (and waits for) consumer tasks
+    only once every workgroup of its grid has started."""
     import torch
 
     import gpu_util
