@@ -266,6 +266,36 @@ int moe_gemm2_combine_ex(const void* x_perm, const void* w2, const int32_t* expe
                          void* workspace, size_t workspace_bytes, void* stream,
                          uint64_t* trace, size_t trace_bytes);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the stage
+ * exactly as moe_gemm2_combine_ex with no trace, but its workspace is the
+ * library's own scratch, a static device array of
+ * MOE_GEMM2_NOALLOC_SCRATCH_BYTES that every GPU the library runs on holds
+ * until the process ends (each GPU its own copy, looked up on the first call
+ * on that device).  The call allocates nothing: no hipMalloc, hipFree or
+ * allocating library routine, on the host or the device.  The caller still
+ * passes inputs and outputs (same meaning, layout and alignment as for
+ * moe_gemm2_combine_ex).
+ *   - Workloads whose moe_gemm2_workspace_size exceeds
+ *     MOE_GEMM2_NOALLOC_SCRATCH_BYTES are rejected with MOE_ERR_WORKSPACE
+ *     before anything is enqueued.
+ *   - Every call on a GPU shares that GPU's scratch, which keeps the last
+ *     call's contents: the first call on a device, and any call whose
+ *     workload has another layout than the previous call's, first zeroes
+ *     the scratch's metadata with a small kernel on stream.  Calls that may
+ *     overlap in time on one GPU (other streams, other threads) race on it
+ *     and must not be issued.
+ *   - The device status word (MOE_ERR_TIMEOUT, MOE_ERR_BAD_ROUTING) lives
+ *     in the scratch and is not reported; bad routing entries are skipped
+ *     and waits are bounded as for moe_gemm2_combine.
+ * Returns the number of consumer workgroups launched (>= 0) or a negative
+ * status as moe_gemm2_combine_ex does. */
+#define MOE_GEMM2_NOALLOC_SCRATCH_BYTES (96u << 20)
+int moe_gemm2_combine_noalloc(const void* x_perm, const void* w2, const int32_t* expert_offsets,
+                              const int32_t* token_ids, const float* gate_w, float* out,
+                              const moe_workload_t* wl, int32_t num_consumers, int32_t mode,
+                              void* stream);
+
 /* Bytes the trace buffer needs for this workload (0 for an invalid one):
  * 4 * max_tiles words for the compute tiles, then 4 words for each of
  * max(splits * tasks_per_split, max_tiles) consumer tasks (tasks_per_split
@@ -350,7 +380,7 @@ int moe_gemm2_status(void* workspace, void* stream, int clear);
 /* Static description of an error code. */
 const char* moe_strerror(int status);
 
-/* ABI version of this header (major * 100 + minor): 103. */
+/* ABI version of this header (major * 100 + minor): 104. */
 int moe_gemm2_abi_version(void);
 
 #ifdef __cplusplus

@@ -33,7 +33,11 @@ EXPORTED = (
     "moe_strerror", "moe_gemm2_abi_version", "moe_gemm2_default_params_ex",
     "moe_gemm2_combine_ex", "moe_gemm2_launch_params", "moe_gemm1_pack_weights",
     "moe_gemm1_swiglu", "moe_layer_workspace_size", "moe_layer_forward",
+    "moe_gemm2_combine_noalloc",
 )
+
+# size of the library's own scratch behind moe_gemm2_combine_noalloc
+NOALLOC_SCRATCH_BYTES = 96 << 20
 
 MODE_OWNER_WRITE = 0
 MODE_ATOMIC_SCATTER = 1
@@ -124,6 +128,9 @@ def lib() -> ctypes.CDLL:
                                                ctypes.POINTER(Workload), i32, i32, vp, sz,
                                                vp, vp, sz]
             L.moe_gemm2_combine_ex.restype = ctypes.c_int
+            L.moe_gemm2_combine_noalloc.argtypes = [vp, vp, vp, vp, vp, vp,
+                                                    ctypes.POINTER(Workload), i32, i32, vp]
+            L.moe_gemm2_combine_noalloc.restype = ctypes.c_int
             L.moe_gemm1_pack_weights.argtypes = [vp, vp, i32, i32, i32, vp]
             L.moe_gemm1_pack_weights.restype = ctypes.c_int
             L.moe_gemm1_swiglu.argtypes = [vp, vp, vp, vp, vp, ctypes.POINTER(Workload), vp, sz, vp]
@@ -294,6 +301,35 @@ def combine(x_perm, w2, expert_offsets, token_ids, gate_w, T: int, splits: int =
     if r < 0:
         raise MoeError(r, "moe_gemm2_combine")
     return out, r
+
+
+def combine_noalloc(x_perm, w2, expert_offsets, token_ids, gate_w, out, T: int,
+                    splits: int = 1, topk: Optional[int] = None,
+                    counts: Optional[Sequence[int]] = None, num_consumers: int = -1,
+                    mode: int = 0, stream=None) -> int:
+    """moe_gemm2_combine_noalloc: the stage into the caller's `out` (fp32
+    [T, H]) with the library's own scratch as workspace; nothing is
+    allocated.  Returns C."""
+    import torch
+    rows, I = int(x_perm.shape[0]), int(x_perm.shape[1])
+    E, H = int(w2.shape[0]), int(w2.shape[2])
+    if topk is None:
+        topk = max(1, -(-rows // max(T, 1)))
+    for t, dt in ((x_perm, torch.bfloat16), (w2, torch.bfloat16),
+                  (expert_offsets, torch.int32), (token_ids, torch.int32),
+                  (gate_w, torch.float32), (out, torch.float32)):
+        if t.dtype != dt or not t.is_contiguous() or not t.is_cuda:
+            raise TypeError(f"expected a contiguous CUDA {dt} tensor, got {t.dtype}")
+    wl, keep = make_workload(T, H, I, E, topk, splits, counts, rows=rows)
+    vp = ctypes.c_void_p
+    r = lib().moe_gemm2_combine_noalloc(
+        vp(x_perm.data_ptr()), vp(w2.data_ptr()), vp(expert_offsets.data_ptr()),
+        vp(token_ids.data_ptr()), vp(gate_w.data_ptr()), vp(out.data_ptr()),
+        ctypes.byref(wl), int(num_consumers), int(mode), _stream(stream))
+    del keep
+    if r < 0:
+        raise MoeError(r, "moe_gemm2_combine_noalloc")
+    return r
 
 
 # ---- the up-projection and the whole post-router layer -----------------------------

@@ -1704,6 +1704,36 @@ bool workspace_needs_clear(const void* ws, uint64_t sig) {
   return true;
 }
 
+// The workspace of moe_gemm2_combine_noalloc, for callers that cannot
+// allocate device memory: one array in the code object's device memory,
+// which every GPU the library runs on holds (at its own address) until the
+// process ends.  Host code never uses its name as an address: the device
+// address is looked up once per device (hipGetSymbolAddress) and kept.
+constexpr size_t kScratchBytes = (size_t)MOE_GEMM2_NOALLOC_SCRATCH_BYTES;
+static_assert(kScratchBytes % 256 == 0, "scratch size");
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+struct ScratchDev {
+  void* ptr = nullptr;   // device address of `scratch` on that device
+  uint64_t layout = 0;   // layout of its last launch (0: none yet, so the first clears it)
+};
+ScratchDev g_scratch[64];   // guarded by g_mu
+
+// The scratch's device address on `dev` (the current device), looked up on
+// the first call on that device.
+int scratch_on_device(int dev, ScratchDev** out) {
+  if (dev < 0 || dev >= 64) return MOE_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_scratch[dev].ptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MOE_ERR_HIP;
+    if (!aligned(p, 256)) return MOE_ERR_HIP;
+    g_scratch[dev].ptr = p;
+  }
+  *out = &g_scratch[dev];
+  return MOE_OK;
+}
+
 // Zeroes `bytes` (a multiple of 4) at p on stream with a fill kernel (no
 // memset node, so that a captured graph replays it correctly).
 hipError_t zero_async(void* p, size_t bytes, hipStream_t stream) {
@@ -1714,20 +1744,42 @@ hipError_t zero_async(void* p, size_t bytes, hipStream_t stream) {
   return hipGetLastError();
 }
 
-int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
-           const int32_t* token_ids, const float* gate_w, float* out, const moe_workload_t* wl,
-           int32_t num_consumers, int32_t mode, void* workspace, size_t workspace_bytes,
-           void* stream, uint64_t* trace, size_t trace_bytes) {
+// Host-side checks of a launch's arguments other than the workspace (no HIP
+// call); fills *L.
+int validate_args(const void* x_perm, const void* w2, const int32_t* expert_offsets,
+                  const int32_t* token_ids, const float* gate_w, const float* out,
+                  const moe_workload_t* wl, int32_t num_consumers, int32_t mode, Layout* L) {
   int st = check_shape(wl);
   if (st != MOE_OK) return st;
   if (mode != 0 && mode != 1) return MOE_ERR_INVALID_ARG;
-  Layout L;
-  if (!make_layout(wl, &L)) return MOE_ERR_INVALID_ARG;
-  if (!expert_offsets || !out || (L.rows > 0 && (!x_perm || !token_ids || !gate_w)) || !w2)
+  if (!make_layout(wl, L)) return MOE_ERR_INVALID_ARG;
+  if (!expert_offsets || !out || (L->rows > 0 && (!x_perm || !token_ids || !gate_w)) || !w2)
     return MOE_ERR_INVALID_ARG;
   if (!aligned(x_perm, 16) || !aligned(w2, 16) || !aligned(out, 16) ||
       !aligned(expert_offsets, 4) || !aligned(token_ids, 4) || !aligned(gate_w, 4))
     return MOE_ERR_ALIGNMENT;
+  if (wl->host_expert_counts) {
+    long long sum = 0;
+    for (int e = 0; e < wl->E; ++e) {
+      if (wl->host_expert_counts[e] < 0) return MOE_ERR_INVALID_ARG;
+      sum += wl->host_expert_counts[e];
+    }
+    if (sum != L->rows) return MOE_ERR_INVALID_ARG;
+  }
+  if (num_consumers < -1) return MOE_ERR_INVALID_ARG;
+  return MOE_OK;
+}
+
+// `layout_slot`: where the workspace's last layout is kept when the
+// workspace is the library's own scratch (NULL: the per-address record).
+int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
+           const int32_t* token_ids, const float* gate_w, float* out, const moe_workload_t* wl,
+           int32_t num_consumers, int32_t mode, void* workspace, size_t workspace_bytes,
+           void* stream, uint64_t* trace, size_t trace_bytes, uint64_t* layout_slot = nullptr) {
+  Layout L;
+  int st = validate_args(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl, num_consumers,
+                         mode, &L);
+  if (st != MOE_OK) return st;
   if (!workspace) return MOE_ERR_WORKSPACE;
   if (!aligned(workspace, 256)) return MOE_ERR_ALIGNMENT;
   if (workspace_bytes < L.total) return MOE_ERR_WORKSPACE;
@@ -1735,15 +1787,6 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
     if (!aligned(trace, 8)) return MOE_ERR_ALIGNMENT;
     if (trace_bytes < moe_gemm2_trace_size(wl)) return MOE_ERR_INVALID_ARG;
   }
-  if (wl->host_expert_counts) {
-    long long sum = 0;
-    for (int e = 0; e < wl->E; ++e) {
-      if (wl->host_expert_counts[e] < 0) return MOE_ERR_INVALID_ARG;
-      sum += wl->host_expert_counts[e];
-    }
-    if (sum != L.rows) return MOE_ERR_INVALID_ARG;
-  }
-  if (num_consumers < -1) return MOE_ERR_INVALID_ARG;
 
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return MOE_ERR_HIP;
@@ -1835,9 +1878,16 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   }
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (workspace_needs_clear(workspace, layout_signature(wl, L)) &&
-      zero_async(workspace, L.Y, s) != hipSuccess)
-    return MOE_ERR_HIP;
+  const uint64_t sig = layout_signature(wl, L);
+  bool clear;
+  if (layout_slot) {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    clear = *layout_slot != sig;
+    *layout_slot = sig;
+  } else {
+    clear = workspace_needs_clear(workspace, sig);
+  }
+  if (clear && zero_async(workspace, L.Y, s) != hipSuccess) return MOE_ERR_HIP;
   hipLaunchKernelGGL(moe_gemm2_fused, dim3(C + P), dim3(kThreads), 0, s, a);
   if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
   return C;
@@ -1928,6 +1978,25 @@ extern "C" int moe_gemm2_combine_ex(const void* x_perm, const void* w2,
                                     size_t trace_bytes) {
   return launch(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl, num_consumers, mode,
                 workspace, workspace_bytes, stream, trace, trace_bytes);
+}
+
+extern "C" int moe_gemm2_combine_noalloc(const void* x_perm, const void* w2,
+                                         const int32_t* expert_offsets, const int32_t* token_ids,
+                                         const float* gate_w, float* out,
+                                         const moe_workload_t* wl, int32_t num_consumers,
+                                         int32_t mode, void* stream) {
+  Layout L;
+  const int st = validate_args(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl,
+                               num_consumers, mode, &L);
+  if (st != MOE_OK) return st;
+  if (L.total > kScratchBytes) return MOE_ERR_WORKSPACE;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOE_ERR_HIP;
+  ScratchDev* sd = nullptr;
+  const int r = scratch_on_device(dev, &sd);
+  if (r != MOE_OK) return r;
+  return launch(x_perm, w2, expert_offsets, token_ids, gate_w, out, wl, num_consumers, mode,
+                sd->ptr, kScratchBytes, stream, nullptr, 0, &sd->layout);
 }
 
 extern "C" int moe_gemm2_status(void* workspace, void* stream, int clear) {

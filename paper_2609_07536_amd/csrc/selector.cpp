@@ -203,4 +203,4 @@ extern "C" const char* moe_strerror(int status) {
   }
 }
 
-extern "C" int moe_gemm2_abi_version(void) { return 103; }
+extern "C" int moe_gemm2_abi_version(void) { return 104; }

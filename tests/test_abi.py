@@ -27,7 +27,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(B.EXPORTED)
-    assert L.moe_gemm2_abi_version() == 103
+    assert L.moe_gemm2_abi_version() == 104
 
 
 def _params(**kw):
@@ -204,6 +204,27 @@ def test_combine_host_validation_without_gpu():
                                      ctypes.byref(p)) == B.MOE_ERR_UNSUPPORTED
     assert L.moe_gemm2_workspace_init(None, 0, None) == B.MOE_ERR_INVALID_ARG
     assert L.moe_gemm2_status(None, None, 0) == B.MOE_ERR_INVALID_ARG
+
+    # the entry point without a workspace argument: the same argument checks,
+    # and a workload whose workspace would exceed the library's scratch is
+    # refused before any HIP call
+    def call_na(mode=0, C=-1, wlp=wl, out=A, x=A):
+        return L.moe_gemm2_combine_noalloc(vp(x), vp(A), vp(A), vp(A), vp(A), vp(out),
+                                           ctypes.byref(wlp) if wlp is not None else None,
+                                           C, mode, vp(0))
+
+    assert call_na(wlp=None) == B.MOE_ERR_INVALID_ARG
+    assert call_na(mode=2) == B.MOE_ERR_INVALID_ARG
+    assert call_na(C=-2) == B.MOE_ERR_INVALID_ARG
+    assert call_na(x=0) == B.MOE_ERR_INVALID_ARG
+    assert call_na(out=A + 4) == B.MOE_ERR_ALIGNMENT
+    assert call_na(wlp=w3) == B.MOE_ERR_INVALID_ARG
+    big, kbig = B.make_workload(T=8192, H=2048, I=704, E=30, topk=4, splits=2)
+    assert B.workspace_size(big) > B.NOALLOC_SCRATCH_BYTES
+    for mode in (0, 1):
+        assert call_na(mode=mode, wlp=big) == B.MOE_ERR_WORKSPACE
+    fits, kfits = B.make_workload(T=4096, H=1024, I=256, E=16, topk=8, splits=1)
+    assert 0 < B.workspace_size(fits) <= B.NOALLOC_SCRATCH_BYTES
 
 
 def _task_tokens(T, H, L):
