@@ -52,6 +52,7 @@ constexpr int kTaskTarget = 512;        // owner-write tasks wanted per launch (
 constexpr int kCommTN = 1024;           // consumer task: columns (at most)
 constexpr int kMaxE = 1024;
 constexpr int kMaxSplits = 16;
+constexpr int kMaxBandTab = 2048;       // (E + 1) * L entries of the token-band tables
 constexpr int kMaxTopk = 64;
 constexpr int kMaxGrid = 4096;
 
@@ -104,7 +105,8 @@ struct KArgs {
   long long delay_ticks;      //   each split publish by delay_ticks (100 MHz), else 0
   uint32_t* task_ctr;         // [kMaxSplits]: next consumer task of each split (reset by
                               // workgroup 0 each launch)
-  int mode;                   // 0 owner-write, 1 fp32 atomic scatter
+  int mode;                   // 0 owner-write, 1 fp32 atomic scatter, 2 owner-write over
+                              // token bands (splits along the routed rows)
 };
 
 // Arguments of the up-projection stage (grouped GEMM1 with the SwiGLU
@@ -167,8 +169,12 @@ struct Smem {
   int tile_prefix[kMaxE + 1]; // exclusive prefix of ceil(count/kBM)
   int scan[kThreads / 64];   // per-wave totals of the expert scan
   int rowtok[kBM];            // gathering stages: token of each row of the staged tile
+  int band_pre[kMaxBandTab];  // token bands: [b (E+1) + e] exclusive prefix over experts of
+                              // band b's m-tile counts
+  int band_start[kMaxSplits + 1];  // token bands: first global tile of each band
   int flag;
   int task;                   // consumer task claimed by the workgroup
+  int task_band;              // token bands: last band holding a row of the staged task
   u64 epoch;                  // this launch's epoch, read once at the start
 };
 
@@ -639,6 +645,99 @@ __device__ TileInfo decode_tile(const Smem& sm, const Args& a, int W_comp, int g
   return ti;
 }
 
+// ---- token bands (mode 2) ------------------------------------------------------
+// The pipeline splits run along the routed rows instead of the columns: each
+// expert's n_e = ceil(count_e / kBM) m-tiles are cut into L consecutive runs,
+// band b holding m-tiles [b n_e / L, (b+1) n_e / L), and every band covers
+// the full width H.  The global tile sequence is band -> expert -> m-tile ->
+// n-tile, so the n-tiles of an m-tile stay together (its x rows are read once
+// for all of H) and, with rows sorted by token inside each expert, band b
+// holds about the tokens [b T / L, (b+1) T / L).  A consumer task waits for
+// the bands that hold its rows (computed from the rows themselves, so any
+// row order is correct).
+__device__ __forceinline__ int band_lo(int n, int b, int L) { return (int)((long long)b * n / L); }
+
+// band_pre and band_start from the expert table (wave w scans bands w, w+8..)
+__device__ void load_bands(Smem& sm, const KArgs& a) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int E1 = a.E + 1;
+  for (int b = wave; b < a.L; b += kThreads / 64) {
+    int carry = 0;
+    for (int e0 = 0; e0 < a.E; e0 += 64) {
+      const int e = e0 + lane;
+      int c = 0;
+      if (e < a.E) {
+        const int n = (sm.count[e] + kBM - 1) / kBM;
+        c = band_lo(n, b + 1, a.L) - band_lo(n, b, a.L);
+      }
+      int v = c;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int u = __shfl_up(v, d);
+        if (lane >= d) v += u;
+      }
+      if (e < a.E) sm.band_pre[b * E1 + e] = carry + v - c;
+      carry += __shfl(v, 63);
+    }
+    if (lane == 0) sm.band_pre[b * E1 + a.E] = carry;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int b = 0; b < a.L; ++b) {
+      sm.band_start[b] = run;
+      run += sm.band_pre[b * E1 + a.E] * a.ntps;
+    }
+    sm.band_start[a.L] = run;
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ int band_of_tile(const Smem& sm, const KArgs& a, int g) {
+  int b = 0;
+  while (b + 1 < a.L && sm.band_start[b + 1] <= g) ++b;
+  return b;
+}
+
+// Tile g of the band sequence.
+__device__ TileInfo decode_band_tile(const Smem& sm, const KArgs& a, int g) {
+  const int b = band_of_tile(sm, a, g);
+  const int idx = g - sm.band_start[b];
+  const int mt = idx / a.ntps;
+  const int nt = idx - mt * a.ntps;
+  const int* pre = sm.band_pre + b * (a.E + 1);
+  int lo = 0, hi = a.E - 1;
+  while (lo < hi) {   // last expert whose band-b run starts at or before mt
+    const int mid = (lo + hi + 1) >> 1;
+    if (pre[mid] <= mt) lo = mid; else hi = mid - 1;
+  }
+  const int n_e = (sm.count[lo] + kBM - 1) / kBM;
+  const int i = band_lo(n_e, b, a.L) + (mt - pre[lo]);
+  TileInfo ti;
+  ti.e = lo;
+  ti.r0 = sm.start[lo] + i * kBM;
+  ti.rows_valid = min(kBM, sm.count[lo] - i * kBM);
+  ti.n0 = nt * kBN;
+  ti.cols_valid = min(kBN, a.H - ti.n0);
+  return ti;
+}
+
+// The band of the m-tile holding permuted row r (L - 1 for a row outside
+// every expert's range, possible only with bad offsets: such a task then
+// waits for every band).
+__device__ __forceinline__ int band_of_row(const Smem& sm, const KArgs& a, int r) {
+  int lo = 0, hi = a.E - 1;
+  while (lo < hi) {   // last expert starting at or before r
+    const int mid = (lo + hi + 1) >> 1;
+    if (sm.start[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  const int off = r - sm.start[lo];
+  if (off < 0 || off >= sm.count[lo]) return a.L - 1;
+  const int n_e = (sm.count[lo] + kBM - 1) / kBM;
+  const int i = off / kBM;
+  return (int)(((long long)(i + 1) * a.L + n_e - 1) / n_e) - 1;
+}
+
 // This lane's global addresses for its loads of a tile's stages.
 template <class Args>
 __device__ __forceinline__ TileCtx make_ctx(Smem& sm, const Args& a, const TileInfo& ti, int wave) {
@@ -981,8 +1080,14 @@ static_assert(sizeof(TaskMeta) <= sizeof(Smem::a) + sizeof(Smem::b) &&
               "task metadata overlays the operand ring");
 __device__ TaskMeta& task_meta(Smem& sm) { return *reinterpret_cast<TaskMeta*>(&sm.a[0][0]); }
 
-__device__ void load_task_meta(TaskMeta& m, const KArgs& a, u64 cnt_epoch, int t0, int ntok) {
+__device__ void load_task_meta(Smem& sm, TaskMeta& m, const KArgs& a, u64 cnt_epoch, int t0,
+                               int ntok) {
   const int K = a.topk;
+  const bool bands = a.mode == 2;
+  if (bands) {
+    if (threadIdx.x == 0) sm.task_band = 0;
+    __syncthreads();
+  }
   for (int i = opaque_tid(); i < ntok * K; i += kThreads) {
     const int t = i / K;
     const int j = i - t * K;
@@ -993,8 +1098,13 @@ __device__ void load_task_meta(TaskMeta& m, const KArgs& a, u64 cnt_epoch, int t
     int r = 0;
     float g = 0.f;
     if (j < n) {
-      r = a.inv[(long long)(t0 + t) * K + j];
+      // token bands: no acquire precedes these reads (it would invalidate
+      // the L2 under the compute workgroups), so they are agent-coherent
+      r = bands ? __hip_atomic_load(&a.inv[(long long)(t0 + t) * K + j], __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT)
+                : a.inv[(long long)(t0 + t) * K + j];
       g = a.gate_w[r];
+      if (bands) atomicMax(&sm.task_band, band_of_row(sm, a, r));
     }
     m.row[i] = r;
     m.gate[i] = g;
@@ -1037,7 +1147,10 @@ __device__ __forceinline__ void fma4(float (&acc)[4], float g, const u32x2& v) {
 // (a padding row j >= n re-reads row n-1 and gets weight 0), then the FMAs
 // in ascending row order.  n >= 1 for both tokens; every row read is one
 // this launch has written, so its values are finite and weight 0 adds 0.
-template <int U>
+// kCoherent: the loads are agent-coherent (they miss any stale copy in this
+// XCD's caches), for consumers that read Y without an acquire.
+constexpr int kCoherentStream = 16 | 2;   // buffer load cache policy: sc1 nt
+template <int U, bool kCoherent>
 __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&rs)[2],
                                             const int (&gs)[2], const int (&n)[2],
                                             const int (&col)[kColBlocks],
@@ -1049,9 +1162,18 @@ __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&
     for (int u = 0; u < U; ++u) {
       const int j = j0 + u < n[p] ? j0 + u : n[p] - 1;
       const uint16_t* yr = a.Y + (size_t)__builtin_amdgcn_readlane(rs[p], j) * a.ypitch;
+      if constexpr (kCoherent) {
+        // one row of Y as a buffer (wave-uniform base), 32-bit column offsets
+        const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)yr, (short)0, a.ypitch * 2, 0x00020000);
 #pragma unroll
-      for (int b = 0; b < kColBlocks; ++b)
-        v[p][u][b] = __builtin_nontemporal_load((const u32x2*)(yr + col[b]));
+        for (int b = 0; b < kColBlocks; ++b)
+          v[p][u][b] = __builtin_amdgcn_raw_buffer_load_b64(rr, 2 * col[b], 0, kCoherentStream);
+      } else {
+#pragma unroll
+        for (int b = 0; b < kColBlocks; ++b)
+          v[p][u][b] = __builtin_nontemporal_load((const u32x2*)(yr + col[b]));
+      }
     }
 #pragma unroll
   for (int p = 0; p < 2; ++p)
@@ -1068,6 +1190,7 @@ __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&
 // m: wave w takes the token pairs w, w+nwaves, ...; lane l owns columns
 // 256b + 4l .. 256b + 4l + 3 of every block b, so each output store of a
 // wave writes 1 KB of one row contiguously (whole cache lines).
+template <bool kCoherent>
 __device__ void consume_task(const KArgs& a, const TaskMeta& m, int t0, int ntok, int col0,
                              int ncols) {
   const int lane = threadIdx.x & 63;
@@ -1114,13 +1237,13 @@ __device__ void consume_task(const KArgs& a, const TaskMeta& m, int t0, int ntok
     for (int j0 = 0; j0 < nmax; j0 += 8) {
       const int left = nmax - j0;
       if (left <= 2)
-        gather_step<2>(a, j0, rl, gl, nl, col, acc);
+        gather_step<2, kCoherent>(a, j0, rl, gl, nl, col, acc);
       else if (left <= 4)
-        gather_step<4>(a, j0, rl, gl, nl, col, acc);
+        gather_step<4, kCoherent>(a, j0, rl, gl, nl, col, acc);
       else if (left <= 6)
-        gather_step<6>(a, j0, rl, gl, nl, col, acc);
+        gather_step<6, kCoherent>(a, j0, rl, gl, nl, col, acc);
       else
-        gather_step<8>(a, j0, rl, gl, nl, col, acc);
+        gather_step<8, kCoherent>(a, j0, rl, gl, nl, col, acc);
     }
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
@@ -1193,7 +1316,8 @@ __device__ void scatter_tile(const KArgs& a, const TileInfo& ti) {
 
 // What a workgroup knows while it serves consumer tasks.
 struct Consumer {
-  int ready;     // splits [0, ready] were acquired by this workgroup
+  int ready;     // splits [0, ready] were acquired by this workgroup (token bands:
+                 // the tiles [0, ready) are known published)
   int split;     // the first split that may still have unclaimed tasks
   int meta_t0;   // token block whose metadata is in LDS (-1: none)
   bool inv_ok;   // every workgroup's inverse-map share is published
@@ -1205,7 +1329,7 @@ __device__ void ensure_task_meta(Smem& sm, const KArgs& a, int idx, Consumer& cs
   const int t0 = (idx / a.cb_per_split) * a.comm_tm;
   if (t0 != cs.meta_t0) {
     __syncthreads();   // every wave is done with the previous task's metadata
-    load_task_meta(task_meta(sm), a, count_epoch(sm), t0, min(a.comm_tm, a.T - t0));
+    load_task_meta(sm, task_meta(sm), a, count_epoch(sm), t0, min(a.comm_tm, a.T - t0));
     cs.meta_t0 = t0;
   }
 }
@@ -1224,7 +1348,7 @@ __device__ void run_task(Smem& sm, const KArgs& a, int W_comp, int tps, int s, i
     const int col0 = s * a.nsplit + cb * a.comm_tn;
     const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
     ensure_task_meta(sm, a, idx, cs);
-    consume_task(a, task_meta(sm), t0, ntok, col0, ncols);
+    consume_task<false>(a, task_meta(sm), t0, ntok, col0, ncols);
   }
   if (a.trace) {
     __syncthreads();
@@ -1287,6 +1411,59 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
   }
 }
 
+// Token bands (mode 2): one task counter over all tasks (token block major,
+// then column block of the full width).  A task waits until every tile of
+// the bands up to the last one holding its rows is published: the flags of
+// the band sequence's prefix [0, band_start[b+1]), polled incrementally.
+// Nothing here acquires (an acquire would invalidate the XCD's L2 under the
+// compute workgroups still running there): the inverse map and Y are read
+// with agent-coherent loads, which see the data the compute workgroups'
+// releases wrote back.
+__device__ void consumer_loop_bands(Smem& sm, const KArgs& a, Consumer& cs) {
+  const int total = sm.band_start[a.L];
+  if (total > a.max_tiles) return;
+  if (!cs.inv_ok) {
+    if (!wait_flags(sm, a.wg_flags, gridDim.x, a, false)) return;
+    cs.inv_ok = true;
+  }
+  const int ntasks = a.tasks_per_split;
+  while (true) {
+    const u64 t_wait = now_100mhz();
+    if (threadIdx.x == 0)
+      sm.task = (int)min(__hip_atomic_fetch_add(&a.task_ctr[0], 1u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT),
+                         (uint32_t)ntasks);
+    __syncthreads();
+    const int idx = sm.task;
+    __syncthreads();   // sm.task is rewritten by the next claim
+    if (idx >= ntasks) break;
+    const int tb = idx / a.cb_per_split;
+    const int cb = idx - tb * a.cb_per_split;
+    const int t0 = tb * a.comm_tm;
+    const int ntok = min(a.comm_tm, a.T - t0);
+    const int col0 = cb * a.comm_tn;
+    const int ncols = min(a.comm_tn, a.H - col0);
+    ensure_task_meta(sm, a, idx, cs);
+    const int need = sm.band_start[min(sm.task_band, a.L - 1) + 1];
+    if (need > cs.ready) {   // cs.ready: tiles [0, ready) are known published
+      if (!wait_flags(sm, a.tile_flags + cs.ready, need - cs.ready, a, false)) return;
+      cs.ready = need;
+    }
+    const u64 t_go = now_100mhz();
+    consume_task<true>(a, task_meta(sm), t0, ntok, col0, ncols);
+    if (a.trace) {
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        u64* rec = a.trace + 4 * a.max_tiles + 4 * (long long)idx;
+        rec[0] = t_wait;
+        rec[1] = t_go;
+        rec[2] = now_100mhz();
+        rec[3] = blockIdx.x;
+      }
+    }
+  }
+}
+
 // Compute index of workgroup b >= C such that consecutive indices share an
 // XCD (workgroups are dispatched to the 8 XCDs round-robin by id), keeping a
 // wave's neighbouring tiles, which share x rows and W2 columns, in one L2.
@@ -1304,12 +1481,16 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
     __hip_atomic_fetch_add(a.start_ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   load_experts(sm, a);
+  const bool bands = a.mode == 2;
+  if (bands) load_bands(sm, a);
   const long long rows_dev = a.E > 0 ? (long long)sm.start[a.E - 1] + sm.count[a.E - 1] : 0;
   const int m_tiles = sm.tile_prefix[a.E];
-  const int W_comp = m_tiles * a.ntps;
+  const int W_comp = m_tiles * a.ntps;   // tiles per split (column splits)
   const int b = blockIdx.x;
   const int c = b < a.C ? 0 : compute_index(b, a.C, (int)gridDim.x);
-  const int total = W_comp * a.L;
+  const int total = bands ? sm.band_start[a.L] : W_comp * a.L;
+  const int first_split_end = bands ? sm.band_start[1] : W_comp;
+  auto split_of = [&](int g) { return bands ? band_of_tile(sm, a, g) : g / W_comp; };
   // compute workgroup c takes tiles c, c+P, c+2P, ... (XCD-aware: the
   // workgroups of consecutive c share an XCD, and so do their tiles)
   const int g_first = b >= a.C && c < total ? c : -1;
@@ -1319,8 +1500,10 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
   // the share is published at once instead: the consumers then stage their
   // first task's metadata while the split is still computing.
   const bool defer_inverse =
-      a.L > 1 && g_first >= 0 && g_first < W_comp && total <= a.max_tiles;
-  auto decode = [&](int g) { return decode_tile(sm, a, W_comp, g); };
+      a.L > 1 && g_first >= 0 && g_first < first_split_end && total <= a.max_tiles;
+  auto decode = [&](int g) {
+    return bands ? decode_band_tile(sm, a, g) : decode_tile(sm, a, W_comp, g);
+  };
   const int nk = (a.I + kBK - 1) / kBK;
   // A compute workgroup issues its first tile's ring fill before building
   // its share of the inverse map, so those loads fly during its atomics.
@@ -1351,7 +1534,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       const TileInfo nt = next ? decode(g_next) : cur;
       const u64 t_start = now_100mhz();
       u64 t_mid[2];
-      const bool last_of_split = !next || g_next / W_comp != g / W_comp;
+      const bool last_of_split = !next || split_of(g_next) != split_of(g);
       // A split's last tile holds the x half of its next tile's stage 1
       // back until the publish, so that the publish's waits cover nothing
       // issued after the Y stores.
@@ -1419,8 +1602,13 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
   }
   // consumers, and role-switch workgroups after their tiles (one call site,
   // so that the loop is inlined)
-  Consumer cs = {-1, 0, -1, false, false};
-  consumer_loop(sm, a, W_comp, cs);
+  if (bands) {
+    Consumer cs = {0, 0, -1, false, false};
+    consumer_loop_bands(sm, a, cs);
+  } else {
+    Consumer cs = {-1, 0, -1, false, false};
+    consumer_loop(sm, a, W_comp, cs);
+  }
 }
 
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -1506,7 +1694,8 @@ int check_shape(const moe_workload_t* wl) {
       wl->splits <= 0 || wl->rows < 0)
     return MOE_ERR_INVALID_ARG;
   if (wl->E > kMaxE || wl->topk > kMaxTopk || wl->splits > kMaxSplits) return MOE_ERR_UNSUPPORTED;
-  if (wl->I % 8 != 0 || wl->H % (8 * wl->splits) != 0) return MOE_ERR_UNSUPPORTED;
+  // (column splits also need H % (8 splits) == 0, checked per launch mode)
+  if (wl->I % 8 != 0 || wl->H % 8 != 0) return MOE_ERR_UNSUPPORTED;
   // an expert's W2 slice is addressed with 32-bit byte offsets
   if ((long long)wl->I * wl->H * 2 > 0x7fffffffLL) return MOE_ERR_UNSUPPORTED;
   const long long rows = wl->rows > 0 ? wl->rows : (long long)wl->T * wl->topk;
@@ -1514,7 +1703,7 @@ int check_shape(const moe_workload_t* wl) {
     return MOE_ERR_UNSUPPORTED;
   // tile indices are 32-bit on the device, also for the most tiles that
   // bad offsets (every expert spanning all rows) could make
-  const long long ntps = (wl->H / wl->splits + kBN - 1) / kBN;
+  const long long ntps = ((wl->H + wl->splits - 1) / wl->splits + kBN - 1) / kBN;
   if ((long long)wl->E * ((rows + kBM - 1) / kBM + 1) * ntps * wl->splits > (long long)INT32_MAX / 2)
     return MOE_ERR_UNSUPPORTED;
   return MOE_OK;
@@ -1523,7 +1712,7 @@ int check_shape(const moe_workload_t* wl) {
 bool make_layout(const moe_workload_t* wl, Layout* L) {
   if (check_shape(wl) != MOE_OK) return false;
   L->rows = wl->rows > 0 ? wl->rows : (long long)wl->T * wl->topk;
-  L->nsplit = wl->H / wl->splits;
+  L->nsplit = (wl->H + wl->splits - 1) / wl->splits;   // ceil: sizes also cover token bands
   L->ntps = (L->nsplit + kBN - 1) / kBN;
   L->comm_tn = L->nsplit < kCommTN ? L->nsplit : kCommTN;
   L->cb_per_split = (L->nsplit + L->comm_tn - 1) / L->comm_tn;
@@ -1744,6 +1933,26 @@ hipError_t zero_async(void* p, size_t bytes, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Consumer task geometry of a token-band launch (mode 2): tasks of TM tokens
+// x min(1024, H) columns over the full width, TM = kCommTM halved (down to
+// kCommTMMin) while there would be fewer than kTaskTarget tasks.  The
+// workspace layout (sized for column splits) covers it: it has fewer tasks
+// and no more tiles.
+struct BandTasks {
+  int comm_tm, comm_tn, cb, tasks;
+};
+BandTasks band_tasks(const moe_workload_t* wl) {
+  BandTasks t;
+  t.comm_tn = wl->H < kCommTN ? wl->H : kCommTN;
+  t.cb = (wl->H + t.comm_tn - 1) / t.comm_tn;
+  t.comm_tm = kCommTM;
+  while (t.comm_tm > kCommTMMin &&
+         (long long)((wl->T + t.comm_tm - 1) / t.comm_tm) * t.cb < kTaskTarget)
+    t.comm_tm /= 2;
+  t.tasks = ((wl->T + t.comm_tm - 1) / t.comm_tm) * t.cb;
+  return t;
+}
+
 // Host-side checks of a launch's arguments other than the workspace (no HIP
 // call); fills *L.
 int validate_args(const void* x_perm, const void* w2, const int32_t* expert_offsets,
@@ -1751,7 +1960,9 @@ int validate_args(const void* x_perm, const void* w2, const int32_t* expert_offs
                   const moe_workload_t* wl, int32_t num_consumers, int32_t mode, Layout* L) {
   int st = check_shape(wl);
   if (st != MOE_OK) return st;
-  if (mode != 0 && mode != 1) return MOE_ERR_INVALID_ARG;
+  if (mode != 0 && mode != 1 && mode != 2) return MOE_ERR_INVALID_ARG;
+  if (mode == 2 && (long long)(wl->E + 1) * wl->splits > kMaxBandTab) return MOE_ERR_UNSUPPORTED;
+  if (mode != 2 && wl->H % (8 * wl->splits) != 0) return MOE_ERR_UNSUPPORTED;
   if (!make_layout(wl, L)) return MOE_ERR_INVALID_ARG;
   if (!expert_offsets || !out || (L->rows > 0 && (!x_perm || !token_ids || !gate_w)) || !w2)
     return MOE_ERR_INVALID_ARG;
@@ -1801,7 +2012,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
       C = kDefaultFixedC;
     } else {
       moe_select_params_t p;
-      fill_params(d, mode, wl->topk, L.comm_tm, &p);
+      fill_params(d, mode, wl->topk, mode == 2 ? band_tasks(wl).comm_tm : L.comm_tm, &p);
       moe_workload_t w = *wl;
       if (w.ranks <= 0) w.ranks = 1;
       moe_partition_t part;
@@ -1810,7 +2021,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
       C = part.C;
     }
   }
-  int P, drain = 0;
+  int P, drain = mode == 2 ? 1 : 0;   // token bands: compute workgroups always drain
   if (C == 0) {
     P = d.occ * d.cus;
     drain = 1;
@@ -1862,6 +2073,15 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.cb_per_split = L.cb_per_split;
   a.tasks_per_split = L.tasks_per_split;
   a.mode = mode;
+  if (mode == 2) {   // token bands: every band spans the full width
+    const BandTasks bt = band_tasks(wl);
+    a.nsplit = wl->H;
+    a.ntps = (wl->H + kBN - 1) / kBN;
+    a.comm_tm = bt.comm_tm;
+    a.comm_tn = bt.comm_tn;
+    a.cb_per_split = bt.cb;
+    a.tasks_per_split = bt.tasks;
+  }
   a.epoch_word = reinterpret_cast<u64*>(ws + L.status + 320);
   a.done_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 328);
   a.start_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 332);
@@ -1905,7 +2125,11 @@ extern "C" size_t moe_gemm2_trace_size(const moe_workload_t* wl) {
   if (!make_layout(wl, &L)) return 0;
   // compute tiles, then consumer tasks (owner-write tasks or, for the
   // atomic scatter, one per compute tile)
-  const long long tasks = (long long)wl->splits * L.tasks_per_split;
+  // consumer-task records: the most of the column-split tasks, the token-band
+  // tasks and (atomic scatter) the compute tiles
+  long long tasks = (long long)wl->splits * L.tasks_per_split;
+  const long long band = band_tasks(wl).tasks;
+  if (band > tasks) tasks = band;
   return (size_t)(4 * L.max_tiles + 4 * (tasks > L.max_tiles ? tasks : L.max_tiles)) * 8;
 }
 
@@ -1939,14 +2163,16 @@ extern "C" int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t top
 
 extern "C" int moe_gemm2_launch_params(int device, int32_t mode, const moe_workload_t* wl,
                                        moe_select_params_t* out) {
-  if (!out || (mode != 0 && mode != 1)) return MOE_ERR_INVALID_ARG;
+  if (!out || (mode != 0 && mode != 1 && mode != 2)) return MOE_ERR_INVALID_ARG;
   Layout L;
   if (!make_layout(wl, &L)) return check_shape(wl) == MOE_ERR_UNSUPPORTED ? MOE_ERR_UNSUPPORTED
                                                                           : MOE_ERR_INVALID_ARG;
+  if (mode != 2 && wl->H % (8 * wl->splits) != 0) return MOE_ERR_UNSUPPORTED;
+  if (mode == 2 && (long long)(wl->E + 1) * wl->splits > kMaxBandTab) return MOE_ERR_UNSUPPORTED;
   DevInfo d;
   const int st = device_info(device, &d);
   if (st != MOE_OK) return st;
-  fill_params(d, mode, wl->topk, L.comm_tm, out);
+  fill_params(d, mode, wl->topk, mode == 2 ? band_tasks(wl).comm_tm : L.comm_tm, out);
   return MOE_OK;
 }
 

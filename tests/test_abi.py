@@ -177,7 +177,9 @@ def test_combine_host_validation_without_gpu():
         args.update(kw)
         w2, k2 = B.make_workload(**args)
         assert call(wlp=w2) == B.MOE_ERR_UNSUPPORTED, kw
-        assert B.workspace_size(w2) == 0
+        # column splits need H % (8 splits) == 0; token bands (mode 2) do not,
+        # so the workspace size is defined for any split count
+        assert (B.workspace_size(w2) == 0) == ("splits" not in kw), kw
     w3, k3 = B.make_workload(T=256, H=1024, I=512, E=8, topk=2, splits=1,
                              counts=[64] * 7 + [63])         # sums to 511 != 512
     assert call(wlp=w3) == B.MOE_ERR_INVALID_ARG
@@ -188,15 +190,15 @@ def test_combine_host_validation_without_gpu():
                                       ctypes.byref(wlp), C, mode, vp(A), ctypes.c_size_t(need),
                                       vp(0), vp(0), ctypes.c_size_t(0))
 
-    for mode in (-1, 2, 7):
+    for mode in (-1, 3, 7):
         assert call_ex(mode) == B.MOE_ERR_INVALID_ARG, mode
-    for mode in (0, 1):
+    for mode in (0, 1, 2):
         assert call_ex(mode, out=A + 4) == B.MOE_ERR_ALIGNMENT
         assert call_ex(mode, C=-2) == B.MOE_ERR_INVALID_ARG
     assert L.moe_gemm2_default_params_ex(0, 2, 1, None) == B.MOE_ERR_INVALID_ARG
     p = B.SelectParams()
     assert L.moe_gemm2_launch_params(0, 0, ctypes.byref(wl), None) == B.MOE_ERR_INVALID_ARG
-    for mode in (-1, 2):
+    for mode in (-1, 3):
         assert L.moe_gemm2_launch_params(0, mode, ctypes.byref(wl),
                                          ctypes.byref(p)) == B.MOE_ERR_INVALID_ARG
     bad, kb = B.make_workload(T=256, H=1020, I=512, E=8, topk=2, splits=1)
@@ -214,7 +216,7 @@ def test_combine_host_validation_without_gpu():
                                            C, mode, vp(0))
 
     assert call_na(wlp=None) == B.MOE_ERR_INVALID_ARG
-    assert call_na(mode=2) == B.MOE_ERR_INVALID_ARG
+    assert call_na(mode=3) == B.MOE_ERR_INVALID_ARG
     assert call_na(C=-2) == B.MOE_ERR_INVALID_ARG
     assert call_na(x=0) == B.MOE_ERR_INVALID_ARG
     assert call_na(out=A + 4) == B.MOE_ERR_ALIGNMENT
