@@ -86,6 +86,12 @@ typedef struct {
   int32_t groups;                    /* g, input groups (1) */
   int64_t rho_ref_num, rho_ref_den;  /* rho_ref as a positive rational */
   int32_t k_ref, tile_m_ref, tile_n_ref, d_ref;
+  int32_t split_axis;                /* 0: the L splits cut the output columns N (the paper);
+                                        1: they cut the routed rows (token bands, see
+                                        moe_gemm2_combine_ex mode 2) */
+  int32_t drain;                     /* 0: the paper's recurrence; 1: compute slots join the
+                                        consumers after their tiles (the last split is served
+                                        by all C + P slots) */
 } moe_select_params_t;
 
 /* The chosen partition.  T(C) = T_num / T_den in compute-wave units; W_comp
@@ -110,12 +116,32 @@ typedef struct {
  * P0 = o_comp G slots run every compute tile and then all serve the consumer
  * tasks: T(0) = ceil(L W_comp / P0) + rho ceil(L W_comm / P0), R = 0, P = P0,
  * Delta = ceil(W_comp/P0) P0 - W_comp.
+ * Extensions selected by the parameters (both 0 gives the paper's model):
+ *   split_axis = 1 (token bands): per-split work
+ *     W_comp = ceil(g sum_e ceil(M_e/T_M) / L) ceil(N/T_N),
+ *     W_comm = ceil(ceil(ceil(M/D)/T_M^comm) / L) ceil(N/T_N^comm);
+ *   drain = 1: the last split's service uses every slot,
+ *     F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P)).
  * Pure host code: no HIP call, no allocation, thread-safe.
  * Returns C* >= c_min and fills *out when out != NULL; MOE_ERR_INVALID_ARG for a
  * null wl/p, non-positive dimensions or parameters, a negative host count or
  * arithmetic overflow; MOE_ERR_NO_LEGAL_PARTITION when no candidate is legal. */
 int moe_select_partition(const moe_workload_t* wl, const moe_select_params_t* p,
                          moe_partition_t* out);
+
+/* L as a second decision variable (Method, eq:split-arrival and
+ * eq:split-finish take L as given; here it is chosen as well): for every
+ * L = l_min..l_max, moe_select_partition on the workload with splits = L;
+ * returns the C of the (L, C) pair with the least T(C), ties to the least L
+ * (fewer publishes), and writes that L to *splits_out and its partition to
+ * *out (each when non-NULL).  wl->splits is ignored.  The caller keeps L
+ * within what the launch accepts (column splits: H % (8 L) == 0; token
+ * bands: (E + 1) L <= 2048).  Returns C >= 0, MOE_ERR_INVALID_ARG
+ * (l_min < 1, l_max < l_min, or as moe_select_partition) or
+ * MOE_ERR_NO_LEGAL_PARTITION. */
+int moe_select_partition_splits(const moe_workload_t* wl, const moe_select_params_t* p,
+                                int32_t l_min, int32_t l_max, moe_partition_t* out,
+                                int32_t* splits_out);
 
 /* The whole T(C) table of the same model: T_num_out[i] is the numerator of
  * T(c_min + i) over the common denominator *T_den_out, or -1 where P <= 0.
@@ -139,9 +165,11 @@ int moe_gemm2_default_params(int device, moe_select_params_t* out);
  * task per compute tile) sets the consumer tile to
  * max(1, tile_m / topk) tokens x tile_n columns, so that W_comm counts
  * about one task per compute tile, and rho_ref to that mode's calibration
- * (MOE_GEMM2_RHO_REF_SCATTER="num/den" overrides it).  Returns 0 or
- * MOE_ERR_HIP / MOE_ERR_INVALID_ARG (also for a mode other than 0 or 1 or
- * topk <= 0). */
+ * (MOE_GEMM2_RHO_REF_SCATTER="num/den" overrides it); mode 2 (token bands)
+ * sets split_axis = 1, drain = 1 and rho_ref to that mode's calibration
+ * (MOE_GEMM2_RHO_REF_BANDS overrides it).  Modes 0 and 1 leave split_axis
+ * and drain 0.  Returns 0 or MOE_ERR_HIP / MOE_ERR_INVALID_ARG (also for a
+ * mode other than 0, 1 or 2 or topk <= 0). */
 int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk, moe_select_params_t* out);
 
 /* The parameters a launch of this workload hands to the selector (what
@@ -151,10 +179,13 @@ int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk, moe_sele
  * ceil(H/splits/1024)), so that a small batch's combine still spreads over
  * every CU; comm_tile_m = TM and rho_ref, calibrated for 64-token tasks, is
  * scaled by TM/64 (a task's bytes are proportional to its tokens).  Mode 1:
- * as moe_gemm2_default_params_ex(device, 1, wl->topk).  Returns 0,
- * MOE_ERR_INVALID_ARG (null pointer, mode other than 0 or 1, invalid
- * workload), MOE_ERR_UNSUPPORTED (shape outside moe_gemm2_combine's range)
- * or MOE_ERR_HIP. */
+ * as moe_gemm2_default_params_ex(device, 1, wl->topk).  Mode 2: tasks of
+ * TM tokens x min(1024, H) columns of the full width, TM = 64 halved down
+ * to 16 while there would be fewer than 512 (ceil(T/TM) ceil(H/1024)),
+ * rho_ref scaled by TM/64, split_axis = 1, drain = 1.  Returns 0,
+ * MOE_ERR_INVALID_ARG (null pointer, mode other than 0, 1 or 2, invalid
+ * workload), MOE_ERR_UNSUPPORTED (shape outside moe_gemm2_combine_ex's
+ * range for that mode) or MOE_ERR_HIP. */
 int moe_gemm2_launch_params(int device, int32_t mode, const moe_workload_t* wl,
                             moe_select_params_t* out);
 
@@ -228,7 +259,7 @@ int moe_gemm2_combine(const void* x_perm, const void* w2, const int32_t* expert_
  * tile g of the global sequence, words 4g..4g+3 = start, end of the
  * reduction loop, end of the Y stores, end of the tile (after the split's
  * publish for a workgroup's last tile of a split); then, from word
- * 4 * max_tiles (max_tiles = splits * ceil(H/splits/256) *
+ * 4 * max_tiles (max_tiles = splits * ceil(ceil(H/splits)/256) *
  * (ceil(rows/256) + E)), for each consumer task j, words 4j..4j+3 = wait
  * start, wait end, finish, workgroup id (task j: split j / tasks_per_split,
  * token block and column block from j % tasks_per_split, with
@@ -254,12 +285,27 @@ int moe_gemm2_combine_traced(const void* x_perm, const void* w2, const int32_t* 
  *           additions varies from run to run, so the result does too, by
  *           rounding only.  Rows with an out-of-range token id are skipped
  *           and flagged; the topk bound per token is not checked (every
- *           in-range row is added).
+ *           in-range row is added);
+ *   mode 2  owner-write over token bands: the wl->splits = L pipeline
+ *           splits cut the routed rows instead of the columns.  Expert
+ *           e's n_e = ceil(M_e/256) m-tiles are cut into L runs, band b
+ *           holding m-tiles [b n_e / L, (b+1) n_e / L) over the full width
+ *           H; tiles run band -> expert -> m-tile -> n-tile.  A consumer
+ *           task (TM tokens x min(1024, H) columns, one counter over all
+ *           tasks) waits until every tile of the bands up to the last band
+ *           holding one of its rows is published, reads the inverse map and
+ *           Y with agent-coherent loads (no acquire), and compute
+ *           workgroups always join the consumers after their tiles.  The
+ *           result is bitwise that of mode 0 (same per-token order).  Any
+ *           L >= 1 with (E + 1) L <= 2048 (else MOE_ERR_UNSUPPORTED); H % 8
+ *           == 0 suffices (modes 0 and 1 need H % (8 L) == 0).
  * trace: NULL, or a buffer as for moe_gemm2_combine_traced (in mode 1 the
  * consumer-task words hold one record per compute tile of the global
- * sequence).  With num_consumers = -1 the selector runs with
+ * sequence; in mode 2 record j is task j of the single task sequence).
+ * With num_consumers = -1 the selector runs with
  * moe_gemm2_launch_params(device, mode, wl).  Everything else is as
- * for moe_gemm2_combine; MOE_ERR_INVALID_ARG for a mode other than 0 or 1. */
+ * for moe_gemm2_combine; MOE_ERR_INVALID_ARG for a mode other than 0, 1
+ * or 2. */
 int moe_gemm2_combine_ex(const void* x_perm, const void* w2, const int32_t* expert_offsets,
                          const int32_t* token_ids, const float* gate_w, float* out,
                          const moe_workload_t* wl, int32_t num_consumers, int32_t mode,
@@ -298,8 +344,10 @@ int moe_gemm2_combine_noalloc(const void* x_perm, const void* w2, const int32_t*
 
 /* Bytes the trace buffer needs for this workload (0 for an invalid one):
  * 4 * max_tiles words for the compute tiles, then 4 words for each of
- * max(splits * tasks_per_split, max_tiles) consumer tasks (tasks_per_split
- * as for moe_gemm2_combine_traced). */
+ * max(splits * tasks_per_split, band tasks, max_tiles) consumer tasks
+ * (tasks_per_split as for moe_gemm2_combine_traced, band tasks as for
+ * moe_gemm2_combine_ex mode 2); max_tiles = splits * ceil(ceil(H/splits)/256)
+ * * (ceil(rows/256) + E). */
 size_t moe_gemm2_trace_size(const moe_workload_t* wl);
 
 /* ---- The rest of the post-router layer on one GPU: the up-projection.
@@ -380,7 +428,7 @@ int moe_gemm2_status(void* workspace, void* stream, int clear);
 /* Static description of an error code. */
 const char* moe_strerror(int status);
 
-/* ABI version of this header (major * 100 + minor): 104. */
+/* ABI version of this header (major * 100 + minor): 105. */
 int moe_gemm2_abi_version(void);
 
 #ifdef __cplusplus

@@ -31,6 +31,19 @@ Extension beyond the paper's legal set (only when c_min = 0): the
 role-switch candidate C = 0, where all o_comp * G slots run every compute
 tile and then all of them serve the consumer tasks,
 T(0) = ceil(L W_comp / P0) + rho ceil(L W_comm / P0) with P0 = o_comp G.
+
+Further extensions, off unless asked for (the paper's model is their
+special case split_axis = 0, drain = False, one given L):
+  * split_axis = 1, token bands: the L splits cut the routed rows instead
+    of the output columns, so a split holds about 1/L of the m-tiles over
+    the full width and 1/L of the token blocks:
+    W_comp = ceil(g m_tiles / L) ceil(N / T_N),
+    W_comm = ceil(ceil(ceil(M/D) / T_M^comm) / L) ceil(N / T_N^comm);
+  * drain: compute slots join the consumers after their last tile, so the
+    last split is served by all C + P slots:
+    F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
+  * L as a decision variable: the (L, C) pair with the least T(C) over a
+    range of L, ties to the smaller L.
 """
 from __future__ import annotations
 
@@ -66,14 +79,22 @@ def routed_m_tiles(counts: Optional[Sequence[int]], tile_m: int, E: int,
     return E * cdiv(per_expert, tile_m)
 
 
-def compute_work(m_tiles: int, N: int, L: int, tile_n: int, g: int = 1) -> int:
-    """W_comp = g * (sum_e ceil(M_e/T_M)) * ceil(ceil(N/L) / T_N)."""
-    return g * m_tiles * cdiv(cdiv(N, L), tile_n)
+def compute_work(m_tiles: int, N: int, L: int, tile_n: int, g: int = 1,
+                 split_axis: int = 0) -> int:
+    """Column splits: W_comp = g * (sum_e ceil(M_e/T_M)) * ceil(ceil(N/L) / T_N).
+    Token bands: ceil(g * sum_e ceil(M_e/T_M) / L) * ceil(N / T_N)."""
+    if split_axis == 0:
+        return g * m_tiles * cdiv(cdiv(N, L), tile_n)
+    return cdiv(g * m_tiles, L) * cdiv(N, tile_n)
 
 
-def comm_work(M: int, D: int, N: int, L: int, comm_m: int, comm_n: int) -> int:
-    """W_comm = ceil(ceil(M/D) / T_M^comm) * ceil(ceil(N/L) / T_N^comm)."""
-    return cdiv(cdiv(M, D), comm_m) * cdiv(cdiv(N, L), comm_n)
+def comm_work(M: int, D: int, N: int, L: int, comm_m: int, comm_n: int,
+              split_axis: int = 0) -> int:
+    """Column splits: W_comm = ceil(ceil(M/D) / T_M^comm) * ceil(ceil(N/L) / T_N^comm).
+    Token bands: ceil(ceil(ceil(M/D) / T_M^comm) / L) * ceil(N / T_N^comm)."""
+    if split_axis == 0:
+        return cdiv(cdiv(M, D), comm_m) * cdiv(cdiv(N, L), comm_n)
+    return cdiv(cdiv(cdiv(M, D), comm_m), L) * cdiv(N, comm_n)
 
 
 def rho_scaled(rho_ref: Fraction, K: int, K_ref: int, tile_m: int, tile_n: int,
@@ -84,7 +105,7 @@ def rho_scaled(rho_ref: Fraction, K: int, K_ref: int, tile_m: int, tile_n: int,
 
 
 def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
-             o_comp: int, rho: Fraction) -> Optional[Candidate]:
+             o_comp: int, rho: Fraction, drain: bool = False) -> Optional[Candidate]:
     """The recurrence for one candidate C; None if P(C) <= 0 (illegal)."""
     if C == 0:
         P0 = o_comp * G
@@ -104,7 +125,11 @@ def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
     F: List[Fraction] = []
     prev = Fraction(0)
     for s in range(L):
-        prev = max(Fraction(A[s]), prev) + q
+        if drain and s == L - 1:
+            # every slot serves the last split once its tiles are done
+            prev = max(Fraction(A[s]), prev) + Fraction(rho) * cdiv(W_comm, C + P)
+        else:
+            prev = max(Fraction(A[s]), prev) + q
         F.append(prev)
     V_comp = cdiv(W_comp, P)
     return Candidate(C=C, R=R, P=P, A=A, V_comm=V_comm, q=q, F=F, T=F[-1],
@@ -112,13 +137,14 @@ def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
 
 
 def select_from_work(W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
-                     o_comp: int, rho: Fraction, c_min: int, c_max: int):
+                     o_comp: int, rho: Fraction, c_min: int, c_max: int,
+                     drain: bool = False):
     """Argmin of T(C) over the legal C, then smallest Delta, then smallest C.
 
     Returns (best Candidate or None, list of all legal candidates)."""
     cands = []
     for C in range(c_min, c_max + 1):
-        c = evaluate(C, W_comp, W_comm, L, G, o_comm, o_comp, rho)
+        c = evaluate(C, W_comp, W_comm, L, G, o_comm, o_comp, rho, drain)
         if c is not None:
             cands.append(c)
     if not cands:
@@ -144,16 +170,32 @@ class SelectParams:
     tile_n_ref: int
     d_ref: int
     groups: int = 1
+    split_axis: int = 0
+    drain: bool = False
 
 
 def select(T: int, H: int, I: int, E: int, topk: int, L: int,
            counts: Optional[Sequence[int]], p: SelectParams, D: int = 1):
     """Algorithm 1 on a workload: returns (best, candidates, W_comp, W_comm, rho)."""
     m_tiles = routed_m_tiles(counts, p.tile_m, E, T * topk)
-    W_comp = compute_work(m_tiles, H, L, p.tile_n, p.groups)
-    W_comm = comm_work(T, D, H, L, p.comm_tile_m, p.comm_tile_n)
+    W_comp = compute_work(m_tiles, H, L, p.tile_n, p.groups, p.split_axis)
+    W_comm = comm_work(T, D, H, L, p.comm_tile_m, p.comm_tile_n, p.split_axis)
     rho = rho_scaled(p.rho_ref, I, p.k_ref, p.tile_m, p.tile_n,
                      p.tile_m_ref, p.tile_n_ref, D, p.d_ref)
     best, cands = select_from_work(W_comp, W_comm, L, p.num_cus, p.occ_comm,
-                                   p.occ_comp, rho, p.c_min, p.c_max)
+                                   p.occ_comp, rho, p.c_min, p.c_max, bool(p.drain))
     return best, cands, W_comp, W_comm, rho
+
+
+def select_splits(T: int, H: int, I: int, E: int, topk: int,
+                  counts: Optional[Sequence[int]], p: SelectParams,
+                  l_min: int, l_max: int, D: int = 1):
+    """L as a decision variable: the model for every L in [l_min, l_max];
+    returns (L, best Candidate) with the least T, ties to the smaller L, or
+    (None, None) when no L has a legal candidate."""
+    best_L, best = None, None
+    for L in range(l_min, l_max + 1):
+        b, _, _, _, _ = select(T, H, I, E, topk, L, counts, p, D)
+        if b is not None and (best is None or b.T < best.T):
+            best_L, best = L, b
+    return best_L, best

@@ -33,7 +33,7 @@ EXPORTED = (
     "moe_strerror", "moe_gemm2_abi_version", "moe_gemm2_default_params_ex",
     "moe_gemm2_combine_ex", "moe_gemm2_launch_params", "moe_gemm1_pack_weights",
     "moe_gemm1_swiglu", "moe_layer_workspace_size", "moe_layer_forward",
-    "moe_gemm2_combine_noalloc",
+    "moe_gemm2_combine_noalloc", "moe_select_partition_splits",
 )
 
 # size of the library's own scratch behind moe_gemm2_combine_noalloc
@@ -41,6 +41,7 @@ NOALLOC_SCRATCH_BYTES = 96 << 20
 
 MODE_OWNER_WRITE = 0
 MODE_ATOMIC_SCATTER = 1
+MODE_TOKEN_BANDS = 2
 
 
 class Workload(ctypes.Structure):
@@ -58,7 +59,8 @@ class SelectParams(ctypes.Structure):
                 ("c_max", ctypes.c_int32), ("groups", ctypes.c_int32),
                 ("rho_ref_num", ctypes.c_int64), ("rho_ref_den", ctypes.c_int64),
                 ("k_ref", ctypes.c_int32), ("tile_m_ref", ctypes.c_int32),
-                ("tile_n_ref", ctypes.c_int32), ("d_ref", ctypes.c_int32)]
+                ("tile_n_ref", ctypes.c_int32), ("d_ref", ctypes.c_int32),
+                ("split_axis", ctypes.c_int32), ("drain", ctypes.c_int32)]
 
 
 class Partition(ctypes.Structure):
@@ -98,6 +100,11 @@ def lib() -> ctypes.CDLL:
                                                ctypes.POINTER(SelectParams),
                                                ctypes.POINTER(Partition)]
             L.moe_select_partition.restype = ctypes.c_int
+            L.moe_select_partition_splits.argtypes = [ctypes.POINTER(Workload),
+                                                      ctypes.POINTER(SelectParams), i32, i32,
+                                                      ctypes.POINTER(Partition),
+                                                      ctypes.POINTER(ctypes.c_int32)]
+            L.moe_select_partition_splits.restype = ctypes.c_int
             L.moe_select_evaluate.argtypes = [ctypes.POINTER(Workload),
                                               ctypes.POINTER(SelectParams),
                                               ctypes.POINTER(ctypes.c_int64), i32,
@@ -170,6 +177,15 @@ def select_partition(wl: Workload, params: SelectParams):
     out = Partition()
     r = lib().moe_select_partition(ctypes.byref(wl), ctypes.byref(params), ctypes.byref(out))
     return r, out
+
+
+def select_partition_splits(wl: Workload, params: SelectParams, l_min: int, l_max: int):
+    """moe_select_partition_splits: returns (C or error, L, Partition)."""
+    out = Partition()
+    L = ctypes.c_int32(0)
+    r = lib().moe_select_partition_splits(ctypes.byref(wl), ctypes.byref(params), int(l_min),
+                                          int(l_max), ctypes.byref(out), ctypes.byref(L))
+    return r, L.value, out
 
 
 def select_evaluate(wl: Workload, params: SelectParams):

@@ -1801,6 +1801,10 @@ constexpr int64_t kRhoRefDen = 100;
 // rows), measured the same way: 26.2 us / 22.3 us = 1.18.
 constexpr int64_t kRhoScatterNum = 118;
 constexpr int64_t kRhoScatterDen = 100;
+// The same for token bands (mode 2, agent-coherent reads of Y), 64-token
+// tasks over 1024 columns.
+constexpr int64_t kRhoBandsNum = 149;
+constexpr int64_t kRhoBandsDen = 100;
 constexpr int kDefaultFixedC = 8;
 
 // Selector parameters of a launch.  comm_tm is the owner-write task's token
@@ -1825,16 +1829,20 @@ void fill_params(const DevInfo& d, int mode, int topk, int comm_tm, moe_select_p
   p->c_min = 0;
   p->c_max = 64;
   p->groups = 1;
-  p->rho_ref_num = mode == 1 ? kRhoScatterNum : kRhoRefNum;
-  p->rho_ref_den = mode == 1 ? kRhoScatterDen : kRhoRefDen;
-  if (const char* s = std::getenv(mode == 1 ? "MOE_GEMM2_RHO_REF_SCATTER" : "MOE_GEMM2_RHO_REF")) {
+  p->rho_ref_num = mode == 1 ? kRhoScatterNum : mode == 2 ? kRhoBandsNum : kRhoRefNum;
+  p->rho_ref_den = mode == 1 ? kRhoScatterDen : mode == 2 ? kRhoBandsDen : kRhoRefDen;
+  p->split_axis = mode == 2 ? 1 : 0;
+  p->drain = mode == 2 ? 1 : 0;
+  const char* env = mode == 1 ? "MOE_GEMM2_RHO_REF_SCATTER"
+                    : mode == 2 ? "MOE_GEMM2_RHO_REF_BANDS" : "MOE_GEMM2_RHO_REF";
+  if (const char* s = std::getenv(env)) {
     long long n = 0, q = 0;
     if (std::sscanf(s, "%lld/%lld", &n, &q) == 2 && n > 0 && q > 0) {
       p->rho_ref_num = n;
       p->rho_ref_den = q;
     }
   }
-  if (mode == 0 && comm_tm != kCommTM) {
+  if (mode != 1 && comm_tm != kCommTM) {
     p->rho_ref_num *= comm_tm;
     p->rho_ref_den *= kCommTM;
   }
@@ -2153,7 +2161,7 @@ extern "C" int moe_gemm2_default_params(int device, moe_select_params_t* out) {
 
 extern "C" int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk,
                                            moe_select_params_t* out) {
-  if (!out || (mode != 0 && mode != 1) || topk <= 0) return MOE_ERR_INVALID_ARG;
+  if (!out || (mode != 0 && mode != 1 && mode != 2) || topk <= 0) return MOE_ERR_INVALID_ARG;
   DevInfo d;
   const int st = device_info(device, &d);
   if (st != MOE_OK) return st;

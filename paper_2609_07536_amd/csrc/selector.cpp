@@ -18,6 +18,16 @@
 // role-switch candidate C = 0, where all o_comp G slots compute every tile
 // and then all of them serve the consumer tasks:
 //   T(0) = ceil(L W_comp / P0) + rho ceil(L W_comm / P0),   P0 = o_comp G.
+//
+// Two further extensions, each off unless its parameter asks for it:
+//   split_axis = 1: the L splits cut the routed rows (token bands) instead
+//     of the output columns; a band holds about 1/L of the m-tiles over the
+//     full width and 1/L of the token blocks:
+//       W_comp = ceil(g m_tiles / L) ceil(N / T_N)
+//       W_comm = ceil(ceil(ceil(M/D) / T_M^comm) / L) ceil(N / T_N^comm)
+//   drain = 1: the compute slots join the consumers after their last tile,
+//     so the last split is served by all C + P slots:
+//       F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P)).
 #include <cstdint>
 #include <cstdlib>
 
@@ -35,6 +45,7 @@ struct Model {
   int64_t W_comp = 0, W_comm = 0;
   int64_t rho_num = 0, rho_den = 1;
   int L = 1;
+  int drain = 0;
 };
 
 // Builds the per-split work counts and the scaled rho; returns a status.
@@ -62,10 +73,19 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
     int64_t total = wl->rows > 0 ? wl->rows : (int64_t)wl->T * wl->topk;
     m_tiles = (int64_t)wl->E * cdiv64(cdiv64(total, wl->E), p->tile_m);
   }
-  const int64_t n_split = cdiv64(wl->H, wl->splits);
-  m->W_comp = (int64_t)p->groups * m_tiles * cdiv64(n_split, p->tile_n);
-  m->W_comm = cdiv64(cdiv64(wl->T, wl->ranks), p->comm_tile_m) * cdiv64(n_split, p->comm_tile_n);
+  if (p->split_axis != 0 && p->split_axis != 1) return MOE_ERR_INVALID_ARG;
+  if (p->drain != 0 && p->drain != 1) return MOE_ERR_INVALID_ARG;
+  const int64_t token_blocks = cdiv64(cdiv64(wl->T, wl->ranks), p->comm_tile_m);
+  if (p->split_axis == 0) {
+    const int64_t n_split = cdiv64(wl->H, wl->splits);
+    m->W_comp = (int64_t)p->groups * m_tiles * cdiv64(n_split, p->tile_n);
+    m->W_comm = token_blocks * cdiv64(n_split, p->comm_tile_n);
+  } else {
+    m->W_comp = cdiv64((int64_t)p->groups * m_tiles, wl->splits) * cdiv64(wl->H, p->tile_n);
+    m->W_comm = cdiv64(token_blocks, wl->splits) * cdiv64(wl->H, p->comm_tile_n);
+  }
   m->L = wl->splits;
+  m->drain = p->drain;
 
   // eq:rho-scaling: rho = rho_ref (K_ref/K) (T_M,ref T_N,ref)/(T_M T_N) (D/D_ref)
   i128 num = (i128)p->rho_ref_num * p->k_ref * p->tile_m_ref * p->tile_n_ref * wl->ranks;
@@ -107,10 +127,11 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
   const int64_t P = (int64_t)p->occ_comp * ((int64_t)p->num_cus - R);
   if (P <= 0) return false;
   const i128 q = (i128)m.rho_num * cdiv64(m.W_comm, C);
+  const i128 q_drain = (i128)m.rho_num * cdiv64(m.W_comm, (int64_t)C + P);
   i128 F = 0;
   for (int s = 0; s < m.L; ++s) {
     const i128 A = (i128)cdiv64((int64_t)(s + 1) * m.W_comp, P) * m.rho_den;
-    F = (A > F ? A : F) + q;
+    F = (A > F ? A : F) + (m.drain && s == m.L - 1 ? q_drain : q);
     if (F > kI64Max) {
       *status = MOE_ERR_INVALID_ARG;
       return false;
@@ -166,6 +187,36 @@ extern "C" int moe_select_partition(const moe_workload_t* wl, const moe_select_p
   return bestC;
 }
 
+extern "C" int moe_select_partition_splits(const moe_workload_t* wl, const moe_select_params_t* p,
+                                          int32_t l_min, int32_t l_max, moe_partition_t* out,
+                                          int32_t* splits_out) {
+  if (!wl || !p || l_min < 1 || l_max < l_min) return MOE_ERR_INVALID_ARG;
+  bool found = false;
+  moe_partition_t best{};
+  int32_t bestL = 0;
+  for (int32_t L = l_min; L <= l_max; ++L) {
+    moe_workload_t w = *wl;
+    w.splits = L;
+    moe_partition_t cur;
+    const int r = moe_select_partition(&w, p, &cur);
+    if (r == MOE_ERR_NO_LEGAL_PARTITION) continue;
+    if (r < 0) return r;
+    // T(C) of different L share the unit (compute waves of the same P(C)),
+    // but not the denominator: compare T_num / T_den exactly
+    const i128 lhs = (i128)cur.T_num * (found ? best.T_den : 1);
+    const i128 rhs = (i128)(found ? best.T_num : 0) * cur.T_den;
+    if (!found || lhs < rhs) {   // L ascends: ties keep the smaller L
+      found = true;
+      best = cur;
+      bestL = L;
+    }
+  }
+  if (!found) return MOE_ERR_NO_LEGAL_PARTITION;
+  if (out) *out = best;
+  if (splits_out) *splits_out = bestL;
+  return best.C;
+}
+
 extern "C" int moe_select_evaluate(const moe_workload_t* wl, const moe_select_params_t* p,
                                    int64_t* T_num_out, int32_t n, int64_t* T_den_out) {
   Model m;
@@ -203,4 +254,4 @@ extern "C" const char* moe_strerror(int status) {
   }
 }
 
-extern "C" int moe_gemm2_abi_version(void) { return 104; }
+extern "C" int moe_gemm2_abi_version(void) { return 105; }

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(B.EXPORTED)
-    assert L.moe_gemm2_abi_version() == 104
+    assert L.moe_gemm2_abi_version() == 105
 
 
 def _params(**kw):
@@ -46,7 +46,8 @@ def _oracle_params(p):
         comm_tile_n=p.comm_tile_n, occ_comp=p.occ_comp, occ_comm=p.occ_comm,
         num_cus=p.num_cus, c_min=p.c_min, c_max=p.c_max,
         rho_ref=Fraction(p.rho_ref_num, p.rho_ref_den), k_ref=p.k_ref,
-        tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups)
+        tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups,
+        split_axis=p.split_axis, drain=bool(p.drain))
 
 
 def test_hand_example_through_the_abi():
@@ -89,7 +90,8 @@ def _random_case(rnd):
                 c_max=rnd.randint(1, 80), rho_ref_num=rnd.randint(1, 100000),
                 rho_ref_den=rnd.randint(1, 10000), k_ref=rnd.choice([352, 704, 1408]),
                 tile_m_ref=rnd.choice([128, 256]), tile_n_ref=rnd.choice([128, 256]),
-                d_ref=rnd.choice([1, 4]))
+                d_ref=rnd.choice([1, 4]), split_axis=rnd.choice([0, 0, 1]),
+                drain=rnd.choice([0, 0, 1]))
     D = rnd.choice([1, 1, 2, 4])
     return T, H, I, E, topk, L, counts, p, D
 
@@ -123,6 +125,34 @@ def test_selector_bit_exact_against_oracle():
                 assert tnum == -1
         n_checked += 1
     assert n_checked > 2000
+
+
+def test_split_selection_bit_exact_against_oracle():
+    """moe_select_partition_splits (L as a decision variable) against the
+    oracle's select_splits on random workloads, both split axes, with and
+    without the drain term."""
+    rnd = random.Random(77)
+    n = 0
+    for _ in range(400):
+        T, H, I, E, topk, L, counts, p, D = _random_case(rnd)
+        l_min = rnd.randint(1, 3)
+        l_max = l_min + rnd.randint(0, 6)
+        wl, keep = B.make_workload(T, H, I, E, topk, L, counts, ranks=D)
+        r, Lb, part = B.select_partition_splits(wl, p, l_min, l_max)
+        L_o, best = osel.select_splits(T, H, I, E, topk, counts, _oracle_params(p), l_min,
+                                       l_max, D=D)
+        if best is None:
+            assert r == B.MOE_ERR_NO_LEGAL_PARTITION
+            continue
+        assert (r, Lb) == (best.C, L_o)
+        assert Fraction(part.T_num, part.T_den) == best.T
+        n += 1
+    assert n > 300
+    wl, keep = B.make_workload(100, 256, 64, 4, 2, 1, [50, 50, 50, 50])
+    assert B.select_partition_splits(wl, _params(), 0, 3)[0] == B.MOE_ERR_INVALID_ARG
+    assert B.select_partition_splits(wl, _params(), 3, 2)[0] == B.MOE_ERR_INVALID_ARG
+    for field in ("split_axis", "drain"):
+        assert B.select_partition(wl, _params(**{field: 2}))[0] == B.MOE_ERR_INVALID_ARG
 
 
 def test_selector_argument_errors():

@@ -146,3 +146,88 @@ def test_role_switch_candidate_closed_form():
     assert best.C == 0                      # 4.5 beats the paper's best (9)
     best1, _ = sel.select_from_work(30, 6, 2, 10, 1, 2, Fraction(3, 2), 1, 6)
     assert best1.C == 5
+
+
+# ---- the extensions: token-band work counts, the drain term, L as a variable ----
+
+def test_band_work_counts_by_hand():
+    """10 routed m-tiles, N = 1024 in 256-wide tiles, T = 1000 tokens in
+    64-token x 1024-column consumer tasks, L = 4.
+    Column splits: W_comp = 10 * ceil(256/256) = 10, W_comm = ceil(1000/64)
+    * ceil(256/1024) = 16.  Token bands: W_comp = ceil(10/4) * 4 = 12,
+    W_comm = ceil(16/4) * 1 = 4."""
+    assert sel.compute_work(10, 1024, 4, 256) == 10
+    assert sel.comm_work(1000, 1, 1024, 4, 64, 1024) == 16
+    assert sel.compute_work(10, 1024, 4, 256, split_axis=1) == 12
+    assert sel.comm_work(1000, 1, 1024, 4, 64, 1024, split_axis=1) == 4
+    # with one split both axes describe the same work
+    for m, N, T in ((37, 2048, 16384), (5, 200, 3), (1, 64, 1)):
+        assert sel.compute_work(m, N, 1, 256) == sel.compute_work(m, N, 1, 256, split_axis=1)
+        assert sel.comm_work(T, 1, N, 1, 64, 1024) == sel.comm_work(T, 1, N, 1, 64, 1024,
+                                                                    split_axis=1)
+
+
+def test_drain_hand_example():
+    """G=10, o_comm=o_comp=1, W_comp=30, W_comm=6, L=2, rho=3/2, drain.
+
+    Worked by hand (P = 10 - C; A_s = ceil((s+1) 30 / P); the first split is
+    served by the C consumers, q = 1.5 ceil(6/C); the last by all C + P = 10
+    slots, 1.5 ceil(6/10) = 1.5):
+      C=1: P=9 A=(4,7)  F0=4+9=13     T=max(7,13)+1.5=14.5
+      C=2: P=8 A=(4,8)  F0=4+4.5=8.5  T=max(8,8.5)+1.5=10
+      C=3: P=7 A=(5,9)  F0=5+3=8      T=max(9,8)+1.5=10.5
+      C=4: P=6 A=(5,10) F0=5+3=8      T=10+1.5=11.5
+      C=5: P=5 A=(6,12) F0=6+3=9      T=12+1.5=13.5
+      C=6: P=4 A=(8,15) F0=8+1.5=9.5  T=15+1.5=16.5
+    and without the drain term (the paper's recurrence) the last split also
+    takes q: T = 22, 13, 12, 13, 15, 16.5."""
+    rho = Fraction(3, 2)
+    want = {1: ([4, 7], Fraction(29, 2), Fraction(22)), 2: ([4, 8], Fraction(10), Fraction(13)),
+            3: ([5, 9], Fraction(21, 2), Fraction(12)), 4: ([5, 10], Fraction(23, 2), Fraction(13)),
+            5: ([6, 12], Fraction(27, 2), Fraction(15)),
+            6: ([8, 15], Fraction(33, 2), Fraction(33, 2))}
+    for C, (A, T_drain, T_plain) in want.items():
+        c = sel.evaluate(C, 30, 6, 2, 10, 1, 1, rho, drain=True)
+        assert (c.A, c.T) == (A, T_drain), C
+        assert sel.evaluate(C, 30, 6, 2, 10, 1, 1, rho).T == T_plain, C
+    best, _ = sel.select_from_work(30, 6, 2, 10, 1, 1, rho, 1, 6, drain=True)
+    assert (best.C, best.T) == (2, 10)
+    best, _ = sel.select_from_work(30, 6, 2, 10, 1, 1, rho, 1, 6)
+    assert (best.C, best.T) == (3, 12)
+
+
+def test_drain_single_split_closed_form():
+    """L = 1: T(C) = ceil(W_comp/P) + rho ceil(W_comm/(C+P)) with drain."""
+    for (W, Wc, G, rho) in ((100, 37, 16, Fraction(7, 5)), (1, 1, 2, Fraction(1)),
+                            (513, 99, 256, Fraction(141, 100))):
+        for C in range(1, G):
+            P = G - C
+            c = sel.evaluate(C, W, Wc, 1, G, 1, 1, rho, drain=True)
+            assert c.T == sel.cdiv(W, P) + rho * sel.cdiv(Wc, C + P)
+
+
+def test_split_count_as_a_decision_variable_by_hand():
+    """Token bands, G=10, o=1, rho=1, 40 routed m-tiles over one 256-wide
+    n-tile, T=1280 tokens in 64-token tasks (20 token blocks), one column
+    block; candidates C = 1..3.  Per L (W_comp = ceil(40/L), W_comm =
+    ceil(20/L)), worked by hand:
+      L=1: C=3 best: P=7, A=ceil(40/7)=6, q=ceil(20/3)=7       -> T=13
+      L=2: C=3 best: P=7, A=(3,6), q=ceil(10/3)=4, F=(7,11)    -> T=11
+      L=3: C=3 best: P=7, A=(2,4,6), q=ceil(7/3)=3, F=(5,8,11) -> T=11
+      L=4: C=3 best: P=7, A=(2,3,5,6), q=ceil(5/3)=2,
+           F=(4,6,8,10)                                        -> T=10
+    so L in 1..4 picks (L=4, C=3, T=10) and L in 1..2 picks (L=2, C=3)."""
+    p = sel.SelectParams(tile_m=256, tile_n=256, comm_tile_m=64, comm_tile_n=1024,
+                         occ_comp=1, occ_comm=1, num_cus=10, c_min=1, c_max=3,
+                         rho_ref=Fraction(1), k_ref=704, tile_m_ref=256, tile_n_ref=256,
+                         d_ref=1, split_axis=1)
+    counts = [256 * 10] * 4                   # 4 experts x 10 m-tiles = 40
+    per_L = {1: (3, Fraction(13)), 2: (3, Fraction(11)), 4: (3, Fraction(10))}
+    for L, (C, T) in per_L.items():
+        best, _, W_comp, W_comm, rho = sel.select(1280, 256, 704, 4, 8, L, counts, p)
+        assert (W_comp, W_comm, rho) == (sel.cdiv(40, L), sel.cdiv(20, L), 1)
+        assert (best.C, best.T) == (C, T), L
+    L, best = sel.select_splits(1280, 256, 704, 4, 8, counts, p, 1, 4)
+    assert (L, best.C, best.T) == (4, 3, Fraction(10))
+    L, best = sel.select_splits(1280, 256, 704, 4, 8, counts, p, 1, 2)
+    assert (L, best.C, best.T) == (2, 3, Fraction(11))
