@@ -194,8 +194,11 @@ int moe_gemm2_launch_params(int device, int32_t mode, const moe_workload_t* wl,
  * Returns 0 for an invalid workload. */
 size_t moe_gemm2_workspace_size(const moe_workload_t* wl);
 
-/* Zero a workspace (required once after allocating it, before its first
- * use).  Enqueued on stream.  Returns 0 or MOE_ERR_HIP / MOE_ERR_INVALID_ARG. */
+/* Prepare a workspace (required once after allocating it, before its first
+ * use): zero it and give it a launch epoch no earlier initialisation in
+ * this process used, so that readiness flags left in that memory by an
+ * earlier user can never read as published.  Enqueued on stream.  Returns
+ * 0 or MOE_ERR_HIP / MOE_ERR_INVALID_ARG. */
 int moe_gemm2_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
 
 /* The stage.
@@ -293,9 +296,10 @@ int moe_gemm2_combine_traced(const void* x_perm, const void* w2, const int32_t* 
  *           H; tiles run band -> expert -> m-tile -> n-tile.  A consumer
  *           task (TM tokens x min(1024, H) columns, one counter over all
  *           tasks) waits until every tile of the bands up to the last band
- *           holding one of its rows is published, reads the inverse map and
- *           Y with agent-coherent loads (no acquire), and compute
- *           workgroups always join the consumers after their tiles.  The
+ *           holding one of its rows is published (an agent-scope acquire
+ *           for the inverse map and one per newly published band prefix),
+ *           and compute workgroups always join the consumers after their
+ *           tiles.  The
  *           result is bitwise that of mode 0 (same per-token order).  Any
  *           L >= 1 with (E + 1) L <= 2048 (else MOE_ERR_UNSUPPORTED); H % 8
  *           == 0 suffices (modes 0 and 1 need H % (8 L) == 0).

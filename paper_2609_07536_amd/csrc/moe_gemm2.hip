@@ -28,12 +28,14 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <chrono>
 #include <cstddef>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
+#include <random>
 #include <unordered_map>
 
 #include "moe_gemm2.h"
@@ -60,6 +62,12 @@ constexpr int kMaxGrid = 4096;
 // the rows of a tile fall on few memory channels, which cost ~18% of the
 // write bandwidth of row-strided stores in a microbenchmark.
 constexpr int kYPad = 64;     // Y row padding, elements
+// Every 128-byte line of Y is written by exactly one compute tile: rows
+// start on a line, and so does each column split's segment of a row.  (Two
+// workgroups writing disjoint parts of one line was measured to lose data
+// now and then, when they ran on different XCDs.)
+constexpr int kYLine = 64;    // elements per 128-byte line
+__host__ __device__ inline int round_up_line(int n) { return (n + kYLine - 1) / kYLine * kYLine; }
 constexpr uint32_t kStBadRouting = 1u;
 constexpr uint32_t kStTimeout = 2u;
 
@@ -89,7 +97,9 @@ struct KArgs {
   long long max_tiles;        // capacity of tile_flags
   long long spin_limit;
   int T, H, I, E, topk, L;
-  int ypitch;                 // row pitch of Y in elements (H + kYPad)
+  int ypitch;                 // row pitch of Y in elements: L ysplit + kYPad
+  int ysplit;                 // elements of a row's segment for one split (nsplit rounded up
+                              // to a line); column c of split s is at s ysplit + c - s nsplit
   int nsplit;                 // columns per split (H / L)
   int ntps;                   // compute n-tiles per split
   int C, P;                   // consumer and compute workgroups
@@ -205,6 +215,24 @@ __device__ __forceinline__ uint32_t epoch_count(u64 v, u64 cnt_epoch) {
 __device__ __forceinline__ u64 launch_epoch(const KArgs& a) {
   return __hip_atomic_load(a.epoch_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
 }
+// Agent-scope release and acquire with the wait for the cache operation
+// itself.  The release writes back the L2 (buffer_wbl2) and the acquire
+// invalidates it (buffer_inv); both are vector memory operations counted in
+// vmcnt.  The compiler places its wait after them only while it tracks some
+// other vector memory operation in flight, and here the callers have waited
+// for everything already, so it drops the wait: a flag store could then
+// become visible before the written-back lines, or the barrier could let the
+// workgroup's other waves read before the invalidate has finished.  The
+// explicit wait closes both.
+__device__ __forceinline__ void release_agent() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+__device__ __forceinline__ void acquire_agent() {
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
 __device__ __forceinline__ uint32_t flag_epoch(const Smem& sm) { return (uint32_t)sm.epoch; }
 __device__ __forceinline__ u64 count_epoch(const Smem& sm) {
   return (sm.epoch & ((1ull << (64 - kCntBits)) - 1)) << kCntBits;
@@ -262,7 +290,7 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
   // workgroup shares, and the barrier orders the other waves' reads after
   // it.  (An acquire in every wave made eight L2 invalidates per workgroup;
   // with all workgroups acquiring at once they queued for microseconds.)
-  if (acquire && threadIdx.x < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  if (acquire && threadIdx.x < 64) acquire_agent();
   __syncthreads();  // sm.flag may be rewritten by the next wait
   return ok;
 }
@@ -366,7 +394,7 @@ __device__ void consumer_prologue(const Smem& sm, const KArgs& a, long long rows
   __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));
   __syncthreads();
   if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    release_agent();
     __hip_atomic_store(&a.wg_flags[blockIdx.x], flag_epoch(sm), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -598,6 +626,7 @@ __device__ __forceinline__ void mfma_step_loads(f32x16 (&acc)[kNB][kMB], const b
 // columns n0 .. n0+cols_valid-1 of Y.
 struct TileInfo {
   int e, r0, rows_valid, n0, cols_valid;
+  int ny0;   // Y column of the tile's first column (the split's line-aligned segment)
 };
 
 // Gathering stages: the token of tile row threadIdx.x (rows past the
@@ -621,6 +650,9 @@ __device__ __forceinline__ void gather_commit(Smem& sm, const G1Args& a, int t) 
   }
 }
 
+__device__ __forceinline__ int y_split_pitch(const KArgs& a) { return a.ysplit; }
+__device__ __forceinline__ int y_split_pitch(const G1Args& a) { return a.nsplit; }
+
 // Tile g of the global sequence (split-major, then expert, m-tile, n-tile).
 // Every tile count fits in 32 bits (checked on the host for the worst case
 // of overlapping expert ranges).
@@ -642,6 +674,7 @@ __device__ TileInfo decode_tile(const Smem& sm, const Args& a, int W_comp, int g
   ti.rows_valid = min(kBM, sm.start[lo] + sm.count[lo] - ti.r0);
   ti.n0 = s * a.nsplit + nt * kBN;
   ti.cols_valid = min(kBN, (s + 1) * a.nsplit - ti.n0);
+  ti.ny0 = s * y_split_pitch(a) + nt * kBN;
   return ti;
 }
 
@@ -719,6 +752,7 @@ __device__ TileInfo decode_band_tile(const Smem& sm, const KArgs& a, int g) {
   ti.rows_valid = min(kBM, sm.count[lo] - i * kBM);
   ti.n0 = nt * kBN;
   ti.cols_valid = min(kBN, a.H - ti.n0);
+  ti.ny0 = ti.n0;
   return ti;
 }
 
@@ -812,7 +846,7 @@ __device__ __forceinline__ void boundary_steps(f32x16 (&acc)[kNB][kMB], bf16x8 (
 __device__ __forceinline__ void epilogue_store(Smem& sm, const KArgs& a, f32x16 (&acc)[kNB][kMB],
                                                int eslot, int lane, int wave, int wn0, int wm0,
                                                const TileInfo& ti) {
-  const int rows_valid = ti.rows_valid, cols_valid = ti.cols_valid, r0 = ti.r0, n0 = ti.n0;
+  const int rows_valid = ti.rows_valid, cols_valid = ti.cols_valid, r0 = ti.r0;
   // The wave's kWM x kWN block goes through LDS one 32-row m-block at a
   // time (4 KB per wave, all eight in the x part of slot eslot, so that its
   // W2 part can take the next tile's stage already) as bf16 rows of 2 kWN
@@ -858,7 +892,7 @@ __device__ __forceinline__ void epilogue_store(Smem& sm, const KArgs& a, f32x16 
       const bf16x8 v =
           *(const __attribute__((address_space(3))) bf16x8*)(ep + row * kWN + ((j ^ sw) << 3));
       if (n_ok && m < rows_valid)
-        store16_nt(a.Y + (size_t)(r0 + m) * a.ypitch + n0 + n, __builtin_bit_cast(u32x4, v));
+        store16_nt(a.Y + (size_t)(r0 + m) * a.ypitch + ti.ny0 + n, __builtin_bit_cast(u32x4, v));
     }
   }
 }
@@ -1098,11 +1132,7 @@ __device__ void load_task_meta(Smem& sm, TaskMeta& m, const KArgs& a, u64 cnt_ep
     int r = 0;
     float g = 0.f;
     if (j < n) {
-      // token bands: no acquire precedes these reads (it would invalidate
-      // the L2 under the compute workgroups), so they are agent-coherent
-      r = bands ? __hip_atomic_load(&a.inv[(long long)(t0 + t) * K + j], __ATOMIC_RELAXED,
-                                    __HIP_MEMORY_SCOPE_AGENT)
-                : a.inv[(long long)(t0 + t) * K + j];
+      r = a.inv[(long long)(t0 + t) * K + j];
       g = a.gate_w[r];
       if (bands) atomicMax(&sm.task_band, band_of_row(sm, a, r));
     }
@@ -1147,13 +1177,10 @@ __device__ __forceinline__ void fma4(float (&acc)[4], float g, const u32x2& v) {
 // (a padding row j >= n re-reads row n-1 and gets weight 0), then the FMAs
 // in ascending row order.  n >= 1 for both tokens; every row read is one
 // this launch has written, so its values are finite and weight 0 adds 0.
-// kCoherent: the loads are agent-coherent (they miss any stale copy in this
-// XCD's caches), for consumers that read Y without an acquire.
-constexpr int kCoherentStream = 16 | 2;   // buffer load cache policy: sc1 nt
-template <int U, bool kCoherent>
+template <int U>
 __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&rs)[2],
                                             const int (&gs)[2], const int (&n)[2],
-                                            const int (&col)[kColBlocks],
+                                            const int (&col)[kColBlocks], int ydelta,
                                             float (&acc)[2][kColBlocks][4]) {
   u32x2 v[2][U][kColBlocks];
 #pragma unroll
@@ -1161,19 +1188,11 @@ __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = j0 + u < n[p] ? j0 + u : n[p] - 1;
-      const uint16_t* yr = a.Y + (size_t)__builtin_amdgcn_readlane(rs[p], j) * a.ypitch;
-      if constexpr (kCoherent) {
-        // one row of Y as a buffer (wave-uniform base), 32-bit column offsets
-        const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)yr, (short)0, a.ypitch * 2, 0x00020000);
+      const uint16_t* yr =
+          a.Y + (size_t)__builtin_amdgcn_readlane(rs[p], j) * a.ypitch + ydelta;
 #pragma unroll
-        for (int b = 0; b < kColBlocks; ++b)
-          v[p][u][b] = __builtin_amdgcn_raw_buffer_load_b64(rr, 2 * col[b], 0, kCoherentStream);
-      } else {
-#pragma unroll
-        for (int b = 0; b < kColBlocks; ++b)
-          v[p][u][b] = __builtin_nontemporal_load((const u32x2*)(yr + col[b]));
-      }
+      for (int b = 0; b < kColBlocks; ++b)
+        v[p][u][b] = __builtin_nontemporal_load((const u32x2*)(yr + col[b]));
     }
 #pragma unroll
   for (int p = 0; p < 2; ++p)
@@ -1190,9 +1209,10 @@ __device__ __forceinline__ void gather_step(const KArgs& a, int j0, const int (&
 // m: wave w takes the token pairs w, w+nwaves, ...; lane l owns columns
 // 256b + 4l .. 256b + 4l + 3 of every block b, so each output store of a
 // wave writes 1 KB of one row contiguously (whole cache lines).
-template <bool kCoherent>
+// ydelta: Y column minus output column for the task's columns (its split's
+// segment of a Y row starts on a line).
 __device__ void consume_task(const KArgs& a, const TaskMeta& m, int t0, int ntok, int col0,
-                             int ncols) {
+                             int ncols, int ydelta) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
@@ -1237,13 +1257,13 @@ __device__ void consume_task(const KArgs& a, const TaskMeta& m, int t0, int ntok
     for (int j0 = 0; j0 < nmax; j0 += 8) {
       const int left = nmax - j0;
       if (left <= 2)
-        gather_step<2, kCoherent>(a, j0, rl, gl, nl, col, acc);
+        gather_step<2>(a, j0, rl, gl, nl, col, ydelta, acc);
       else if (left <= 4)
-        gather_step<4, kCoherent>(a, j0, rl, gl, nl, col, acc);
+        gather_step<4>(a, j0, rl, gl, nl, col, ydelta, acc);
       else if (left <= 6)
-        gather_step<6, kCoherent>(a, j0, rl, gl, nl, col, acc);
+        gather_step<6>(a, j0, rl, gl, nl, col, ydelta, acc);
       else
-        gather_step<8, kCoherent>(a, j0, rl, gl, nl, col, acc);
+        gather_step<8>(a, j0, rl, gl, nl, col, ydelta, acc);
     }
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
@@ -1288,7 +1308,7 @@ __device__ void scatter_tile(const KArgs& a, const TileInfo& ti) {
       const long long r = (long long)ti.r0 + m;
       tok[u] = a.token_ids[r];
       g[u] = m0 + u < ti.rows_valid ? a.gate_w[r] : 0.f;
-      const uint16_t* yr = a.Y + r * a.ypitch + ti.n0;
+      const uint16_t* yr = a.Y + r * a.ypitch + ti.ny0;
 #pragma unroll
       for (int i = 0; i < kCols; ++i) {
         const int c = lane + 64 * i;
@@ -1348,7 +1368,7 @@ __device__ void run_task(Smem& sm, const KArgs& a, int W_comp, int tps, int s, i
     const int col0 = s * a.nsplit + cb * a.comm_tn;
     const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
     ensure_task_meta(sm, a, idx, cs);
-    consume_task<false>(a, task_meta(sm), t0, ntok, col0, ncols);
+    consume_task(a, task_meta(sm), t0, ntok, col0, ncols, s * (a.ysplit - a.nsplit));
   }
   if (a.trace) {
     __syncthreads();
@@ -1414,16 +1434,14 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
 // Token bands (mode 2): one task counter over all tasks (token block major,
 // then column block of the full width).  A task waits until every tile of
 // the bands up to the last one holding its rows is published: the flags of
-// the band sequence's prefix [0, band_start[b+1]), polled incrementally.
-// Nothing here acquires (an acquire would invalidate the XCD's L2 under the
-// compute workgroups still running there): the inverse map and Y are read
-// with agent-coherent loads, which see the data the compute workgroups'
-// releases wrote back.
+// the band sequence's prefix [0, band_start[b+1]), polled incrementally,
+// with one acquire per newly published prefix (and one for the inverse map,
+// which a task's band requirement is computed from).
 __device__ void consumer_loop_bands(Smem& sm, const KArgs& a, Consumer& cs) {
   const int total = sm.band_start[a.L];
   if (total > a.max_tiles) return;
   if (!cs.inv_ok) {
-    if (!wait_flags(sm, a.wg_flags, gridDim.x, a, false)) return;
+    if (!wait_flags(sm, a.wg_flags, gridDim.x, a)) return;
     cs.inv_ok = true;
   }
   const int ntasks = a.tasks_per_split;
@@ -1445,12 +1463,12 @@ __device__ void consumer_loop_bands(Smem& sm, const KArgs& a, Consumer& cs) {
     const int ncols = min(a.comm_tn, a.H - col0);
     ensure_task_meta(sm, a, idx, cs);
     const int need = sm.band_start[min(sm.task_band, a.L - 1) + 1];
-    if (need > cs.ready) {   // cs.ready: tiles [0, ready) are known published
-      if (!wait_flags(sm, a.tile_flags + cs.ready, need - cs.ready, a, false)) return;
+    if (need > cs.ready) {   // cs.ready: tiles [0, ready) are published and acquired
+      if (!wait_flags(sm, a.tile_flags + cs.ready, need - cs.ready, a)) return;
       cs.ready = need;
     }
     const u64 t_go = now_100mhz();
-    consume_task<true>(a, task_meta(sm), t0, ntok, col0, ncols);
+    consume_task(a, task_meta(sm), t0, ntok, col0, ncols, 0);
     if (a.trace) {
       __syncthreads();
       if (threadIdx.x == 0) {
@@ -1560,7 +1578,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
         }
         __syncthreads();
         if (threadIdx.x == 0) {
-          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+          release_agent();
           const uint32_t epoch = flag_epoch(sm);
           for (int gg = split_first; gg <= g; gg += a.P)
             __hip_atomic_store(&a.tile_flags[gg], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1672,10 +1690,12 @@ __global__ void pack_w1_kernel(const uint16_t* src, uint16_t* dst, long long n, 
   }
 }
 
-__global__ void fill_zero_kernel(uint32_t* p, size_t n) {
+// Zeroes n words at p, except the 64-bit word at word index epoch_at (when
+// epoch_at + 1 < n), which takes `epoch`.
+__global__ void fill_zero_kernel(uint32_t* p, size_t n, size_t epoch_at, u64 epoch) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (size_t)gridDim.x * blockDim.x)
-    p[i] = 0u;
+    p[i] = i == epoch_at ? (uint32_t)epoch : i == epoch_at + 1 ? (uint32_t)(epoch >> 32) : 0u;
 }
 
 // ---- host side -----------------------------------------------------------------
@@ -1742,7 +1762,10 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   L->inv = off;
   off = round_up(off + (size_t)wl->T * wl->topk * 8, 256);
   L->Y = off;
-  off = round_up(off + (size_t)L->rows * (wl->H + kYPad) * 2, 256);
+  // rows of L line-aligned split segments plus the padding (token bands use
+  // one segment of round_up(H) <= L round_up(ceil(H/L)) elements)
+  off = round_up(off + (size_t)L->rows * ((size_t)wl->splits * round_up_line(L->nsplit) + kYPad) * 2,
+                 256);
   L->total = off;
   return true;
 }
@@ -1801,7 +1824,7 @@ constexpr int64_t kRhoRefDen = 100;
 // rows), measured the same way: 26.2 us / 22.3 us = 1.18.
 constexpr int64_t kRhoScatterNum = 118;
 constexpr int64_t kRhoScatterDen = 100;
-// The same for token bands (mode 2, agent-coherent reads of Y), 64-token
+// The same for token bands (mode 2), 64-token
 // tasks over 1024 columns.
 constexpr int64_t kRhoBandsNum = 149;
 constexpr int64_t kRhoBandsDen = 100;
@@ -1931,13 +1954,34 @@ int scratch_on_device(int dev, ScratchDev** out) {
   return MOE_OK;
 }
 
-// Zeroes `bytes` (a multiple of 4) at p on stream with a fill kernel (no
-// memset node, so that a captured graph replays it correctly).
+// The launch epoch a freshly zeroed workspace starts from.  Readiness flags
+// hold the low 32 bits of a launch's epoch, and a flag left by an earlier
+// use of the same memory (another workspace at a reused address, or this
+// workspace before a re-initialisation) must never equal a new launch's
+// epoch, also where a stale copy of it may still be visible: so every
+// initialisation starts 2^20 launches past the previous one, from a
+// per-process random origin, and never at the zeroed state.  Epochs stay
+// in [2^32, 2^33 + 2^32), far below the 2^40 at which the per-token
+// counters' epoch tags would wrap.
+std::atomic<uint64_t> g_epoch_inits{0};
+uint64_t fresh_epoch_base() {
+  static const uint64_t origin = [] {
+    std::random_device rd;
+    return ((uint64_t)rd() << 16) ^ (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
+  }();
+  const uint64_t k = g_epoch_inits.fetch_add(1, std::memory_order_relaxed);
+  return (1ull << 32) | ((origin + (k << 20)) & 0xffffffffull);
+}
+constexpr size_t kEpochWordIndex = 320 / 4;   // the header's launch-epoch word (bytes 320..327)
+
+// Zeroes `bytes` (a multiple of 4) at workspace p on stream with a fill
+// kernel (no memset node, so that a captured graph replays it correctly),
+// and gives the workspace a fresh launch epoch.
 hipError_t zero_async(void* p, size_t bytes, hipStream_t stream) {
   const size_t words = bytes / 4;
   const unsigned blocks = (unsigned)((words + 255) / 256 < 4096 ? (words + 255) / 256 : 4096);
   hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks ? blocks : 1), dim3(256), 0, stream,
-                     static_cast<uint32_t*>(p), words);
+                     static_cast<uint32_t*>(p), words, kEpochWordIndex, fresh_epoch_base());
   return hipGetLastError();
 }
 
@@ -2066,7 +2110,8 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   }
   a.T = wl->T;
   a.H = wl->H;
-  a.ypitch = wl->H + kYPad;
+  a.ysplit = round_up_line(L.nsplit);
+  a.ypitch = wl->splits * a.ysplit + kYPad;
   a.I = wl->I;
   a.E = wl->E;
   a.topk = wl->topk;
@@ -2085,6 +2130,8 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
     const BandTasks bt = band_tasks(wl);
     a.nsplit = wl->H;
     a.ntps = (wl->H + kBN - 1) / kBN;
+    a.ysplit = round_up_line(wl->H);   // one segment; fits the column-split layout
+    a.ypitch = a.ysplit + kYPad;
     a.comm_tm = bt.comm_tm;
     a.comm_tn = bt.comm_tn;
     a.cb_per_split = bt.cb;
