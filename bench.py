@@ -93,30 +93,40 @@ class DevWorkload:
         self.g = torch.from_numpy(w.gate_w).to(dev)
         self.out = torch.empty((w.T, w.H), dtype=torch.float32, device=dev)
         self.wl, self._keep = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, w.counts)
-        self.ws = B.Workspace(B.workspace_size(self.wl))
+        # sized for every split count up to 8 (token-band sweeps vary L)
+        wl8, _ = B.make_workload(w.T, w.H, w.I, w.E, w.topk, 8, w.counts)
+        self.ws = B.Workspace(max(B.workspace_size(self.wl), B.workspace_size(wl8)))
 
-    def run(self, C=-1, trace=None, mode=None):
-        """One launch; mode None is moe_gemm2_combine (owner-write), 0/1 go
-        through moe_gemm2_combine_ex."""
+    def workload(self, splits=None):
+        return self.B.make_workload(self.w.T, self.w.H, self.w.I, self.w.E, self.w.topk,
+                                    splits or self.w.L, self.w.counts)
+
+    def run(self, C=-1, trace=None, mode=None, splits=None):
+        """One launch; mode None is moe_gemm2_combine (owner-write, column
+        splits), 0/1/2 go through moe_gemm2_combine_ex."""
         w = self.w
-        return self.B.combine(self.x, self.w2, self.off, self.tid, self.g, T=w.T, splits=w.L,
-                              topk=w.topk, counts=w.counts, num_consumers=C, out=self.out,
-                              workspace=self.ws, trace=trace, mode=mode)[1]
+        return self.B.combine(self.x, self.w2, self.off, self.tid, self.g, T=w.T,
+                              splits=splits or w.L, topk=w.topk, counts=w.counts,
+                              num_consumers=C, out=self.out, workspace=self.ws, trace=trace,
+                              mode=mode)[1]
 
-    def trace(self, C, mode=None):
-        """One traced launch: (C used, tiles [n,4], tasks [m,4]) timestamps."""
+    def trace(self, C, mode=None, splits=None):
+        """One traced launch: (C used, tiles [n,4], tasks [m,4]) timestamps
+        (tile records in global tile order, task records in task order)."""
         torch, B, w = self.torch, self.B, self.w
-        buf = torch.zeros(B.trace_size(self.wl) // 8, dtype=torch.int64, device="cuda")
-        used = self.run(C, trace=buf, mode=mode)
+        L = splits or w.L
+        wl, _keep = self.workload(L)
+        buf = torch.zeros(B.trace_size(wl) // 8, dtype=torch.int64, device="cuda")
+        used = self.run(C, trace=buf, mode=mode, splits=L)
         torch.cuda.synchronize()
         tr = buf.cpu().numpy().astype(np.int64)
-        part = B.select_partition(self.wl, B.launch_params(self.wl, mode or 0))[1]
-        n_tiles = int(part.W_comp) * w.L
-        ntasks = n_tiles if mode == 1 else int(part.W_comm) * w.L
-        # tile records first (room for max_tiles), then the task records
-        max_tiles = w.L * (-(-(w.H // w.L) // 256)) * (-(-w.Mtot // 256) + w.E)
-        tiles = tr[: 4 * n_tiles].reshape(-1, 4)
-        tasks = tr[4 * max_tiles: 4 * (max_tiles + ntasks)].reshape(-1, 4)
+        max_tiles = L * (-(-(-(-w.H // L)) // 256)) * (-(-w.Mtot // 256) + w.E)
+        tiles = tr[: 4 * max_tiles].reshape(-1, 4)
+        n_tiles = int(np.flatnonzero(tiles[:, 3])[-1]) + 1 if tiles[:, 3].any() else 0
+        tiles = tiles[:n_tiles]
+        tasks = tr[4 * max_tiles:].reshape(-1, 4)
+        n_tasks = int(np.flatnonzero(tasks[:, 2])[-1]) + 1 if tasks[:, 2].any() else 0
+        tasks = tasks[:n_tasks]
         return used, tiles, tasks
 
 
@@ -165,84 +175,249 @@ def calibrate(dw, C_ref=32, reps=5, mode=None):
             "consumer_wave_us": round(task_us, 3), "rho_ref": round(task_us / tile_us, 4)}
 
 
-def time_launches(dw, Cs, samples, torch):
-    """Median event time per C, samples interleaved forward/backward (ABBA).
-    A C may be a (C, mode) pair to time moe_gemm2_combine_ex in that mode."""
+def time_launches(dw, Cs, samples, torch, warmups=1):
+    """Median event time per configuration (ms), samples interleaved
+    forward/backward (ABBA).  A configuration is C, or (C, mode) to time
+    moe_gemm2_combine_ex in that mode, or (C, mode, splits)."""
+    t = time_configs(lambda c: launch_cfg(dw, c), list(Cs), samples, warmups, torch)
+    return {c: float(np.median(v)) / 1e3 for c, v in t.items()}
+
+
+def launch_cfg(dw, c):
+    if isinstance(c, tuple):
+        return dw.run(c[0], mode=c[1], splits=c[2] if len(c) > 2 else None)
+    return dw.run(c)
+
+
+def time_configs(launch, keys, samples, warmups, torch):
+    """Event time (us) of every key, `samples` times each: `warmups`
+    untimed passes over all keys, then passes alternately forward and
+    backward over the keys (ABBA), one stream synchronisation per pass."""
     stream = torch.cuda.current_stream()
-    times = {C: [] for C in Cs}
-
-    def launch(C):
-        return dw.run(C[0], mode=C[1]) if isinstance(C, tuple) else dw.run(C)
-
-    for C in Cs:               # warm-up of every partition
-        launch(C)
+    for _ in range(warmups):
+        for k in keys:
+            launch(k)
     torch.cuda.synchronize()
+    times = {k: [] for k in keys}
     for s in range(samples):
-        order = list(Cs) if s % 2 == 0 else list(reversed(Cs))
+        order = keys if s % 2 == 0 else keys[::-1]
         evs = []
-        for C in order:
+        for k in order:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            launch(C)
+            launch(k)
             b.record(stream)
-            evs.append((C, a, b))
+            evs.append((k, a, b))
         torch.cuda.synchronize()
-        for C, a, b in evs:
-            times[C].append(a.elapsed_time(b))
-    return {C: float(np.median(v)) for C, v in times.items()}
+        for k, a, b in evs:
+            times[k].append(a.elapsed_time(b) * 1e3)
+    return times
 
 
-def run_sweep(B, torch, samples, c_max=64):
-    """Time every C in 0..c_max on the 12 sweep workloads; compare the
-    selector's pick with the fastest (regret = (t_pick - t_best) / t_best).
-    The library's candidate set is 0..64 (C = 0: role switch); the paper's
-    legal set is 1..C_max, reported separately."""
-    from workloads import sweep_workload, sweep_workloads
-    base_params = B.default_params(0)
-    rows = []
-    for name, _ in sweep_workloads():
+def median_ci(v, reps=1000, seed=0):
+    """Median and a bootstrap 95% confidence interval of the median (us)."""
+    v = np.asarray(v, dtype=np.float64)
+    rng = np.random.default_rng(seed)
+    meds = np.median(v[rng.integers(0, len(v), size=(reps, len(v)))], axis=1)
+    return (float(np.median(v)), float(np.percentile(meds, 2.5)),
+            float(np.percentile(meds, 97.5)))
+
+
+def _pick(stats, keys):
+    """The key with the least median among keys."""
+    return min(keys, key=lambda k: stats[k][0])
+
+
+def _regret(stats, pick, best):
+    return (stats[pick][0] - stats[best][0]) / stats[best][0]
+
+
+def _agg(v):
+    return {"mean": round(float(np.mean(v)), 4), "max": round(float(np.max(v)), 4)}
+
+
+class SweepPoint:
+    """A sweep workload on the device, its selector picks and its timings."""
+
+    def __init__(self, name, B, torch):
+        from workloads import sweep_workload
+        self.name = name
         w = sweep_workload(name, with_tensors=False)
-        log(f"sweep {name}: rows={w.Mtot} r_expert={w.r_expert:.2f}")
-        dw = DevWorkload(w, B, torch, synth_tensors=True)
-        params = B.launch_params(dw.wl)        # what a launch with C = -1 uses
-        params_paper = B.launch_params(dw.wl)
-        params_paper.c_min = 1
-        Cs = list(range(0, c_max + 1))
-        med = time_launches(dw, Cs, samples, torch)
-        best_all = min(Cs, key=lambda c: med[c])
-        best_dom = min(Cs[1:], key=lambda c: med[c])
-        pick = B.select_partition(dw.wl, params)[0]
-        pick_p = B.select_partition(dw.wl, params_paper)[0]
-        # the selector without the routed counts (even-load estimate), as a
-        # launch that reads nothing back from the device would run it
-        wl_est, _ = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, None)
-        pick_e = B.select_partition(wl_est, B.launch_params(wl_est))[0]
-        rows.append({
-            "workload": name, "T": w.T, "r_expert": round(w.r_expert, 3),
-            "task_tokens": params.comm_tile_m,
-            "best_C": best_all, "best_us": round(med[best_all] * 1e3, 1),
-            "pick_C": pick, "pick_us": round(med[pick] * 1e3, 1),
-            "regret": round((med[pick] - med[best_all]) / med[best_all], 4),
-            "pick_C_estimate": pick_e, "pick_us_estimate": round(med[pick_e] * 1e3, 1),
-            "regret_estimate": round((med[pick_e] - med[best_all]) / med[best_all], 4),
-            "best_C_1_64": best_dom, "best_us_1_64": round(med[best_dom] * 1e3, 1),
-            "pick_C_paper_set": pick_p, "pick_us_paper_set": round(med[pick_p] * 1e3, 1),
-            "regret_paper_set_vs_best_1_64": round((med[pick_p] - med[best_dom]) / med[best_dom], 4),
-            "us_by_C": {str(c): round(med[c] * 1e3, 1) for c in Cs},
-        })
-        del dw
-        torch.cuda.empty_cache()
+        self.w = w
+        self.dw = DevWorkload(w, B, torch, synth_tensors=True)
+        # the paper's column splits (owner-write), at the selector's pick
+        self.params = B.launch_params(self.dw.wl)
+        self.params_paper = B.launch_params(self.dw.wl)
+        self.params_paper.c_min = 1
+        self.pick = B.select_partition(self.dw.wl, self.params)[0]
+        self.pick_paper = B.select_partition(self.dw.wl, self.params_paper)[0]
+        wl_est, self._k = B.make_workload(w.T, w.H, w.I, w.E, w.topk, w.L, None)
+        self.pick_est = B.select_partition(wl_est, B.launch_params(wl_est))[0]
+        # token bands: (C, L) chosen together over L = 1..4
+        self.params_bands = B.launch_params(self.dw.wl, 2)
+        r, L, _ = B.select_partition_splits(self.dw.wl, self.params_bands, 1, 4)
+        self.pick_bands = (r, 2, L)
 
-    def agg(key):
-        v = [r[key] for r in rows]
-        return {"mean": round(float(np.mean(v)), 4), "max": round(float(np.max(v)), 4)}
 
-    return {"workloads": len(rows), "samples_per_C": samples, "C_range": [0, c_max],
-            "rho_ref_64_token_task": [base_params.rho_ref_num, base_params.rho_ref_den],
-            "regret": agg("regret"),
-            "regret_estimate": agg("regret_estimate"),
-            "regret_paper_set_vs_best_1_64": agg("regret_paper_set_vs_best_1_64"),
-            "per_workload": rows}
+def run_sweep(B, torch, samples, warmups, repeats=2, c_max=64):
+    """The selector sweep: the 12 workloads x C = 0..c_max (owner-write,
+    column splits, as the selector's launch uses), every C timed `samples`
+    times (ABBA) after `warmups` passes; the whole sweep is repeated
+    `repeats` times (independent passes, the second over the workloads in
+    reverse order).  Regret = (t(pick) - t(best)) / t(best) on medians, for
+    the library's candidate set 0..64 and for the paper's 1..64 (against
+    the best in 1..64).  Also the token-band consumer over a grid of (C, L)
+    with the selector's joint (C, L) pick."""
+    from workloads import sweep_workloads
+    names = [n for n, _ in sweep_workloads()]
+    points = []
+    for n in names:
+        log(f"sweep setup {n}")
+        points.append(SweepPoint(n, B, torch))
+    Cs = list(range(0, c_max + 1))
+    band_grid = [(c, 2, L) for L in (1, 2, 3, 4) for c in (0, 1, 2, 4, 8, 16, 24, 32, 48, 64)]
+    runs = []     # per repeat: {name: {key: (median, lo, hi)}}
+    for rep_i in range(repeats):
+        order = points if rep_i % 2 == 0 else points[::-1]
+        res = {}
+        for pt in order:
+            log(f"sweep {rep_i + 1}/{repeats} {pt.name}")
+            keys = Cs + [k for k in band_grid] + ([pt.pick_bands] if pt.pick_bands not in
+                                                  band_grid else [])
+            t = time_configs(lambda c: launch_cfg(pt.dw, c), keys, samples, warmups, torch)
+            assert pt.dw.ws.status() == 0
+            res[pt.name] = {k: median_ci(v) for k, v in t.items()}
+        runs.append(res)
+    rows = []
+    per_rep = {"regret": [], "paper": [], "estimate": [], "bands": []}
+    for pt in points:
+        row = {"w": pt.name, "r_expert": round(pt.w.r_expert, 2)}
+        for ri, res in enumerate(runs):
+            st = res[pt.name]
+            best = _pick(st, Cs)
+            best_dom = _pick(st, Cs[1:])
+            keys_b = band_grid + [pt.pick_bands]
+            best_b = _pick(st, keys_b)
+            r = _regret(st, pt.pick, best)
+            rp = _regret(st, pt.pick_paper, best_dom)
+            re = _regret(st, pt.pick_est, best)
+            rb = _regret(st, pt.pick_bands, best_b)
+            per_rep["regret"].append((ri, r))
+            per_rep["paper"].append((ri, rp))
+            per_rep["estimate"].append((ri, re))
+            per_rep["bands"].append((ri, rb))
+            f = lambda k: [round(x, 1) for x in st[k]]   # noqa: E731
+            row[f"s{ri + 1}"] = {
+                "best": [best] + f(best), "pick": [pt.pick] + f(pt.pick), "regret": round(r, 4),
+                "best_1_64": [best_dom] + f(best_dom),
+                "pick_paper": [pt.pick_paper] + f(pt.pick_paper), "regret_paper": round(rp, 4),
+                "regret_estimate": round(re, 4),
+                "bands_best": [best_b[0], best_b[2]] + f(best_b),
+                "bands_pick": [pt.pick_bands[0], pt.pick_bands[2]] + f(pt.pick_bands),
+                "regret_bands": round(rb, 4),
+                "c0_vs_best_1_64": round(st[0][0] / st[best_dom][0], 4)}
+        rows.append(row)
+
+    def by_rep(key):
+        v = per_rep[key]
+        reps = [_agg([r for i, r in v if i == k]) for k in range(repeats)]
+        allv = [r for _, r in v]
+        return {"mean": round(float(np.mean([x["mean"] for x in reps])), 4),
+                "max": round(float(np.max(allv)), 4),
+                "per_sweep_mean": [x["mean"] for x in reps],
+                "per_sweep_max": [x["max"] for x in reps]}
+
+    summary = {"workloads": len(rows), "samples_per_C": samples, "warmups": warmups,
+               "sweeps": repeats, "C_range": [0, c_max],
+               "regret": by_rep("regret"), "regret_paper_set": by_rep("paper"),
+               "regret_estimate": by_rep("estimate"), "regret_bands": by_rep("bands")}
+    detail = {"per_workload": rows,
+              "us_by_C_sweep1": {pt.name: {str(c): round(runs[0][pt.name][c][0], 1) for c in Cs}
+                                 for pt in points}}
+    return summary, detail, points, runs
+
+
+def model_validation(B, torch, points, runs, Cs):
+    """The makespan model against the measured sweep: T(C) in compute waves
+    times the measured mean tile time (one traced launch at C = 0) against
+    the measured median, per workload; and, on two workloads, the split
+    arrival and finish times A_s, F_s rebuilt from the traced tile and task
+    timestamps at C = 16 and C = 64 against the model's."""
+    out = []
+    for pt in points:
+        dw = pt.dw
+        _, tiles, _ = dw.trace(0)
+        t_tile = float((tiles[:, 3] - tiles[:, 0]).mean()) * TICK_S * 1e6
+        n, table, den = B.select_evaluate(dw.wl, pt.params)
+        pred = {pt.params.c_min + i: table[i] / den * t_tile for i in range(n) if table[i] >= 0}
+        meas = {c: runs[0][pt.name][c][0] for c in Cs}
+        errs = {c: (pred[c] - meas[c]) / meas[c] for c in Cs if c in pred}
+        dom = [c for c in Cs if c >= 1 and c in errs]
+        rank_p = np.argsort(np.argsort([pred[c] for c in dom]))
+        rank_m = np.argsort(np.argsort([meas[c] for c in dom]))
+        rho_s = float(np.corrcoef(rank_p, rank_m)[0, 1])
+        out.append({"w": pt.name, "tile_us": round(t_tile, 2),
+                    "mape_1_64": round(float(np.mean([abs(errs[c]) for c in dom])), 4),
+                    "err_C0": round(errs[0], 4), "err_C16": round(errs[16], 4),
+                    "err_C64": round(errs[64], 4), "spearman_1_64": round(rho_s, 4),
+                    "pred_over_meas_T0_T64": round((pred[0] / pred[64]) / (meas[0] / meas[64]), 4)})
+    splits = []
+    for pt in points:
+        if pt.name not in ("sweep_T16384_uniform", "sweep_T32768_uniform"):
+            continue
+        dw = pt.dw
+        part0 = B.select_partition(dw.wl, pt.params)[1]
+        W_comp, W_comm = int(part0.W_comp), int(part0.W_comm)
+        _, tiles0, _ = dw.trace(0)
+        t_tile = float((tiles0[:, 3] - tiles0[:, 0]).mean()) * TICK_S * 1e6
+        for C in (16, 64):
+            _, tiles, tasks = dw.trace(C)
+            t0 = tiles[:, 0].min()
+            L = dw.w.L
+            A = [float((tiles[s * W_comp:(s + 1) * W_comp, 3].max() - t0) * TICK_S * 1e6)
+                 for s in range(L)]
+            F = [float((tasks[s * W_comm:(s + 1) * W_comm, 2].max() - t0) * TICK_S * 1e6)
+                 for s in range(L)]
+            p = B.SelectParams.from_buffer_copy(pt.params)
+            p.c_min = p.c_max = C
+            cands = __import__("oracle.selector", fromlist=["x"])
+            best, _, _, _, rho = cands.select(dw.w.T, dw.w.H, dw.w.I, dw.w.E, dw.w.topk, L,
+                                              dw.w.counts, _oracle_params(p))
+            splits.append({"w": pt.name, "C": C,
+                           "A_us_meas": [round(x, 1) for x in A],
+                           "A_us_model": [round(a * t_tile, 1) for a in best.A],
+                           "F_us_meas": [round(x, 1) for x in F],
+                           "F_us_model": [round(float(f) * t_tile, 1) for f in best.F]})
+    return {"per_workload": out,
+            "mape_1_64_mean": round(float(np.mean([o["mape_1_64"] for o in out])), 4),
+            "err_C0_mean": round(float(np.mean([o["err_C0"] for o in out])), 4),
+            "spearman_1_64_mean": round(float(np.mean([o["spearman_1_64"] for o in out])), 4),
+            "split_times": splits}
+
+
+def _oracle_params(p):
+    from fractions import Fraction
+
+    from oracle import selector as osel
+    return osel.SelectParams(
+        tile_m=p.tile_m, tile_n=p.tile_n, comm_tile_m=p.comm_tile_m, comm_tile_n=p.comm_tile_n,
+        occ_comp=p.occ_comp, occ_comm=p.occ_comm, num_cus=p.num_cus, c_min=p.c_min,
+        c_max=p.c_max, rho_ref=Fraction(p.rho_ref_num, p.rho_ref_den), k_ref=p.k_ref,
+        tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups,
+        split_axis=p.split_axis, drain=bool(p.drain))
+
+
+def saturation(B, torch, samples, warmups, name="sweep_T16384_uniform"):
+    """C past the paper-set bound of 64 on a workload whose time still falls
+    at C = 64: where does T(C) stop falling (the one-time saturation
+    characterisation that sets C_max)?"""
+    pt = SweepPoint(name, B, torch)
+    Cs = [32, 48, 56, 64, 72, 80, 96, 112, 128, 160, 192]
+    t = time_configs(lambda c: pt.dw.run(c), Cs, samples, warmups, torch)
+    st = {c: median_ci(v) for c, v in t.items()}
+    best = _pick(st, Cs)
+    return {"w": name, "us_by_C": {str(c): [round(x, 1) for x in st[c]] for c in Cs},
+            "best_C": best, "best_us": round(st[best][0], 1)}
 
 
 def layer_measure(dw, B, torch, samples=20):
@@ -333,11 +508,20 @@ def cpu_baseline(w, budget_s=12.0):
             break
     per = el / n
     flops = 2 * w.Mtot * w.I * w.H
+    # the per-token brute force (one vector-matrix product per routed row)
+    # on the tiny configuration, where it runs in full
+    from workloads import config
+    wt = config("tiny")
+    t0 = time.perf_counter()
+    oc.combine_bruteforce(wt.x_perm, wt.w2, wt.expert_offsets, wt.token_ids, wt.gate_w, wt.T)
+    bf_s = time.perf_counter() - t0
     return {"value": round(flops / per / 1e12, 4), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"whole {w.name} workload (numpy fp32 per-expert matmul + per-token "
                       f"weighted sum), {n} run(s), {per * 1e3:.1f} ms each; "
-                      f"host os.cpu_count()={os.cpu_count()}"}
+                      f"host os.cpu_count()={os.cpu_count()}",
+            "bruteforce_tiny": {"seconds": round(bf_s, 3), "tokens": wt.T, "rows": wt.Mtot,
+                                "tflops": round(2 * wt.Mtot * wt.I * wt.H / bf_s / 1e12, 5)}}
 
 
 def main():
@@ -349,7 +533,16 @@ def main():
     ap.add_argument("--consumers", type=int, default=-1)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
-    ap.add_argument("--sweep-samples", type=int, default=7)
+    ap.add_argument("--sweep-samples", type=int, default=30,
+                    help="timed samples per configuration in the selector sweep (ABBA)")
+    ap.add_argument("--sweep-warmups", type=int, default=20,
+                    help="untimed passes over all configurations before the samples")
+    ap.add_argument("--sweep-repeats", type=int, default=2,
+                    help="independent repetitions of the whole sweep")
+    ap.add_argument("--no-validate", action="store_true",
+                    help="skip the model-against-measurement validation and the C_max sweep")
+    ap.add_argument("--detail-out", default="",
+                    help="write the per-workload sweep tables (JSON) to this path")
     ap.add_argument("--calibrate", action="store_true",
                     help="print the rho_ref calibration at C=32 (both consumer modes) and exit")
     ap.add_argument("--no-layer", action="store_true",
@@ -388,9 +581,11 @@ def main():
     if args.calibrate:
         dw.run(32)
         dw.run(32, mode=1)
+        dw.run(32, mode=2)
         torch.cuda.synchronize()
         print(json.dumps({"calibration": calibrate(dw),
                           "calibration_scatter": calibrate(dw, mode=1),
+                          "calibration_bands": calibrate(dw, mode=2),
                           "kernel_sha": kernel_sha()}), flush=True)
         return
     stream = torch.cuda.current_stream()
@@ -530,7 +725,30 @@ def main():
         del dw
         torch.cuda.empty_cache()
         log("selector sweep")
-        res["sweep"] = run_sweep(B, torch, args.sweep_samples)
+        summary, detail, points, runs = run_sweep(B, torch, args.sweep_samples,
+                                                  args.sweep_warmups, args.sweep_repeats)
+        # short top-level keys first, so that a truncated line still has them
+        head = {"sweep_regret": {k: summary["regret"][k] for k in ("mean", "max")},
+                "sweep_regret_paper_set": {k: summary["regret_paper_set"][k]
+                                           for k in ("mean", "max")},
+                "sweep_regret_bands": {k: summary["regret_bands"][k] for k in ("mean", "max")}}
+        res = {**{k: res[k] for k in list(res)[:13]}, **head,
+               **{k: res[k] for k in list(res)[13:]}}
+        res["sweep"] = summary
+        if not args.no_validate:
+            log("model against measurement")
+            res["model_validation"] = model_validation(B, torch, points, runs,
+                                                       list(range(0, 65)))
+        del points
+        torch.cuda.empty_cache()
+        if not args.no_validate:
+            log("C past 64")
+            res["c_max_saturation"] = saturation(B, torch, args.sweep_samples,
+                                                 args.sweep_warmups)
+        if args.detail_out:
+            detail["model_validation"] = res.get("model_validation")
+            with open(args.detail_out, "w") as f:
+                json.dump(detail, f)
     if not args.no_cpu:
         log("timing the CPU oracle")
         res["cpu_baseline"] = cpu_baseline(w)
