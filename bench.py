@@ -333,7 +333,10 @@ def run_sweep(B, torch, samples, warmups, repeats=2, c_max=64):
                "regret_estimate": by_rep("estimate"), "regret_bands": by_rep("bands")}
     detail = {"per_workload": rows,
               "us_by_C_sweep1": {pt.name: {str(c): round(runs[0][pt.name][c][0], 1) for c in Cs}
-                                 for pt in points}}
+                                 for pt in points},
+              "bands_us_by_C_L": [{pt.name: {f"C{k[0]}_L{k[2]}": round(res[pt.name][k][0], 1)
+                                             for k in band_grid + [pt.pick_bands]}
+                                   for pt in points} for res in runs]}
     return summary, detail, points, runs
 
 
