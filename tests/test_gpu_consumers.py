@@ -157,3 +157,33 @@ def test_workspace_reused_across_layouts(gpu_lib):
                 print(f"relayout round {rnd} shape {i} C={C} mode={mode}", flush=True)
                 got, used, ws = gpu_util.run(w, C=C, workspace=ws, mode=mode)
                 _check(got, ref, f"shape {i} C={C} mode={mode}")
+
+
+def test_fresh_workspaces_read_published_y_only(gpu_lib):
+    """Regression for the readiness publish: a compute workgroup's release
+    writes back the L2 and must wait for that write-back before it stores
+    the flags, or a consumer on another XCD may read Y before it arrives.
+    With a fresh (zeroed) workspace per launch such a read returns the
+    workspace's zeros instead of the previous launch's identical Y, so the
+    output differs.  Shapes whose tiles are a single reduction stage (I = 40)
+    or have a partial width (H = 200) publish soonest after their stores;
+    every launch must be bitwise equal to the first (mode 0 and token bands,
+    dedicated consumers and the role switch)."""
+    import gpu_util
+    cases = [
+        (custom(T=257, H=264, I=40, E=5, topk=2, L=1, routing=("uniform",), seed=13),
+         [(0, None, None), (3, None, None)], 150),
+        (custom(T=129, H=200, I=72, E=4, topk=2, L=1, routing=("zipf", 1.0), seed=13),
+         [(5, 2, 5), (0, 2, 5)], 100),
+    ]
+    for w, cfgs, reps in cases:
+        ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+        dev = gpu_util.to_device(w)
+        base, _, _ = gpu_util.run(w, C=0, dev=dev)
+        _check(base, ref, f"fresh T={w.T} H={w.H} I={w.I} base")
+        for C, mode, L in cfgs:
+            print(f"fresh workspaces T={w.T} H={w.H} I={w.I} C={C} mode={mode} L={L} x{reps}",
+                  flush=True)
+            for it in range(reps):
+                got, _, _ = gpu_util.run(w, C=C, dev=dev, mode=mode, splits=L)
+                assert np.array_equal(got.view(np.uint32), base.view(np.uint32)), (C, mode, L, it)
