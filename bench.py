@@ -381,16 +381,13 @@ def model_validation(B, torch, points, runs, Cs):
                  for s in range(L)]
             F = [float((tasks[s * W_comm:(s + 1) * W_comm, 2].max() - t0) * TICK_S * 1e6)
                  for s in range(L)]
-            p = B.SelectParams.from_buffer_copy(pt.params)
-            p.c_min = p.c_max = C
-            cands = __import__("oracle.selector", fromlist=["x"])
-            best, _, _, _, rho = cands.select(dw.w.T, dw.w.H, dw.w.I, dw.w.E, dw.w.topk, L,
-                                              dw.w.counts, _oracle_params(p))
+            # the model's A_s and F_s of this candidate, as the library evaluates them
+            _, _, den, A_m, F_m = B.select_candidate(dw.wl, pt.params, C)
             splits.append({"w": pt.name, "C": C,
                            "A_us_meas": [round(x, 1) for x in A],
-                           "A_us_model": [round(a * t_tile, 1) for a in best.A],
+                           "A_us_model": [round(a / den * t_tile, 1) for a in A_m],
                            "F_us_meas": [round(x, 1) for x in F],
-                           "F_us_model": [round(float(f) * t_tile, 1) for f in best.F]})
+                           "F_us_model": [round(f / den * t_tile, 1) for f in F_m]})
     return {"per_workload": out,
             "mape_1_64_mean": round(float(np.mean([o["mape_1_64"] for o in out])), 4),
             "err_C0_mean": round(float(np.mean([o["err_C0"] for o in out])), 4),
@@ -398,16 +395,44 @@ def model_validation(B, torch, points, runs, Cs):
             "split_times": splits}
 
 
-def _oracle_params(p):
-    from fractions import Fraction
-
-    from oracle import selector as osel
-    return osel.SelectParams(
-        tile_m=p.tile_m, tile_n=p.tile_n, comm_tile_m=p.comm_tile_m, comm_tile_n=p.comm_tile_n,
-        occ_comp=p.occ_comp, occ_comm=p.occ_comm, num_cus=p.num_cus, c_min=p.c_min,
-        c_max=p.c_max, rho_ref=Fraction(p.rho_ref_num, p.rho_ref_den), k_ref=p.k_ref,
-        tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups,
-        split_axis=p.split_axis, drain=bool(p.drain))
+def rho_validation(B, torch, reps=5, C_ref=32):
+    """rho measured on each configuration by the calibration procedure (mean
+    consumer-task time over mean compute-tile time in traced launches at
+    C = 32) against the rho the selector would use (the library's, from
+    moe_select_candidate): eq:rho-scaling from the calibration on the
+    DeepSeek-V2-Lite-like share (with the task-token factor of the launch),
+    and the same with the k/H-aware extension (rho_kh = 1)."""
+    from workloads import config
+    rows = []
+    for name in ("tiny", "granite", "qwen", "dsv2lite"):
+        w = config(name)
+        dw = DevWorkload(w, B, torch)
+        for _ in range(3):
+            dw.run(C_ref)
+        torch.cuda.synchronize()
+        task_t, tile_t = [], []
+        for _ in range(reps):
+            _, tiles, tasks = dw.trace(C_ref)
+            tile_t.append((tiles[:, 3] - tiles[:, 0]).mean())
+            task_t.append((tasks[:, 2] - tasks[:, 1]).mean())
+        tile_us = float(np.median(tile_t)) * TICK_S * 1e6
+        task_us = float(np.median(task_t)) * TICK_S * 1e6
+        p = B.launch_params(dw.wl)
+        p.rho_kh = 0
+        _, n0, d0, _, _ = B.select_candidate(dw.wl, p, 0)
+        p.rho_kh = 1
+        _, n1, d1, _, _ = B.select_candidate(dw.wl, p, 0)
+        paper, kh = n0 / d0, n1 / d1
+        meas = task_us / tile_us
+        rows.append({"w": name, "I": w.I, "topk": w.topk, "task_tokens": p.comm_tile_m,
+                     "tile_us": round(tile_us, 2), "task_us": round(task_us, 2),
+                     "rho_measured": round(meas, 3), "rho_paper": round(float(paper), 3),
+                     "rho_kh": round(float(kh), 3),
+                     "err_paper": round(float(paper) / meas - 1, 3),
+                     "err_kh": round(float(kh) / meas - 1, 3)})
+        del dw
+        torch.cuda.empty_cache()
+    return rows
 
 
 def saturation(B, torch, samples, warmups, name="sweep_T16384_uniform"):
@@ -748,6 +773,8 @@ def main():
             log("C past 64")
             res["c_max_saturation"] = saturation(B, torch, args.sweep_samples,
                                                  args.sweep_warmups)
+            log("rho across the configurations")
+            res["rho_validation"] = rho_validation(B, torch)
         if args.detail_out:
             detail["model_validation"] = res.get("model_validation")
             with open(args.detail_out, "w") as f:

@@ -92,6 +92,13 @@ typedef struct {
   int32_t drain;                     /* 0: the paper's recurrence; 1: compute slots join the
                                         consumers after their tiles (the last split is served
                                         by all C + P slots) */
+  int32_t rho_kh;                    /* 0: eq:rho-scaling as printed; 1: also scale rho by the
+                                        consumer task's bytes relative to the calibration:
+                                        (2 topk + 4) / (2 topk_ref + 4) for the Y rows read
+                                        (bf16) and the output written (fp32) per token, and
+                                        the task width over comm_tile_n_ref */
+  int32_t topk_ref, comm_tile_n_ref; /* top-k and task width at the calibration (used with
+                                        rho_kh = 1) */
 } moe_select_params_t;
 
 /* The chosen partition.  T(C) = T_num / T_den in compute-wave units; W_comp
@@ -121,7 +128,11 @@ typedef struct {
  *     W_comp = ceil(g sum_e ceil(M_e/T_M) / L) ceil(N/T_N),
  *     W_comm = ceil(ceil(ceil(M/D)/T_M^comm) / L) ceil(N/T_N^comm);
  *   drain = 1: the last split's service uses every slot,
- *     F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P)).
+ *     F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
+ *   rho_kh = 1: rho of eq:rho-scaling times
+ *     (2 topk + 4) / (2 topk_ref + 4) * w / comm_tile_n_ref, with the task
+ *     width w = min(comm_tile_n, ceil(N/L)) (column splits) or
+ *     min(comm_tile_n, N) (token bands); topk_ref, comm_tile_n_ref > 0.
  * Pure host code: no HIP call, no allocation, thread-safe.
  * Returns C* >= c_min and fills *out when out != NULL; MOE_ERR_INVALID_ARG for a
  * null wl/p, non-positive dimensions or parameters, a negative host count or
@@ -142,6 +153,21 @@ int moe_select_partition(const moe_workload_t* wl, const moe_select_params_t* p,
 int moe_select_partition_splits(const moe_workload_t* wl, const moe_select_params_t* p,
                                 int32_t l_min, int32_t l_max, moe_partition_t* out,
                                 int32_t* splits_out);
+
+/* The model's internals for one candidate C, for checking the model against
+ * measured traces: rho = *rho_num / *rho_den after eq:rho-scaling (and the
+ * extensions the parameters select), and the split arrival and finish
+ * times A_s and F_s (eq:split-arrival, eq:split-finish) in units of
+ * 1 / *rho_den compute waves, written to A_out[s] and F_out[s] for s < L;
+ * for C = 0 (the role switch) one entry each, the end of all tiles and the
+ * end of all tasks.  rho_num, rho_den, A_out and F_out may each be NULL;
+ * n is the capacity of A_out and F_out (at least L, or 1 for C = 0, when
+ * either is given).  Pure host code.  Returns the number of entries (L, or
+ * 1 for C = 0), MOE_ERR_INVALID_ARG (as moe_select_partition, C < 0, or n
+ * too small) or MOE_ERR_NO_LEGAL_PARTITION when P(C) <= 0. */
+int moe_select_candidate(const moe_workload_t* wl, const moe_select_params_t* p, int32_t C,
+                         int64_t* rho_num, int64_t* rho_den, int64_t* A_out, int64_t* F_out,
+                         int32_t n);
 
 /* The whole T(C) table of the same model: T_num_out[i] is the numerator of
  * T(c_min + i) over the common denominator *T_den_out, or -1 where P <= 0.
@@ -168,7 +194,9 @@ int moe_gemm2_default_params(int device, moe_select_params_t* out);
  * (MOE_GEMM2_RHO_REF_SCATTER="num/den" overrides it); mode 2 (token bands)
  * sets split_axis = 1, drain = 1 and rho_ref to that mode's calibration
  * (MOE_GEMM2_RHO_REF_BANDS overrides it).  Modes 0 and 1 leave split_axis
- * and drain 0.  Returns 0 or MOE_ERR_HIP / MOE_ERR_INVALID_ARG (also for a
+ * and drain 0.  Every mode sets topk_ref = 6 and comm_tile_n_ref = 1024 (the
+ * calibration's) and rho_kh = 0; modes 0 and 2 set rho_kh = 1 when the
+ * environment sets MOE_GEMM2_RHO_KH=1.  Returns 0 or MOE_ERR_HIP / MOE_ERR_INVALID_ARG (also for a
  * mode other than 0, 1 or 2 or topk <= 0). */
 int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk, moe_select_params_t* out);
 
@@ -432,7 +460,7 @@ int moe_gemm2_status(void* workspace, void* stream, int clear);
 /* Static description of an error code. */
 const char* moe_strerror(int status);
 
-/* ABI version of this header (major * 100 + minor): 105. */
+/* ABI version of this header (major * 100 + minor): 106. */
 int moe_gemm2_abi_version(void);
 
 #ifdef __cplusplus

@@ -43,7 +43,12 @@ special case split_axis = 0, drain = False, one given L):
     last split is served by all C + P slots:
     F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
   * L as a decision variable: the (L, C) pair with the least T(C) over a
-    range of L, ties to the smaller L.
+    range of L, ties to the smaller L;
+  * rho_kh = 1: rho also scales with the bytes of one consumer task against
+    the calibration's, k bf16 rows read and one fp32 output written per
+    token and column: rho times (2 k + 4) / (2 k_ref + 4) times w / w_ref,
+    with the task width w = min(T_N^comm, ceil(N/L)) for column splits and
+    min(T_N^comm, N) for token bands.
 """
 from __future__ import annotations
 
@@ -99,9 +104,21 @@ def comm_work(M: int, D: int, N: int, L: int, comm_m: int, comm_n: int,
 
 def rho_scaled(rho_ref: Fraction, K: int, K_ref: int, tile_m: int, tile_n: int,
                tile_m_ref: int, tile_n_ref: int, D: int, D_ref: int) -> Fraction:
+    """eq:rho-scaling."""
     return (Fraction(rho_ref) * Fraction(K_ref, K)
             * Fraction(tile_m_ref * tile_n_ref, tile_m * tile_n)
             * Fraction(D, D_ref))
+
+
+def task_bytes_factor(topk: int, topk_ref: int, width: int, width_ref: int) -> Fraction:
+    """The k/H-aware extension: a task's bytes per token and column are
+    2 k (its k bf16 rows) + 4 (one fp32 output), times the task width."""
+    return Fraction(2 * topk + 4, 2 * topk_ref + 4) * Fraction(width, width_ref)
+
+
+def task_width(H: int, L: int, comm_n: int, split_axis: int = 0) -> int:
+    span = cdiv(H, L) if split_axis == 0 else H
+    return min(span, comm_n)
 
 
 def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
@@ -172,6 +189,9 @@ class SelectParams:
     groups: int = 1
     split_axis: int = 0
     drain: bool = False
+    rho_kh: bool = False
+    topk_ref: int = 6
+    comm_tile_n_ref: int = 1024
 
 
 def select(T: int, H: int, I: int, E: int, topk: int, L: int,
@@ -182,6 +202,10 @@ def select(T: int, H: int, I: int, E: int, topk: int, L: int,
     W_comm = comm_work(T, D, H, L, p.comm_tile_m, p.comm_tile_n, p.split_axis)
     rho = rho_scaled(p.rho_ref, I, p.k_ref, p.tile_m, p.tile_n,
                      p.tile_m_ref, p.tile_n_ref, D, p.d_ref)
+    if p.rho_kh:
+        rho *= task_bytes_factor(topk, p.topk_ref,
+                                 task_width(H, L, p.comm_tile_n, p.split_axis),
+                                 p.comm_tile_n_ref)
     best, cands = select_from_work(W_comp, W_comm, L, p.num_cus, p.occ_comm,
                                    p.occ_comp, rho, p.c_min, p.c_max, bool(p.drain))
     return best, cands, W_comp, W_comm, rho

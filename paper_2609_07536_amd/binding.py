@@ -33,7 +33,7 @@ EXPORTED = (
     "moe_strerror", "moe_gemm2_abi_version", "moe_gemm2_default_params_ex",
     "moe_gemm2_combine_ex", "moe_gemm2_launch_params", "moe_gemm1_pack_weights",
     "moe_gemm1_swiglu", "moe_layer_workspace_size", "moe_layer_forward",
-    "moe_gemm2_combine_noalloc", "moe_select_partition_splits",
+    "moe_gemm2_combine_noalloc", "moe_select_partition_splits", "moe_select_candidate",
 )
 
 # size of the library's own scratch behind moe_gemm2_combine_noalloc
@@ -60,7 +60,9 @@ class SelectParams(ctypes.Structure):
                 ("rho_ref_num", ctypes.c_int64), ("rho_ref_den", ctypes.c_int64),
                 ("k_ref", ctypes.c_int32), ("tile_m_ref", ctypes.c_int32),
                 ("tile_n_ref", ctypes.c_int32), ("d_ref", ctypes.c_int32),
-                ("split_axis", ctypes.c_int32), ("drain", ctypes.c_int32)]
+                ("split_axis", ctypes.c_int32), ("drain", ctypes.c_int32),
+                ("rho_kh", ctypes.c_int32), ("topk_ref", ctypes.c_int32),
+                ("comm_tile_n_ref", ctypes.c_int32)]
 
 
 class Partition(ctypes.Structure):
@@ -151,6 +153,13 @@ def lib() -> ctypes.CDLL:
             L.moe_gemm2_status.restype = ctypes.c_int
             L.moe_strerror.argtypes = [ctypes.c_int]
             L.moe_strerror.restype = ctypes.c_char_p
+            L.moe_select_candidate.argtypes = [ctypes.POINTER(Workload),
+                                               ctypes.POINTER(SelectParams), i32,
+                                               ctypes.POINTER(ctypes.c_int64),
+                                               ctypes.POINTER(ctypes.c_int64),
+                                               ctypes.POINTER(ctypes.c_int64),
+                                               ctypes.POINTER(ctypes.c_int64), i32]
+            L.moe_select_candidate.restype = ctypes.c_int
             L.moe_gemm2_abi_version.argtypes = []
             L.moe_gemm2_abi_version.restype = ctypes.c_int
             _lib = L
@@ -186,6 +195,20 @@ def select_partition_splits(wl: Workload, params: SelectParams, l_min: int, l_ma
     r = lib().moe_select_partition_splits(ctypes.byref(wl), ctypes.byref(params), int(l_min),
                                           int(l_max), ctypes.byref(out), ctypes.byref(L))
     return r, L.value, out
+
+
+def select_candidate(wl: Workload, params: SelectParams, C: int):
+    """moe_select_candidate: (entries or error, rho_num, rho_den, A, F) with
+    A and F the split arrival and finish times in units of 1/rho_den compute
+    waves."""
+    n = max(16, int(wl.splits))
+    A = (ctypes.c_int64 * n)()
+    F = (ctypes.c_int64 * n)()
+    num, den = ctypes.c_int64(0), ctypes.c_int64(0)
+    r = lib().moe_select_candidate(ctypes.byref(wl), ctypes.byref(params), int(C),
+                                   ctypes.byref(num), ctypes.byref(den), A, F, n)
+    k = max(r, 0)
+    return r, num.value, den.value, [A[i] for i in range(k)], [F[i] for i in range(k)]
 
 
 def select_evaluate(wl: Workload, params: SelectParams):

@@ -1873,6 +1873,14 @@ void fill_params(const DevInfo& d, int mode, int topk, int comm_tm, moe_select_p
   p->tile_m_ref = kBM;
   p->tile_n_ref = kBN;
   p->d_ref = 1;
+  // the calibration's top-k and task width, for the k/H-aware rho of the
+  // owner-write consumers (off unless MOE_GEMM2_RHO_KH=1; a scatter task's
+  // bytes do not depend on top-k)
+  p->topk_ref = 6;
+  p->comm_tile_n_ref = kCommTN;
+  p->rho_kh = 0;
+  if (mode != 1)
+    if (const char* s = std::getenv("MOE_GEMM2_RHO_KH")) p->rho_kh = std::atoi(s) == 1 ? 1 : 0;
 }
 
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }

@@ -19,7 +19,7 @@
 // and then all of them serve the consumer tasks:
 //   T(0) = ceil(L W_comp / P0) + rho ceil(L W_comm / P0),   P0 = o_comp G.
 //
-// Two further extensions, each off unless its parameter asks for it:
+// Further extensions, each off unless its parameter asks for it:
 //   split_axis = 1: the L splits cut the routed rows (token bands) instead
 //     of the output columns; a band holds about 1/L of the m-tiles over the
 //     full width and 1/L of the token blocks:
@@ -27,7 +27,9 @@
 //       W_comm = ceil(ceil(ceil(M/D) / T_M^comm) / L) ceil(N / T_N^comm)
 //   drain = 1: the compute slots join the consumers after their last tile,
 //     so the last split is served by all C + P slots:
-//       F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P)).
+//       F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
+//   rho_kh = 1: rho also scales with the consumer task's bytes,
+//       (2 k + 4) / (2 k_ref + 4) * w / w_ref (w: the task width).
 #include <cstdint>
 #include <cstdlib>
 
@@ -90,6 +92,17 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
   // eq:rho-scaling: rho = rho_ref (K_ref/K) (T_M,ref T_N,ref)/(T_M T_N) (D/D_ref)
   i128 num = (i128)p->rho_ref_num * p->k_ref * p->tile_m_ref * p->tile_n_ref * wl->ranks;
   i128 den = (i128)p->rho_ref_den * wl->I * p->tile_m * p->tile_n * p->d_ref;
+  if (p->rho_kh != 0 && p->rho_kh != 1) return MOE_ERR_INVALID_ARG;
+  if (p->rho_kh) {
+    // extension: the consumer task's bytes relative to the calibration's,
+    // (2 k + 4) per token and column (k bf16 rows read, one fp32 written)
+    // times the task width
+    if (p->topk_ref <= 0 || p->comm_tile_n_ref <= 0) return MOE_ERR_INVALID_ARG;
+    const int64_t span = p->split_axis == 0 ? cdiv64(wl->H, wl->splits) : (int64_t)wl->H;
+    const int64_t width = span < p->comm_tile_n ? span : p->comm_tile_n;
+    num *= (i128)(2 * (int64_t)wl->topk + 4) * width;
+    den *= (i128)(2 * (int64_t)p->topk_ref + 4) * p->comm_tile_n_ref;
+  }
   // reduce in 128 bits, then require both to fit in 63 bits
   i128 a = num, b = den;
   while (b != 0) {
@@ -106,9 +119,12 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
 }
 
 // One candidate; returns false if P(C) <= 0.  Status MOE_ERR_INVALID_ARG on
-// overflow of the scaled integer time.
+// overflow of the scaled integer time.  With A_rec / F_rec, also records the
+// split arrival and finish times (one entry for C = 0: all tiles, then all
+// tasks; else L).
 bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int64_t* T_out,
-                    int64_t* delta_out, int32_t* R_out, int32_t* P_out, int* status) {
+                    int64_t* delta_out, int32_t* R_out, int32_t* P_out, int* status,
+                    int64_t* A_rec = nullptr, int64_t* F_rec = nullptr) {
   if (C == 0) {
     const int64_t P0 = (int64_t)p->occ_comp * p->num_cus;
     const i128 A = (i128)cdiv64((int64_t)m.L * m.W_comp, P0) * m.rho_den;
@@ -117,6 +133,8 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
       *status = MOE_ERR_INVALID_ARG;
       return false;
     }
+    if (A_rec) A_rec[0] = (int64_t)A;
+    if (F_rec) F_rec[0] = (int64_t)F;
     *T_out = (int64_t)F;
     *delta_out = cdiv64(m.W_comp, P0) * P0 - m.W_comp;
     *R_out = 0;
@@ -136,6 +154,8 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
       *status = MOE_ERR_INVALID_ARG;
       return false;
     }
+    if (A_rec) A_rec[s] = (int64_t)A;
+    if (F_rec) F_rec[s] = (int64_t)F;
   }
   const int64_t V_comp = cdiv64(m.W_comp, P);
   *T_out = (int64_t)F;
@@ -239,6 +259,25 @@ extern "C" int moe_select_evaluate(const moe_workload_t* wl, const moe_select_pa
   return count;
 }
 
+extern "C" int moe_select_candidate(const moe_workload_t* wl, const moe_select_params_t* p,
+                                    int32_t C, int64_t* rho_num, int64_t* rho_den,
+                                    int64_t* A_out, int64_t* F_out, int32_t n) {
+  Model m;
+  int st = build_model(wl, p, &m);
+  if (st != MOE_OK) return st;
+  if (C < 0) return MOE_ERR_INVALID_ARG;
+  const int32_t entries = C == 0 ? 1 : m.L;
+  if ((A_out || F_out) && n < entries) return MOE_ERR_INVALID_ARG;
+  int64_t T, D;
+  int32_t R, P;
+  st = MOE_OK;
+  if (!eval_candidate(m, p, C, &T, &D, &R, &P, &st, A_out, F_out))
+    return st != MOE_OK ? st : MOE_ERR_NO_LEGAL_PARTITION;
+  if (rho_num) *rho_num = m.rho_num;
+  if (rho_den) *rho_den = m.rho_den;
+  return entries;
+}
+
 extern "C" const char* moe_strerror(int status) {
   switch (status) {
     case MOE_OK: return "ok";
@@ -254,4 +293,4 @@ extern "C" const char* moe_strerror(int status) {
   }
 }
 
-extern "C" int moe_gemm2_abi_version(void) { return 105; }
+extern "C" int moe_gemm2_abi_version(void) { return 106; }

@@ -1,5 +1,6 @@
 """The C ABI on the CPU: exports, the selector (bit-exact against the Python
 oracle) and host-side validation.  Nothing here launches GPU work."""
+import ctypes
 import os
 import random
 import re
@@ -27,14 +28,14 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(B.EXPORTED)
-    assert L.moe_gemm2_abi_version() == 105
+    assert L.moe_gemm2_abi_version() == 106
 
 
 def _params(**kw):
     p = B.SelectParams(tile_m=256, tile_n=256, comm_tile_m=128, comm_tile_n=1024,
                        occ_comp=1, occ_comm=1, num_cus=256, c_min=1, c_max=64, groups=1,
                        rho_ref_num=4, rho_ref_den=3, k_ref=704, tile_m_ref=256,
-                       tile_n_ref=256, d_ref=1)
+                       tile_n_ref=256, d_ref=1, rho_kh=0, topk_ref=6, comm_tile_n_ref=1024)
     for k, v in kw.items():
         setattr(p, k, v)
     return p
@@ -47,7 +48,8 @@ def _oracle_params(p):
         num_cus=p.num_cus, c_min=p.c_min, c_max=p.c_max,
         rho_ref=Fraction(p.rho_ref_num, p.rho_ref_den), k_ref=p.k_ref,
         tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups,
-        split_axis=p.split_axis, drain=bool(p.drain))
+        split_axis=p.split_axis, drain=bool(p.drain), rho_kh=bool(p.rho_kh),
+        topk_ref=p.topk_ref, comm_tile_n_ref=p.comm_tile_n_ref)
 
 
 def test_hand_example_through_the_abi():
@@ -68,6 +70,33 @@ def test_hand_example_through_the_abi():
     p.c_max = 4
     r, part = B.select_partition(wl, p)
     assert r == 4
+
+
+def test_rho_kh_hand_example_through_the_abi():
+    """The same instance with the k/H-aware rho: top-1 against a top-1
+    calibration (2k + 4 equal) and a task width of 1 column against 2, so
+    rho = 3/2 * 1/2 = 3/4.  By hand: T(C = 1..6) = 11, 6.5, 6.5, 6.5, 7.5,
+    8.75; the tie at 6.5 goes to the least Delta (C = 2: 2, C = 3: 12,
+    C = 4: 6), so C* = 2 where the printed rho gives C* = 5."""
+    p = _params(tile_m=1, tile_n=1, comm_tile_m=5, comm_tile_n=1, occ_comp=2,
+                occ_comm=1, num_cus=10, c_max=6, rho_ref_num=3, rho_ref_den=2,
+                k_ref=8, tile_m_ref=1, tile_n_ref=1, rho_kh=1, topk_ref=1, comm_tile_n_ref=2)
+    wl, keep = B.make_workload(T=30, H=2, I=8, E=1, topk=1, splits=2, counts=[30])
+    r, part = B.select_partition(wl, p)
+    assert r == 2 and part.delta_comp == 2 and part.T_den == 4
+    assert Fraction(part.T_num, part.T_den) == Fraction(13, 2)
+    n, table, den = B.select_evaluate(wl, p)
+    assert [Fraction(t, den) for t in table] == [11, Fraction(13, 2), Fraction(13, 2),
+                                                 Fraction(13, 2), Fraction(15, 2),
+                                                 Fraction(35, 4)]
+    for bad in (dict(rho_kh=2), dict(topk_ref=0), dict(comm_tile_n_ref=0)):
+        q = _params(tile_m=1, tile_n=1, comm_tile_m=5, comm_tile_n=1, occ_comp=2,
+                    occ_comm=1, num_cus=10, c_max=6, rho_ref_num=3, rho_ref_den=2,
+                    k_ref=8, tile_m_ref=1, tile_n_ref=1, rho_kh=1, topk_ref=1,
+                    comm_tile_n_ref=2)
+        for k, v in bad.items():
+            setattr(q, k, v)
+        assert B.select_partition(wl, q)[0] == B.MOE_ERR_INVALID_ARG, bad
 
 
 def _random_case(rnd):
@@ -91,7 +120,8 @@ def _random_case(rnd):
                 rho_ref_den=rnd.randint(1, 10000), k_ref=rnd.choice([352, 704, 1408]),
                 tile_m_ref=rnd.choice([128, 256]), tile_n_ref=rnd.choice([128, 256]),
                 d_ref=rnd.choice([1, 4]), split_axis=rnd.choice([0, 0, 1]),
-                drain=rnd.choice([0, 0, 1]))
+                drain=rnd.choice([0, 0, 1]), rho_kh=rnd.choice([0, 0, 1]),
+                topk_ref=rnd.randint(1, 16), comm_tile_n_ref=rnd.choice([256, 512, 1024, 2048]))
     D = rnd.choice([1, 1, 2, 4])
     return T, H, I, E, topk, L, counts, p, D
 
@@ -125,6 +155,40 @@ def test_selector_bit_exact_against_oracle():
                 assert tnum == -1
         n_checked += 1
     assert n_checked > 2000
+
+
+def test_candidate_internals_bit_exact_against_oracle():
+    """moe_select_candidate (rho and the split arrival and finish times of
+    one candidate) against the oracle's candidate on random workloads, at
+    random C including the role switch."""
+    rnd = random.Random(91)
+    n = 0
+    for _ in range(600):
+        T, H, I, E, topk, L, counts, p, D = _random_case(rnd)
+        wl, keep = B.make_workload(T, H, I, E, topk, L, counts, ranks=D)
+        C = rnd.randint(p.c_min, p.c_max)
+        r, num, den, A, F = B.select_candidate(wl, p, C)
+        best, cands, W_comp, W_comm, rho = osel.select(T, H, I, E, topk, L, counts,
+                                                        _oracle_params(p), D=D)
+        byC = {c.C: c for c in cands}
+        if C not in byC:
+            assert r == B.MOE_ERR_NO_LEGAL_PARTITION, (r, C)
+            continue
+        cand = byC[C]
+        assert Fraction(num, den) == rho and den == rho.denominator
+        assert r == (1 if C == 0 else L)
+        assert [Fraction(a, den) for a in A] == [Fraction(a) for a in cand.A]
+        assert [Fraction(f, den) for f in F] == list(cand.F)
+        n += 1
+    assert n > 400
+    wl, keep = B.make_workload(100, 256, 64, 4, 2, 2, [50, 50, 50, 50])
+    assert B.select_candidate(wl, _params(), -1)[0] == B.MOE_ERR_INVALID_ARG
+    L_ = B.lib()
+    buf = (ctypes.c_int64 * 1)()
+    assert L_.moe_select_candidate(ctypes.byref(wl), ctypes.byref(_params()), 3, None, None,
+                                   buf, None, 1) == B.MOE_ERR_INVALID_ARG   # n < L
+    assert L_.moe_select_candidate(ctypes.byref(wl), ctypes.byref(_params()), 3, None, None,
+                                   None, None, 0) == 2
 
 
 def test_split_selection_bit_exact_against_oracle():

@@ -231,3 +231,36 @@ def test_split_count_as_a_decision_variable_by_hand():
     assert (L, best.C, best.T) == (4, 3, Fraction(10))
     L, best = sel.select_splits(1280, 256, 704, 4, 8, counts, p, 1, 2)
     assert (L, best.C, best.T) == (2, 3, Fraction(11))
+
+
+def test_task_bytes_factor_by_hand():
+    """The k/H-aware extension's factor: (2k + 4) / (2k_ref + 4) times the
+    task width over the calibration's (a task reads k bf16 rows and writes
+    one fp32 output per token and column)."""
+    assert sel.task_bytes_factor(6, 6, 1024, 1024) == 1
+    assert sel.task_bytes_factor(4, 6, 512, 1024) == Fraction(12, 16) * Fraction(1, 2)
+    assert sel.task_bytes_factor(8, 6, 1024, 1024) == Fraction(20, 16)
+    # the task width: a split's columns capped at the task tile (column
+    # splits), or the full width capped (token bands)
+    assert sel.task_width(2048, 2, 1024) == 1024
+    assert sel.task_width(1024, 4, 1024) == 256
+    assert sel.task_width(200, 5, 1024) == 40
+    assert sel.task_width(200, 5, 1024, split_axis=1) == 200
+    assert sel.task_width(4096, 1, 1024, split_axis=1) == 1024
+
+
+def test_rho_kh_changes_the_pick_by_hand():
+    """The hand instance (G = 10, o_comm = 1, o_comp = 2, W_comp = 30,
+    W_comm = 6, L = 2, rho = 3/2 gives C* = 5) with rho scaled by 1/2:
+    T(C = 1..6) = 11, 6.5, 6.5, 6.5, 7.5, 8.75, ties broken by Delta
+    (2, 12, 6 for C = 2, 3, 4), so C* = 2."""
+    rho = sel.rho_scaled(Fraction(3, 2), 8, 8, 1, 1, 1, 1, 1, 1) * \
+        sel.task_bytes_factor(1, 1, 1, 2)
+    assert rho == Fraction(3, 4)
+    best, cands = sel.select_from_work(30, 6, 2, 10, 1, 2, rho, 1, 6)
+    assert [c.T for c in cands] == [11, Fraction(13, 2), Fraction(13, 2), Fraction(13, 2),
+                                    Fraction(15, 2), Fraction(35, 4)]
+    assert [c.delta for c in cands[1:4]] == [2, 12, 6]
+    assert best.C == 2
+    best0, _ = sel.select_from_work(30, 6, 2, 10, 1, 2, Fraction(3, 2), 1, 6)
+    assert best0.C == 5
