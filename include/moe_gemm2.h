@@ -99,6 +99,9 @@ typedef struct {
                                         the task width over comm_tile_n_ref */
   int32_t topk_ref, comm_tile_n_ref; /* top-k and task width at the calibration (used with
                                         rho_kh = 1) */
+  int32_t readiness;                 /* 0: consumer work becomes ready a split at a time (the
+                                        paper); 1: a compute wave at a time (consumer tasks
+                                        that each need one compute tile, the atomic scatter) */
 } moe_select_params_t;
 
 /* The chosen partition.  T(C) = T_num / T_den in compute-wave units; W_comp
@@ -129,6 +132,14 @@ typedef struct {
  *     W_comm = ceil(ceil(ceil(M/D)/T_M^comm) / L) ceil(N/T_N^comm);
  *   drain = 1: the last split's service uses every slot,
  *     F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
+ *   readiness = 1 (column splits only): the consumer work is released
+ *     a compute wave at a time instead of a split at a time.  The L W_comp
+ *     tiles complete in V = ceil(L W_comp / P) waves, wave v (1-based) the
+ *     tiles [(v-1) P, min(v P, L W_comp)); it releases
+ *     w_v = ceil(t_v L W_comm / (L W_comp)) - ceil(t_{v-1} L W_comm / (L W_comp))
+ *     tasks, t_v = min(v P, L W_comp), and
+ *     F_v = max(v, F_{v-1}) + rho ceil(w_v / C), T(C) = F_V (with drain = 1
+ *     the last wave's tasks are served by C + P slots); C = 0 is unchanged;
  *   rho_kh = 1: rho of eq:rho-scaling times
  *     (2 topk + 4) / (2 topk_ref + 4) * w / comm_tile_n_ref, with the task
  *     width w = min(comm_tile_n, ceil(N/L)) (column splits) or
@@ -160,11 +171,13 @@ int moe_select_partition_splits(const moe_workload_t* wl, const moe_select_param
  * times A_s and F_s (eq:split-arrival, eq:split-finish) in units of
  * 1 / *rho_den compute waves, written to A_out[s] and F_out[s] for s < L;
  * for C = 0 (the role switch) one entry each, the end of all tiles and the
- * end of all tasks.  rho_num, rho_den, A_out and F_out may each be NULL;
- * n is the capacity of A_out and F_out (at least L, or 1 for C = 0, when
- * either is given).  Pure host code.  Returns the number of entries (L, or
- * 1 for C = 0), MOE_ERR_INVALID_ARG (as moe_select_partition, C < 0, or n
- * too small) or MOE_ERR_NO_LEGAL_PARTITION when P(C) <= 0. */
+ * end of all tasks; with readiness = 1 one entry per compute wave (V of
+ * them, as in moe_select_partition).  rho_num, rho_den, A_out and F_out may each be NULL;
+ * n is the capacity of A_out and F_out (at least the number of entries
+ * when either is given).  Pure host code.  Returns the number of entries
+ * (L; 1 for C = 0; V with readiness = 1), MOE_ERR_INVALID_ARG (as
+ * moe_select_partition, C < 0, or n too small) or
+ * MOE_ERR_NO_LEGAL_PARTITION when P(C) <= 0. */
 int moe_select_candidate(const moe_workload_t* wl, const moe_select_params_t* p, int32_t C,
                          int64_t* rho_num, int64_t* rho_den, int64_t* A_out, int64_t* F_out,
                          int32_t n);
@@ -191,7 +204,9 @@ int moe_gemm2_default_params(int device, moe_select_params_t* out);
  * task per compute tile) sets the consumer tile to
  * max(1, tile_m / topk) tokens x tile_n columns, so that W_comm counts
  * about one task per compute tile, and rho_ref to that mode's calibration
- * (MOE_GEMM2_RHO_REF_SCATTER="num/den" overrides it); mode 2 (token bands)
+ * (MOE_GEMM2_RHO_REF_SCATTER="num/den" overrides it) and readiness = 1 (a
+ * scatter task waits only for the published prefix of the tile sequence up
+ * to its own tile); mode 2 (token bands)
  * sets split_axis = 1, drain = 1 and rho_ref to that mode's calibration
  * (MOE_GEMM2_RHO_REF_BANDS overrides it).  Modes 0 and 1 leave split_axis
  * and drain 0.  Every mode sets topk_ref = 6 and comm_tile_n_ref = 1024 (the
@@ -310,8 +325,10 @@ int moe_gemm2_combine_traced(const void* x_perm, const void* w2, const int32_t* 
  *           result does not depend on C or on timing);
  *   mode 1  atomic scatter: the kernel first zeroes out (each workgroup its
  *           share, published like the inverse map of mode 0), then a
- *           consumer task is one published compute tile, whose rows r it
- *           adds, weighted by gate_w[r], into out[token_ids[r], :] with
+ *           consumer task is one published compute tile (it waits for the
+ *           published prefix of the tile sequence up to that tile, i.e. for
+ *           the compute wave that holds it, not for the whole split), whose
+ *           rows r it adds, weighted by gate_w[r], into out[token_ids[r], :] with
  *           fp32 atomic additions at device scope.  The order of the
  *           additions varies from run to run, so the result does too, by
  *           rounding only.  Rows with an out-of-range token id are skipped

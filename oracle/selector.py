@@ -44,6 +44,12 @@ special case split_axis = 0, drain = False, one given L):
     F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
   * L as a decision variable: the (L, C) pair with the least T(C) over a
     range of L, ties to the smaller L;
+  * readiness = 1 (column splits): the consumer work is released a compute
+    wave at a time rather than a split at a time.  The L W_comp tiles end in
+    V = ceil(L W_comp / P) waves; wave v ends t_v = min(v P, L W_comp) of
+    them and releases w_v = ceil(t_v L W_comm / (L W_comp)) - (what earlier
+    waves released) tasks, served as F_v = max(v, F_{v-1}) + rho ceil(w_v / C)
+    (drain: the last wave over C + P slots); T(C) = F_V.  C = 0 is unchanged;
   * rho_kh = 1: rho also scales with the bytes of one consumer task against
     the calibration's, k bf16 rows read and one fp32 output written per
     token and column: rho times (2 k + 4) / (2 k_ref + 4) times w / w_ref,
@@ -122,7 +128,8 @@ def task_width(H: int, L: int, comm_n: int, split_axis: int = 0) -> int:
 
 
 def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
-             o_comp: int, rho: Fraction, drain: bool = False) -> Optional[Candidate]:
+             o_comp: int, rho: Fraction, drain: bool = False,
+             readiness: int = 0) -> Optional[Candidate]:
     """The recurrence for one candidate C; None if P(C) <= 0 (illegal)."""
     if C == 0:
         P0 = o_comp * G
@@ -136,9 +143,12 @@ def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
     P = o_comp * (G - R)
     if P <= 0:
         return None
-    A = [cdiv((s + 1) * W_comp, P) for s in range(L)]
     V_comm = cdiv(W_comm, C)
     q = Fraction(rho) * V_comm
+    V_comp = cdiv(W_comp, P)
+    if readiness == 1:
+        return _per_wave(C, R, P, W_comp, W_comm, L, rho, drain, V_comm, q, V_comp)
+    A = [cdiv((s + 1) * W_comp, P) for s in range(L)]
     F: List[Fraction] = []
     prev = Fraction(0)
     for s in range(L):
@@ -148,20 +158,45 @@ def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
         else:
             prev = max(Fraction(A[s]), prev) + q
         F.append(prev)
-    V_comp = cdiv(W_comp, P)
     return Candidate(C=C, R=R, P=P, A=A, V_comm=V_comm, q=q, F=F, T=F[-1],
                      V_comp=V_comp, delta=V_comp * P - W_comp)
 
 
+def _per_wave(C, R, P, W_comp, W_comm, L, rho, drain, V_comm, q, V_comp) -> Candidate:
+    """The readiness = 1 recurrence: tasks released as compute waves end."""
+    tiles, tasks = L * W_comp, L * W_comm
+    delta = V_comp * P - W_comp
+    if tiles == 0:
+        T = Fraction(rho) * cdiv(tasks, C + P if drain else C)
+        return Candidate(C=C, R=R, P=P, A=[0], V_comm=V_comm, q=q, F=[T], T=T,
+                         V_comp=V_comp, delta=delta)
+    V = cdiv(tiles, P)
+    A: List[int] = []
+    F: List[Fraction] = []
+    released = 0
+    prev = Fraction(0)
+    for v in range(1, V + 1):
+        t = min(v * P, tiles)
+        rel = cdiv(t * tasks, tiles)          # tasks whose tiles have all ended
+        w = rel - released
+        released = rel
+        slots = C + P if (drain and v == V) else C
+        prev = max(Fraction(v), prev) + Fraction(rho) * cdiv(w, slots)
+        A.append(v)
+        F.append(prev)
+    return Candidate(C=C, R=R, P=P, A=A, V_comm=V_comm, q=q, F=F, T=F[-1],
+                     V_comp=V_comp, delta=delta)
+
+
 def select_from_work(W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
                      o_comp: int, rho: Fraction, c_min: int, c_max: int,
-                     drain: bool = False):
+                     drain: bool = False, readiness: int = 0):
     """Argmin of T(C) over the legal C, then smallest Delta, then smallest C.
 
     Returns (best Candidate or None, list of all legal candidates)."""
     cands = []
     for C in range(c_min, c_max + 1):
-        c = evaluate(C, W_comp, W_comm, L, G, o_comm, o_comp, rho, drain)
+        c = evaluate(C, W_comp, W_comm, L, G, o_comm, o_comp, rho, drain, readiness)
         if c is not None:
             cands.append(c)
     if not cands:
@@ -192,6 +227,7 @@ class SelectParams:
     rho_kh: bool = False
     topk_ref: int = 6
     comm_tile_n_ref: int = 1024
+    readiness: int = 0
 
 
 def select(T: int, H: int, I: int, E: int, topk: int, L: int,
@@ -207,7 +243,8 @@ def select(T: int, H: int, I: int, E: int, topk: int, L: int,
                                  task_width(H, L, p.comm_tile_n, p.split_axis),
                                  p.comm_tile_n_ref)
     best, cands = select_from_work(W_comp, W_comm, L, p.num_cus, p.occ_comm,
-                                   p.occ_comp, rho, p.c_min, p.c_max, bool(p.drain))
+                                   p.occ_comp, rho, p.c_min, p.c_max, bool(p.drain),
+                                   p.readiness)
     return best, cands, W_comp, W_comm, rho
 
 

@@ -62,7 +62,7 @@ class SelectParams(ctypes.Structure):
                 ("tile_n_ref", ctypes.c_int32), ("d_ref", ctypes.c_int32),
                 ("split_axis", ctypes.c_int32), ("drain", ctypes.c_int32),
                 ("rho_kh", ctypes.c_int32), ("topk_ref", ctypes.c_int32),
-                ("comm_tile_n_ref", ctypes.c_int32)]
+                ("comm_tile_n_ref", ctypes.c_int32), ("readiness", ctypes.c_int32)]
 
 
 class Partition(ctypes.Structure):
@@ -201,10 +201,13 @@ def select_candidate(wl: Workload, params: SelectParams, C: int):
     """moe_select_candidate: (entries or error, rho_num, rho_den, A, F) with
     A and F the split arrival and finish times in units of 1/rho_den compute
     waves."""
-    n = max(16, int(wl.splits))
+    num, den = ctypes.c_int64(0), ctypes.c_int64(0)
+    n = lib().moe_select_candidate(ctypes.byref(wl), ctypes.byref(params), int(C), None, None,
+                                   None, None, 0)
+    if n < 0:
+        return n, 0, 0, [], []
     A = (ctypes.c_int64 * n)()
     F = (ctypes.c_int64 * n)()
-    num, den = ctypes.c_int64(0), ctypes.c_int64(0)
     r = lib().moe_select_candidate(ctypes.byref(wl), ctypes.byref(params), int(C),
                                    ctypes.byref(num), ctypes.byref(den), A, F, n)
     k = max(r, 0)

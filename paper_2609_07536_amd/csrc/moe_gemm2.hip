@@ -185,6 +185,7 @@ struct Smem {
   int flag;
   int task;                   // consumer task claimed by the workgroup
   int task_band;              // token bands: last band holding a row of the staged task
+  int prefix_end;             // end of the published prefix found by wait_prefix
   u64 epoch;                  // this launch's epoch, read once at the start
 };
 
@@ -293,6 +294,67 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
   if (acquire && threadIdx.x < 64) acquire_agent();
   __syncthreads();  // sm.flag may be rewritten by the next wait
   return ok;
+}
+
+// Waits until flags [from, need) are published, then extends the prefix over
+// the flags that are already published up to `limit` (without waiting), and
+// acquires once for the whole prefix (wave 0 polls; the same bound as
+// wait_flags).  Returns the end of the published prefix (>= need), or -1 if
+// the bound expired.  A consumer that keeps the returned end needs no wait
+// and no acquire for the tiles before it, so it acquires once per catch-up
+// with the compute workgroups rather than once per task.
+__device__ long long wait_prefix(Smem& sm, uint32_t* flags, long long from, long long need,
+                                 long long limit, const KArgs& a) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const uint32_t epoch = flag_epoch(sm);
+    long long i = from, spins = 0;
+    int ok = 1;
+    while (i < need) {
+      const long long idx = i + lane;
+      const uint32_t v = idx < need ? __hip_atomic_load(&flags[idx], __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT)
+                                    : epoch;
+      const u64 ready = __ballot(v == epoch);
+      if (ready == ~0ull) {
+        i += 64;
+        continue;
+      }
+      i += __builtin_ctzll(~ready);
+      if (++spins > a.spin_limit) {
+        ok = 0;
+        if (lane == 0)
+          __hip_atomic_fetch_or(a.status, kStTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(8);
+    }
+    if (ok) {
+      if (i > need) i = need;
+      while (i < limit) {
+        const long long idx = i + lane;
+        const bool set = idx < limit && __hip_atomic_load(&flags[idx], __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT) == epoch;
+        const u64 ready = __ballot(set);
+        if (ready == ~0ull) {
+          i += 64;
+          continue;
+        }
+        i += __builtin_ctzll(~ready);
+        break;
+      }
+    }
+    if (lane == 0) {
+      sm.flag = ok;
+      sm.prefix_end = (int)i;
+    }
+  }
+  __syncthreads();
+  const bool ok = sm.flag != 0;
+  const long long end = sm.prefix_end;
+  if (ok && threadIdx.x < 64) acquire_agent();
+  __syncthreads();  // sm.flag and sm.prefix_end may be rewritten by the next wait
+  return ok ? end : -1;
 }
 
 // ---- prologue: expert ranges and the routed-tile prefix ----------------------
@@ -1342,6 +1404,8 @@ struct Consumer {
   int meta_t0;   // token block whose metadata is in LDS (-1: none)
   bool inv_ok;   // every workgroup's inverse-map share is published
   bool inv_acq;  // ... and acquired by this workgroup
+  int tiles;     // atomic scatter: the tiles [0, tiles) of the global sequence are
+                 // known published and acquired by this workgroup
 };
 
 // The owner-write task idx's metadata in LDS (unless it is there already).
@@ -1418,10 +1482,23 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
       const int idx = sm.task;
       __syncthreads();   // sm.task is rewritten by the next claim
       if (idx >= tps) break;
-      if (s > cs.ready) {
+      if (a.mode == 1) {
+        // a scatter task needs only its own tile: it waits for the published
+        // prefix of the tile sequence up to that tile (tiles are claimed in
+        // sequence order, so this is the compute wave that holds it), and
+        // takes what is published beyond it as well, one acquire for all
+        const long long g = (long long)s * W_comp + idx;
+        if (g >= cs.tiles) {
+          const long long end = wait_prefix(sm, a.tile_flags, cs.tiles, g + 1,
+                                            (long long)W_comp * a.L, a);
+          if (end < 0) return;
+          cs.tiles = (int)end;
+          cs.inv_acq = true;   // that acquire covered the zeroed output as well
+        }
+      } else if (s > cs.ready) {
         // a task's metadata needs the inverse map only: once that is
         // acquired, it loads while the task's split is still computing
-        if (a.mode == 0 && cs.inv_acq) ensure_task_meta(sm, a, idx, cs);
+        if (cs.inv_acq) ensure_task_meta(sm, a, idx, cs);
         if (W_comp > 0 && !wait_flags(sm, a.tile_flags + (long long)s * W_comp, W_comp, a)) return;
         cs.ready = s;
         cs.inv_acq = true;   // that acquire covered the inverse map as well
@@ -1856,6 +1933,9 @@ void fill_params(const DevInfo& d, int mode, int topk, int comm_tm, moe_select_p
   p->rho_ref_den = mode == 1 ? kRhoScatterDen : mode == 2 ? kRhoBandsDen : kRhoRefDen;
   p->split_axis = mode == 2 ? 1 : 0;
   p->drain = mode == 2 ? 1 : 0;
+  // a scatter task needs only its own tile and waits for the published
+  // prefix up to it: its work is released a compute wave at a time
+  p->readiness = mode == 1 ? 1 : 0;
   const char* env = mode == 1 ? "MOE_GEMM2_RHO_REF_SCATTER"
                     : mode == 2 ? "MOE_GEMM2_RHO_REF_BANDS" : "MOE_GEMM2_RHO_REF";
   if (const char* s = std::getenv(env)) {

@@ -28,6 +28,12 @@
 //   drain = 1: the compute slots join the consumers after their last tile,
 //     so the last split is served by all C + P slots:
 //       F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
+//   readiness = 1 (column splits): consumer work is released a compute wave
+//     at a time: of V = ceil(L W_comp / P) waves, wave v releases the tasks
+//     of the tiles it completes, w_v = ceil(t_v L W_comm / (L W_comp)) -
+//     ceil(t_{v-1} ...), t_v = min(v P, L W_comp), and
+//       F_v = max(v, F_{v-1}) + rho ceil(w_v / C),   T(C) = F_V
+//     (drain: the last wave's tasks over C + P slots);
 //   rho_kh = 1: rho also scales with the consumer task's bytes,
 //       (2 k + 4) / (2 k_ref + 4) * w / w_ref (w: the task width).
 #include <cstdint>
@@ -48,6 +54,7 @@ struct Model {
   int64_t rho_num = 0, rho_den = 1;
   int L = 1;
   int drain = 0;
+  int readiness = 0;
 };
 
 // Builds the per-split work counts and the scaled rho; returns a status.
@@ -77,6 +84,8 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
   }
   if (p->split_axis != 0 && p->split_axis != 1) return MOE_ERR_INVALID_ARG;
   if (p->drain != 0 && p->drain != 1) return MOE_ERR_INVALID_ARG;
+  if (p->readiness != 0 && p->readiness != 1) return MOE_ERR_INVALID_ARG;
+  if (p->readiness == 1 && p->split_axis != 0) return MOE_ERR_INVALID_ARG;
   const int64_t token_blocks = cdiv64(cdiv64(wl->T, wl->ranks), p->comm_tile_m);
   if (p->split_axis == 0) {
     const int64_t n_split = cdiv64(wl->H, wl->splits);
@@ -88,6 +97,7 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
   }
   m->L = wl->splits;
   m->drain = p->drain;
+  m->readiness = p->readiness;
 
   // eq:rho-scaling: rho = rho_ref (K_ref/K) (T_M,ref T_N,ref)/(T_M T_N) (D/D_ref)
   i128 num = (i128)p->rho_ref_num * p->k_ref * p->tile_m_ref * p->tile_n_ref * wl->ranks;
@@ -147,6 +157,33 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
   const i128 q = (i128)m.rho_num * cdiv64(m.W_comm, C);
   const i128 q_drain = (i128)m.rho_num * cdiv64(m.W_comm, (int64_t)C + P);
   i128 F = 0;
+  if (m.readiness == 1) {
+    // per compute wave: wave v releases the tasks of the tiles it completes
+    const int64_t tiles = (int64_t)m.L * m.W_comp, tasks = (int64_t)m.L * m.W_comm;
+    if (tiles == 0) {
+      F = (i128)m.rho_num * cdiv64(tasks, m.drain ? (int64_t)C + P : C);
+      if (A_rec) A_rec[0] = 0;
+      if (F_rec) F_rec[0] = (int64_t)F;
+    } else {
+      const int64_t V = cdiv64(tiles, P);
+      int64_t released = 0;
+      for (int64_t v = 1; v <= V; ++v) {
+        const int64_t t = v * P < tiles ? v * P : tiles;
+        const int64_t rel = (int64_t)(((i128)t * tasks + tiles - 1) / tiles);
+        const int64_t w = rel - released;
+        released = rel;
+        const i128 A = (i128)v * m.rho_den;
+        const int64_t slots = m.drain && v == V ? (int64_t)C + P : C;
+        F = (A > F ? A : F) + (i128)m.rho_num * cdiv64(w, slots);
+        if (F > kI64Max) {
+          *status = MOE_ERR_INVALID_ARG;
+          return false;
+        }
+        if (A_rec) A_rec[v - 1] = (int64_t)A;
+        if (F_rec) F_rec[v - 1] = (int64_t)F;
+      }
+    }
+  } else {
   for (int s = 0; s < m.L; ++s) {
     const i128 A = (i128)cdiv64((int64_t)(s + 1) * m.W_comp, P) * m.rho_den;
     F = (A > F ? A : F) + (m.drain && s == m.L - 1 ? q_drain : q);
@@ -156,6 +193,7 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
     }
     if (A_rec) A_rec[s] = (int64_t)A;
     if (F_rec) F_rec[s] = (int64_t)F;
+  }
   }
   const int64_t V_comp = cdiv64(m.W_comp, P);
   *T_out = (int64_t)F;
@@ -266,8 +304,14 @@ extern "C" int moe_select_candidate(const moe_workload_t* wl, const moe_select_p
   int st = build_model(wl, p, &m);
   if (st != MOE_OK) return st;
   if (C < 0) return MOE_ERR_INVALID_ARG;
-  const int32_t entries = C == 0 ? 1 : m.L;
-  if ((A_out || F_out) && n < entries) return MOE_ERR_INVALID_ARG;
+  int64_t entries = C == 0 ? 1 : m.L;
+  if (C > 0 && m.readiness == 1) {
+    const int64_t R = cdiv64(C, p->occ_comm);
+    const int64_t P = (int64_t)p->occ_comp * ((int64_t)p->num_cus - R);
+    const int64_t tiles = (int64_t)m.L * m.W_comp;
+    entries = P <= 0 ? 1 : tiles == 0 ? 1 : cdiv64(tiles, P);
+  }
+  if (entries > INT32_MAX || ((A_out || F_out) && n < entries)) return MOE_ERR_INVALID_ARG;
   int64_t T, D;
   int32_t R, P;
   st = MOE_OK;
@@ -275,7 +319,7 @@ extern "C" int moe_select_candidate(const moe_workload_t* wl, const moe_select_p
     return st != MOE_OK ? st : MOE_ERR_NO_LEGAL_PARTITION;
   if (rho_num) *rho_num = m.rho_num;
   if (rho_den) *rho_den = m.rho_den;
-  return entries;
+  return (int)entries;
 }
 
 extern "C" const char* moe_strerror(int status) {

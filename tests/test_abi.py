@@ -35,7 +35,8 @@ def _params(**kw):
     p = B.SelectParams(tile_m=256, tile_n=256, comm_tile_m=128, comm_tile_n=1024,
                        occ_comp=1, occ_comm=1, num_cus=256, c_min=1, c_max=64, groups=1,
                        rho_ref_num=4, rho_ref_den=3, k_ref=704, tile_m_ref=256,
-                       tile_n_ref=256, d_ref=1, rho_kh=0, topk_ref=6, comm_tile_n_ref=1024)
+                       tile_n_ref=256, d_ref=1, rho_kh=0, topk_ref=6, comm_tile_n_ref=1024,
+                       readiness=0)
     for k, v in kw.items():
         setattr(p, k, v)
     return p
@@ -49,7 +50,7 @@ def _oracle_params(p):
         rho_ref=Fraction(p.rho_ref_num, p.rho_ref_den), k_ref=p.k_ref,
         tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups,
         split_axis=p.split_axis, drain=bool(p.drain), rho_kh=bool(p.rho_kh),
-        topk_ref=p.topk_ref, comm_tile_n_ref=p.comm_tile_n_ref)
+        topk_ref=p.topk_ref, comm_tile_n_ref=p.comm_tile_n_ref, readiness=p.readiness)
 
 
 def test_hand_example_through_the_abi():
@@ -122,6 +123,13 @@ def _random_case(rnd):
                 d_ref=rnd.choice([1, 4]), split_axis=rnd.choice([0, 0, 1]),
                 drain=rnd.choice([0, 0, 1]), rho_kh=rnd.choice([0, 0, 1]),
                 topk_ref=rnd.randint(1, 16), comm_tile_n_ref=rnd.choice([256, 512, 1024, 2048]))
+    if p.split_axis == 0:
+        # per-wave readiness walks every compute wave in the oracle: keep it to
+        # workloads of at most 2000 tiles so the suite stays fast
+        m_tiles = osel.routed_m_tiles(counts, p.tile_m, E, T * topk)
+        tiles = L * osel.compute_work(m_tiles, H, L, p.tile_n, p.groups)
+        if tiles <= 2000:
+            p.readiness = rnd.choice([0, 1, 1])
     D = rnd.choice([1, 1, 2, 4])
     return T, H, I, E, topk, L, counts, p, D
 
@@ -176,7 +184,9 @@ def test_candidate_internals_bit_exact_against_oracle():
             continue
         cand = byC[C]
         assert Fraction(num, den) == rho and den == rho.denominator
-        assert r == (1 if C == 0 else L)
+        assert r == len(cand.A) == len(cand.F)
+        if p.readiness == 0:
+            assert r == (1 if C == 0 else L)
         assert [Fraction(a, den) for a in A] == [Fraction(a) for a in cand.A]
         assert [Fraction(f, den) for f in F] == list(cand.F)
         n += 1
@@ -215,8 +225,11 @@ def test_split_selection_bit_exact_against_oracle():
     wl, keep = B.make_workload(100, 256, 64, 4, 2, 1, [50, 50, 50, 50])
     assert B.select_partition_splits(wl, _params(), 0, 3)[0] == B.MOE_ERR_INVALID_ARG
     assert B.select_partition_splits(wl, _params(), 3, 2)[0] == B.MOE_ERR_INVALID_ARG
-    for field in ("split_axis", "drain"):
+    for field in ("split_axis", "drain", "readiness"):
         assert B.select_partition(wl, _params(**{field: 2}))[0] == B.MOE_ERR_INVALID_ARG
+    # per-wave readiness is defined for column splits only
+    assert B.select_partition(wl, _params(split_axis=1, readiness=1))[0] == \
+        B.MOE_ERR_INVALID_ARG
 
 
 def test_selector_argument_errors():

@@ -264,3 +264,49 @@ def test_rho_kh_changes_the_pick_by_hand():
     assert best.C == 2
     best0, _ = sel.select_from_work(30, 6, 2, 10, 1, 2, Fraction(3, 2), 1, 6)
     assert best0.C == 5
+
+
+def test_per_wave_readiness_by_hand():
+    """readiness = 1 on a small instance worked by hand: G = 4, o_comm =
+    o_comp = 1, W_comp = 6, W_comm = 3, L = 1, rho = 2.
+    C = 1 (P = 3): waves end 3, 6 tiles and release ceil(3/2) = 2, then 1
+    task: F = 1 + 2*2 = 5, then max(2, 5) + 2*1 = 7.
+    C = 2 (P = 2): three waves release 1 task each: F = 3, 5, 7.
+    C = 3 (P = 1): six waves release 1, 0, 1, 0, 1, 0: F = 3, 3, 5, 5, 7, 7.
+    All tie at 7 with Delta = 0, so C* = 1; the split-level model of the
+    paper gives T = 8, 7, 8 (A_0 = 2, 3, 6 and q = 6, 4, 2) and C* = 2."""
+    best, cands = sel.select_from_work(6, 3, 1, 4, 1, 1, Fraction(2), 1, 4, readiness=1)
+    assert [c.C for c in cands] == [1, 2, 3]
+    assert [c.F for c in cands] == [[5, 7], [3, 5, 7], [3, 3, 5, 5, 7, 7]]
+    assert [c.A for c in cands] == [[1, 2], [1, 2, 3], [1, 2, 3, 4, 5, 6]]
+    assert [c.delta for c in cands] == [0, 0, 0]
+    assert best.C == 1
+    best0, cands0 = sel.select_from_work(6, 3, 1, 4, 1, 1, Fraction(2), 1, 4)
+    assert [c.T for c in cands0] == [8, 7, 8] and best0.C == 2
+    # with the drain the last wave is served by C + P slots: C = 1 (P = 3)
+    # then ends at max(2, 5) + 2 * ceil(1 / 4) = 7 as well, C = 3 unchanged
+    bd, cd = sel.select_from_work(6, 3, 1, 4, 1, 1, Fraction(2), 1, 4, drain=True,
+                                  readiness=1)
+    assert [c.T for c in cd] == [7, 7, 7]
+
+
+def test_per_wave_readiness_releases_every_task_once():
+    """The released counts add up to all tasks, each wave's release is what
+    its completed tiles cover, and no wave is served before it ends."""
+    import random
+    rnd = random.Random(3)
+    for _ in range(300):
+        W_comp, W_comm = rnd.randint(0, 400), rnd.randint(1, 300)
+        L, G = rnd.randint(1, 4), rnd.randint(2, 64)
+        C = rnd.randint(1, G - 1)
+        c = sel.evaluate(C, W_comp, W_comm, L, G, 1, 1, Fraction(rnd.randint(1, 9), 4),
+                         readiness=1)
+        P = G - C
+        if L * W_comp == 0:
+            assert len(c.F) == 1
+            continue
+        assert len(c.A) == -(-L * W_comp // P)
+        assert all(f >= a for a, f in zip(c.A, c.F))
+        assert all(b >= a for a, b in zip(c.F, c.F[1:]))
+        # served at least as the split-level model's single last split
+        assert c.T >= Fraction(c.A[-1])
