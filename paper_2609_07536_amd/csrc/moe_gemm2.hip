@@ -256,6 +256,31 @@ __device__ __forceinline__ int opaque_tid() {
 // whole workgroup acquires (without it, a later acquire must precede any
 // read of the data these flags publish).  Returns false (and records a
 // timeout) if the bound expired.
+// One polling round trip of wave 0 over flags [i, min(i + kPollSpan, n)):
+// every lane loads kPollPerLane flags (64 apart, so each load instruction
+// reads 64 consecutive flags) before any is tested, so a split of ~1600
+// flags takes a few round trips of the agent-coherent loads instead of 25.
+// Returns the offset from i of the first flag not yet published, or
+// kPollSpan when all of them are (flags past n count as published).
+constexpr int kPollPerLane = 8;
+constexpr int kPollSpan = 64 * kPollPerLane;
+__device__ __forceinline__ int first_unpublished(uint32_t* flags, long long i, long long n,
+                                                 uint32_t epoch, int lane) {
+  uint32_t v[kPollPerLane];
+#pragma unroll
+  for (int j = 0; j < kPollPerLane; ++j) {
+    const long long idx = i + 64 * j + lane;
+    v[j] = idx < n ? __hip_atomic_load(&flags[idx], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                   : epoch;
+  }
+#pragma unroll
+  for (int j = 0; j < kPollPerLane; ++j) {
+    const u64 ready = __ballot(v[j] == epoch);
+    if (ready != ~0ull) return 64 * j + (int)__builtin_ctzll(~ready);
+  }
+  return kPollSpan;
+}
+
 __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& a,
                            bool acquire = true) {
   if (threadIdx.x < 64) {
@@ -264,16 +289,12 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
     long long i = 0, spins = 0;
     int ok = 1;
     while (i < n) {
-      const long long idx = i + lane;
-      const uint32_t v = idx < n ? __hip_atomic_load(&flags[idx], __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT)
-                                 : epoch;
-      const u64 ready = __ballot(v == epoch);
-      if (ready == ~0ull) {
-        i += 64;
+      const int first = first_unpublished(flags, i, n, epoch, lane);
+      if (first == kPollSpan) {
+        i += kPollSpan;
         continue;
       }
-      i += __builtin_ctzll(~ready);   // leading set flags stay set
+      i += first;   // leading set flags stay set
       if (++spins > a.spin_limit) {
         ok = 0;
         if (lane == 0)
@@ -311,16 +332,12 @@ __device__ long long wait_prefix(Smem& sm, uint32_t* flags, long long from, long
     long long i = from, spins = 0;
     int ok = 1;
     while (i < need) {
-      const long long idx = i + lane;
-      const uint32_t v = idx < need ? __hip_atomic_load(&flags[idx], __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT)
-                                    : epoch;
-      const u64 ready = __ballot(v == epoch);
-      if (ready == ~0ull) {
-        i += 64;
+      const int first = first_unpublished(flags, i, need, epoch, lane);
+      if (first == kPollSpan) {
+        i += kPollSpan;
         continue;
       }
-      i += __builtin_ctzll(~ready);
+      i += first;
       if (++spins > a.spin_limit) {
         ok = 0;
         if (lane == 0)
@@ -332,15 +349,14 @@ __device__ long long wait_prefix(Smem& sm, uint32_t* flags, long long from, long
     if (ok) {
       if (i > need) i = need;
       while (i < limit) {
-        const long long idx = i + lane;
-        const bool set = idx < limit && __hip_atomic_load(&flags[idx], __ATOMIC_RELAXED,
-                                                           __HIP_MEMORY_SCOPE_AGENT) == epoch;
-        const u64 ready = __ballot(set);
-        if (ready == ~0ull) {
-          i += 64;
+        // flags past limit must stop the prefix: test them as unpublished
+        const int first = first_unpublished(flags, i, limit, epoch, lane);
+        const long long room = limit - i;
+        if (first == kPollSpan && room > kPollSpan) {
+          i += kPollSpan;
           continue;
         }
-        i += __builtin_ctzll(~ready);
+        i += first < room ? first : room;
         break;
       }
     }
