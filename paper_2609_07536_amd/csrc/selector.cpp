@@ -47,7 +47,31 @@ typedef __int128 i128;
 
 const i128 kI64Max = (i128)INT64_MAX;
 
-inline int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+// ceil(a / b) for a >= 0, b > 0; in 32 bits when both fit (a 64-bit
+// division costs several times a 32-bit one, and a selection does hundreds)
+inline int64_t cdiv64(int64_t a, int64_t b) {
+  if (a == 0) return 0;
+  if (((uint64_t)a | (uint64_t)b) >> 32 == 0) return (int64_t)(((uint32_t)a - 1u) / (uint32_t)b + 1u);
+  return (a - 1) / b + 1;
+}
+
+inline i128 gcd128(i128 a, i128 b) {
+  if (a <= (i128)INT64_MAX && b <= (i128)INT64_MAX) {
+    uint64_t x = (uint64_t)a, y = (uint64_t)b;
+    while (y != 0) {
+      const uint64_t t = x % y;
+      x = y;
+      y = t;
+    }
+    return (i128)x;
+  }
+  while (b != 0) {
+    const i128 t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
 
 struct Model {
   int64_t W_comp = 0, W_comm = 0;
@@ -113,15 +137,10 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
     num *= (i128)(2 * (int64_t)wl->topk + 4) * width;
     den *= (i128)(2 * (int64_t)p->topk_ref + 4) * p->comm_tile_n_ref;
   }
-  // reduce in 128 bits, then require both to fit in 63 bits
-  i128 a = num, b = den;
-  while (b != 0) {
-    i128 t = a % b;
-    a = b;
-    b = t;
-  }
-  num /= a;
-  den /= a;
+  // reduce, then require both to fit in 63 bits
+  const i128 gd = gcd128(num, den);
+  num /= gd;
+  den /= gd;
   if (num > kI64Max || den > kI64Max) return MOE_ERR_INVALID_ARG;
   m->rho_num = (int64_t)num;
   m->rho_den = (int64_t)den;
@@ -133,7 +152,7 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
 // split arrival and finish times (one entry for C = 0: all tiles, then all
 // tasks; else L).
 bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int64_t* T_out,
-                    int64_t* delta_out, int32_t* R_out, int32_t* P_out, int* status,
+                    int32_t* R_out, int32_t* P_out, int* status,
                     int64_t* A_rec = nullptr, int64_t* F_rec = nullptr) {
   if (C == 0) {
     const int64_t P0 = (int64_t)p->occ_comp * p->num_cus;
@@ -146,7 +165,6 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
     if (A_rec) A_rec[0] = (int64_t)A;
     if (F_rec) F_rec[0] = (int64_t)F;
     *T_out = (int64_t)F;
-    *delta_out = cdiv64(m.W_comp, P0) * P0 - m.W_comp;
     *R_out = 0;
     *P_out = (int32_t)P0;
     return true;
@@ -154,8 +172,6 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
   const int64_t R = cdiv64(C, p->occ_comm);
   const int64_t P = (int64_t)p->occ_comp * ((int64_t)p->num_cus - R);
   if (P <= 0) return false;
-  const i128 q = (i128)m.rho_num * cdiv64(m.W_comm, C);
-  const i128 q_drain = (i128)m.rho_num * cdiv64(m.W_comm, (int64_t)C + P);
   i128 F = 0;
   if (m.readiness == 1) {
     // per compute wave: wave v releases the tasks of the tiles it completes
@@ -184,24 +200,33 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
       }
     }
   } else {
-  for (int s = 0; s < m.L; ++s) {
-    const i128 A = (i128)cdiv64((int64_t)(s + 1) * m.W_comp, P) * m.rho_den;
-    F = (A > F ? A : F) + (m.drain && s == m.L - 1 ? q_drain : q);
-    if (F > kI64Max) {
+    // 64-bit with overflow checks: F_s >= A_s and F_s >= q, so any term
+    // that overflows makes T(C) overflow too, the same error either way
+    int64_t q, q_drain, F64 = 0;
+    bool ovf = __builtin_mul_overflow(m.rho_num, cdiv64(m.W_comm, C), &q);
+    q_drain = q;
+    if (m.drain) ovf |= __builtin_mul_overflow(m.rho_num, cdiv64(m.W_comm, (int64_t)C + P), &q_drain);
+    for (int s = 0; s < m.L && !ovf; ++s) {
+      int64_t A;
+      ovf |= __builtin_mul_overflow(cdiv64((int64_t)(s + 1) * m.W_comp, P), m.rho_den, &A);
+      ovf |= __builtin_add_overflow(A > F64 ? A : F64, m.drain && s == m.L - 1 ? q_drain : q, &F64);
+      if (A_rec) A_rec[s] = A;
+      if (F_rec) F_rec[s] = F64;
+    }
+    if (ovf) {
       *status = MOE_ERR_INVALID_ARG;
       return false;
     }
-    if (A_rec) A_rec[s] = (int64_t)A;
-    if (F_rec) F_rec[s] = (int64_t)F;
+    F = F64;
   }
-  }
-  const int64_t V_comp = cdiv64(m.W_comp, P);
   *T_out = (int64_t)F;
-  *delta_out = V_comp * P - m.W_comp;
   *R_out = (int32_t)R;
   *P_out = (int32_t)P;
   return true;
 }
+
+// eq:tie-breaker: empty slots in the last compute wave of a split.
+inline int64_t delta_of(const Model& m, int64_t P) { return cdiv64(m.W_comp, P) * P - m.W_comp; }
 
 }  // namespace
 
@@ -211,18 +236,25 @@ extern "C" int moe_select_partition(const moe_workload_t* wl, const moe_select_p
   int st = build_model(wl, p, &m);
   if (st != MOE_OK) return st;
   bool found = false;
-  int64_t bestT = 0, bestD = 0;
+  int64_t bestT = 0, bestD = -1;   // bestD < 0: not computed yet (Delta is needed only on ties)
   int32_t bestC = 0, bestR = 0, bestP = 0;
   for (int32_t C = p->c_min; C <= p->c_max; ++C) {
-    int64_t T, D;
+    int64_t T;
     int32_t R, P;
     st = MOE_OK;
-    if (!eval_candidate(m, p, C, &T, &D, &R, &P, &st)) {
+    if (!eval_candidate(m, p, C, &T, &R, &P, &st)) {
       if (st != MOE_OK) return st;
       continue;
     }
     // lexicographic (T, Delta, C); C ascends, so strict improvement only
-    if (!found || T < bestT || (T == bestT && D < bestD)) {
+    bool better = !found || T < bestT;
+    int64_t D = -1;
+    if (!better && T == bestT) {
+      if (bestD < 0) bestD = delta_of(m, bestP);
+      D = delta_of(m, P);
+      better = D < bestD;
+    }
+    if (better) {
       found = true;
       bestT = T;
       bestD = D;
@@ -231,6 +263,7 @@ extern "C" int moe_select_partition(const moe_workload_t* wl, const moe_select_p
       bestP = P;
     }
   }
+  if (found && bestD < 0) bestD = delta_of(m, bestP);
   if (!found) return MOE_ERR_NO_LEGAL_PARTITION;
   if (out) {
     out->C = bestC;
@@ -283,10 +316,10 @@ extern "C" int moe_select_evaluate(const moe_workload_t* wl, const moe_select_pa
   const int32_t count = p->c_max - p->c_min + 1;
   if (!T_num_out || n < count) return MOE_ERR_INVALID_ARG;
   for (int32_t i = 0; i < count; ++i) {
-    int64_t T, D;
+    int64_t T;
     int32_t R, P;
     st = MOE_OK;
-    if (eval_candidate(m, p, p->c_min + i, &T, &D, &R, &P, &st)) {
+    if (eval_candidate(m, p, p->c_min + i, &T, &R, &P, &st)) {
       T_num_out[i] = T;
     } else {
       if (st != MOE_OK) return st;
@@ -312,10 +345,10 @@ extern "C" int moe_select_candidate(const moe_workload_t* wl, const moe_select_p
     entries = P <= 0 ? 1 : tiles == 0 ? 1 : cdiv64(tiles, P);
   }
   if (entries > INT32_MAX || ((A_out || F_out) && n < entries)) return MOE_ERR_INVALID_ARG;
-  int64_t T, D;
+  int64_t T;
   int32_t R, P;
   st = MOE_OK;
-  if (!eval_candidate(m, p, C, &T, &D, &R, &P, &st, A_out, F_out))
+  if (!eval_candidate(m, p, C, &T, &R, &P, &st, A_out, F_out))
     return st != MOE_OK ? st : MOE_ERR_NO_LEGAL_PARTITION;
   if (rho_num) *rho_num = m.rho_num;
   if (rho_den) *rho_den = m.rho_den;

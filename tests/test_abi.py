@@ -201,6 +201,50 @@ def test_candidate_internals_bit_exact_against_oracle():
                                    None, None, 0) == 2
 
 
+def test_scaled_time_overflow_boundary():
+    """The scaled integer time is int64: one tile, one task, L = 1 on two
+    slots, rho = X / 1, so every variant's T(C) is 1 + X compute-wave units
+    (C = 1: A = 1, q = X; C = 0: ceil(1/2) = 1 of each; drain and per-wave
+    readiness likewise).  X = 2^63 - 2 gives exactly INT64_MAX and matches
+    the oracle; X = 2^63 - 1 overflows and is an invalid argument.  The same
+    for the arrival term: two tiles on one compute slot at rho = 1 / X make
+    A = 2 X."""
+    big = 2 ** 63 - 1
+    wl, keep = B.make_workload(T=1, H=1, I=8, E=1, topk=1, splits=1, counts=[1])
+    variants = [dict(), dict(drain=1), dict(readiness=1), dict(readiness=1, drain=1),
+                dict(c_min=0, c_max=0)]
+    for v in variants:
+        kw = dict(tile_m=1, tile_n=1, comm_tile_m=1, comm_tile_n=1, num_cus=2,
+                  c_min=1, c_max=1, k_ref=8, tile_m_ref=1, tile_n_ref=1, rho_ref_den=1)
+        kw.update(v)
+        p = _params(rho_ref_num=big - 1, **kw)
+        r, part = B.select_partition(wl, p)
+        assert r == kw["c_min"] and part.T_num == big and part.T_den == 1, (v, r)
+        best = osel.select(1, 1, 8, 1, 1, 1, [1], _oracle_params(p))[0]
+        assert best.T == big, v
+        n, table, den = B.select_evaluate(wl, p)
+        assert n == 1 and table == [big], v
+        p = _params(rho_ref_num=big, **kw)
+        assert B.select_partition(wl, p)[0] == B.MOE_ERR_INVALID_ARG, v
+        assert B.select_evaluate(wl, p)[0] == B.MOE_ERR_INVALID_ARG, v
+        assert B.select_candidate(wl, p, kw["c_min"])[0] == B.MOE_ERR_INVALID_ARG, v
+    wl2, keep2 = B.make_workload(T=1, H=1, I=8, E=1, topk=1, splits=1, counts=[2])
+    for v in variants[:4]:
+        p = _params(tile_m=1, tile_n=1, comm_tile_m=1, comm_tile_n=1, num_cus=2, c_min=1,
+                    c_max=1, k_ref=8, tile_m_ref=1, tile_n_ref=1, rho_ref_num=1,
+                    rho_ref_den=big, **v)
+        assert B.select_partition(wl2, p)[0] == B.MOE_ERR_INVALID_ARG, v
+        # X = 2^62 - 2: A_0 = 2 X < 2^63 - 1, then + rho_num = 1; with per-wave
+        # readiness the one task is released by the first of the two waves
+        # (F_1 = X + 1), so T = max(2 X, X + 1) + 0 = 2 X
+        p.rho_ref_den = big // 2 - 1
+        r, part = B.select_partition(wl2, p)
+        want = 2 * (big // 2 - 1) + (0 if v.get("readiness") else 1)
+        assert r == 1 and part.T_den == big // 2 - 1 and part.T_num == want, v
+        best = osel.select(1, 1, 8, 1, 1, 1, [2], _oracle_params(p))[0]
+        assert best.T == Fraction(want, big // 2 - 1), v
+
+
 def test_split_selection_bit_exact_against_oracle():
     """moe_select_partition_splits (L as a decision variable) against the
     oracle's select_splits on random workloads, both split axes, with and
