@@ -115,6 +115,8 @@ struct KArgs {
   long long delay_ticks;      //   each split publish by delay_ticks (100 MHz), else 0
   uint32_t* task_ctr;         // [kMaxSplits]: next consumer task of each split (reset by
                               // workgroup 0 each launch)
+  uint32_t* split_flags;      // [L, kMaxGrid]: epoch once compute workgroup c has published
+                              // all its tiles of split s (or has none there); column splits
   int mode;                   // 0 owner-write, 1 fp32 atomic scatter, 2 owner-write over
                               // token bands (splits along the routed rows)
 };
@@ -186,6 +188,7 @@ struct Smem {
   int task;                   // consumer task claimed by the workgroup
   int task_band;              // token bands: last band holding a row of the staged task
   int prefix_end;             // end of the published prefix found by wait_prefix
+  int split_seen;             // a split's workgroup flags all set, seen with the claim
   u64 epoch;                  // this launch's epoch, read once at the start
 };
 
@@ -315,6 +318,12 @@ __device__ bool wait_flags(Smem& sm, uint32_t* flags, long long n, const KArgs& 
   if (acquire && threadIdx.x < 64) acquire_agent();
   __syncthreads();  // sm.flag may be rewritten by the next wait
   return ok;
+}
+
+// The acquire of wait_flags alone, for flags already seen published.
+__device__ __forceinline__ void acquire_workgroup() {
+  if (threadIdx.x < 64) acquire_agent();
+  __syncthreads();
 }
 
 // Waits until flags [from, need) are published, then extends the prefix over
@@ -1486,16 +1495,30 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
   // owner-write: tasks of comm_tm tokens x comm_tn columns; atomic scatter:
   // one task per compute tile
   const int tps = a.mode == 1 ? (int)W_comp : a.tasks_per_split;
+  // owner-write: a split is ready once every compute workgroup has flagged
+  // it (P flags, one per workgroup, instead of one per tile)
+  const bool by_wg = a.mode == 0;
   for (; cs.split < a.L; ++cs.split) {
     const int s = cs.split;
+    uint32_t* sflags = a.split_flags + (long long)s * kMaxGrid;
     while (true) {
       const u64 t_wait = now_100mhz();
-      if (threadIdx.x == 0)
-        sm.task = (int)min(__hip_atomic_fetch_add(&a.task_ctr[s], 1u, __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT),
-                           (uint32_t)tps);
+      if (threadIdx.x < 64) {
+        // the claim, and the first look at the split's flags, in one round trip
+        uint32_t claimed = 0;
+        if (threadIdx.x == 0)
+          claimed = __hip_atomic_fetch_add(&a.task_ctr[s], 1u, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+        const bool look = by_wg && s > cs.ready && a.P <= kPollSpan;
+        const int first = look ? first_unpublished(sflags, 0, a.P, flag_epoch(sm), threadIdx.x) : 0;
+        if (threadIdx.x == 0) {
+          sm.task = (int)min(claimed, (uint32_t)tps);
+          sm.split_seen = look && first == kPollSpan;
+        }
+      }
       __syncthreads();
       const int idx = sm.task;
+      const bool seen = sm.split_seen != 0;
       __syncthreads();   // sm.task is rewritten by the next claim
       if (idx >= tps) break;
       if (a.mode == 1) {
@@ -1514,8 +1537,14 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
       } else if (s > cs.ready) {
         // a task's metadata needs the inverse map only: once that is
         // acquired, it loads while the task's split is still computing
-        if (cs.inv_acq) ensure_task_meta(sm, a, idx, cs);
-        if (W_comp > 0 && !wait_flags(sm, a.tile_flags + (long long)s * W_comp, W_comp, a)) return;
+        if (cs.inv_acq && !seen) ensure_task_meta(sm, a, idx, cs);
+        if (seen) {
+          acquire_workgroup();
+        } else if (W_comp > 0) {
+          const bool ok = by_wg ? wait_flags(sm, sflags, a.P, a)
+                                : wait_flags(sm, a.tile_flags + (long long)s * W_comp, W_comp, a);
+          if (!ok) return;
+        }
         cs.ready = s;
         cs.inv_acq = true;   // that acquire covered the inverse map as well
       }
@@ -1636,6 +1665,18 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
     }
     int split_first = g_first;   // this workgroup's first tile of the current split
     int base = 0;                // ring slot of the current tile's stage 0
+    // Column splits: this workgroup's flag of split s (its compute index c)
+    // says that it has published all its tiles of s, or has none there; the
+    // owner-write consumers wait for a split's P flags.  Thread 0 stores
+    // them, in split order: splits before the first tile (none of its tiles
+    // there) now, the others with each split's publish.
+    int flagged = 0;   // (thread 0) splits [0, flagged) flagged
+    auto flag_splits = [&](int upto) {
+      for (; flagged < upto; ++flagged)
+        __hip_atomic_store(&a.split_flags[(long long)flagged * kMaxGrid + c], flag_epoch(sm),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+    if (!bands && threadIdx.x == 0) flag_splits(g_first >= 0 ? g_first / W_comp : a.L);
     // the inverse-map stores are done before the tile loop (once), so that
     // the compiler has nothing in flight to wait for inside it
     waitcnt_vm<0>();
@@ -1675,6 +1716,8 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
           const uint32_t epoch = flag_epoch(sm);
           for (int gg = split_first; gg <= g; gg += a.P)
             __hip_atomic_store(&a.tile_flags[gg], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          // this workgroup is done with every split before its next tile's
+          if (!bands) flag_splits(next ? g_next / W_comp : a.L);
           if (defer_inverse && split_first == g_first)   // first publish: also the inverse map
             __hip_atomic_store(&a.wg_flags[blockIdx.x], epoch, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
@@ -1794,7 +1837,7 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n, size_t epoch_at, u64 epo
 // ---- host side -----------------------------------------------------------------
 
 struct Layout {
-  size_t status, wg_flags, flags, tok_cnt, inv, Y, total;
+  size_t status, wg_flags, split_flags, flags, tok_cnt, inv, Y, total;
   long long rows, max_tiles;
   int nsplit, ntps, comm_tm, comm_tn, cb_per_split, tasks_per_split;
 };
@@ -1848,6 +1891,8 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
   off += 512;
   L->wg_flags = off;
   off += (size_t)kMaxGrid * 4;
+  L->split_flags = off;
+  off += (size_t)wl->splits * kMaxGrid * 4;
   L->flags = off;
   off = round_up(off + (size_t)L->max_tiles * 4, 256);
   L->tok_cnt = off;
@@ -2204,6 +2249,7 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.inv = reinterpret_cast<int32_t*>(ws + L.inv);
   a.status = reinterpret_cast<uint32_t*>(ws + L.status);
   a.task_ctr = reinterpret_cast<uint32_t*>(ws + L.status + 256);
+  a.split_flags = reinterpret_cast<uint32_t*>(ws + L.split_flags);
   a.trace = reinterpret_cast<u64*>(trace);
   a.rows = L.rows;
   a.max_tiles = L.max_tiles;
