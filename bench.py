@@ -161,6 +161,21 @@ def breakdown(dw, C, mode=None, reps=5):
     return used, gp, comb
 
 
+def task_busy(dw, tasks, mode=None):
+    """Busy time of each traced consumer task, in ticks, scaled to the
+    launch's comm_tile_m tokens: owner-write tasks of the last split hold
+    comm_tile_m_last tokens, and a task's work is proportional to its tokens
+    (the assumption rho's scaling makes)."""
+    busy = (tasks[:, 2] - tasks[:, 1]).astype(np.float64)
+    if mode in (None, 0):
+        p = dw.B.launch_params(dw.wl)
+        tm, tm_last = p.comm_tile_m, p.comm_tile_m_last or p.comm_tile_m
+        if tm_last != tm:
+            tps = -(-dw.w.T // tm) * -(-(-(-dw.w.H // dw.w.L)) // 1024)
+            busy[(dw.w.L - 1) * tps:] *= tm / tm_last
+    return busy
+
+
 def calibrate(dw, C_ref=32, reps=5, mode=None):
     """rho_ref: one consumer-task wave over one compute-tile wave, measured at
     a fixed consumer count (the paper's calibration procedure)."""
@@ -168,7 +183,7 @@ def calibrate(dw, C_ref=32, reps=5, mode=None):
     for _ in range(reps):
         _, tiles, tasks = dw.trace(C_ref, mode)
         tile_t.append((tiles[:, 3] - tiles[:, 0]).mean())
-        task_t.append((tasks[:, 2] - tasks[:, 1]).mean())
+        task_t.append(task_busy(dw, tasks, mode).mean())
     tile_us = float(np.median(tile_t)) * TICK_S * 1e6
     task_us = float(np.median(task_t)) * TICK_S * 1e6
     return {"C_ref": C_ref, "compute_wave_us": round(tile_us, 3),
@@ -379,8 +394,9 @@ def model_validation(B, torch, points, runs, Cs):
             L = dw.w.L
             A = [float((tiles[s * W_comp:(s + 1) * W_comp, 3].max() - t0) * TICK_S * 1e6)
                  for s in range(L)]
-            F = [float((tasks[s * W_comm:(s + 1) * W_comm, 2].max() - t0) * TICK_S * 1e6)
-                 for s in range(L)]
+            # (the last split's records run to the end: its tasks are finer)
+            F = [float((tasks[s * W_comm:(s + 1) * W_comm if s < L - 1 else None, 2].max()
+                        - t0) * TICK_S * 1e6) for s in range(L)]
             # the model's A_s and F_s of this candidate, as the library evaluates them
             _, _, den, A_m, F_m = B.select_candidate(dw.wl, pt.params, C)
             splits.append({"w": pt.name, "C": C,
@@ -414,7 +430,7 @@ def rho_validation(B, torch, reps=5, C_ref=32):
         for _ in range(reps):
             _, tiles, tasks = dw.trace(C_ref)
             tile_t.append((tiles[:, 3] - tiles[:, 0]).mean())
-            task_t.append((tasks[:, 2] - tasks[:, 1]).mean())
+            task_t.append(task_busy(dw, tasks).mean())
         tile_us = float(np.median(tile_t)) * TICK_S * 1e6
         task_us = float(np.median(task_t)) * TICK_S * 1e6
         p = B.launch_params(dw.wl)

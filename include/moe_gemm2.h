@@ -102,6 +102,9 @@ typedef struct {
   int32_t readiness;                 /* 0: consumer work becomes ready a split at a time (the
                                         paper); 1: a compute wave at a time (consumer tasks
                                         that each need one compute tile, the atomic scatter) */
+  int32_t comm_tile_m_last;          /* tokens of the last split's consumer tasks (T_M^last);
+                                        0 or comm_tile_m: as the other splits' (the paper).
+                                        Column splits with readiness = 0 only */
 } moe_select_params_t;
 
 /* The chosen partition.  T(C) = T_num / T_den in compute-wave units; W_comp
@@ -143,7 +146,15 @@ typedef struct {
  *   rho_kh = 1: rho of eq:rho-scaling times
  *     (2 topk + 4) / (2 topk_ref + 4) * w / comm_tile_n_ref, with the task
  *     width w = min(comm_tile_n, ceil(N/L)) (column splits) or
- *     min(comm_tile_n, N) (token bands); topk_ref, comm_tile_n_ref > 0.
+ *     min(comm_tile_n, N) (token bands); topk_ref, comm_tile_n_ref > 0;
+ *   comm_tile_m_last = T_M^last > 0 (column splits, readiness = 0): the last
+ *     split's tasks hold T_M^last tokens:
+ *     W_last = ceil(ceil(M/D)/T_M^last) ceil(ceil(N/L)/T_N^comm) tasks of
+ *     rho_last = rho T_M^last / T_M^comm, the last split served as
+ *     F_{L-1} = max(A_{L-1}, F_{L-2}) + rho_last ceil(W_last / C) (drain:
+ *     C + P slots), and with a : b = T_M^comm : T_M^last in lowest terms
+ *     T(0) = ceil(L W_comp / P0) + (rho/a) ceil((a (L-1) W_comm + b W_last) / P0);
+ *     T_den is then rho's denominator times a / gcd(rho's numerator, a).
  * Pure host code: no HIP call, no allocation, thread-safe.
  * Returns C* >= c_min and fills *out when out != NULL; MOE_ERR_INVALID_ARG for a
  * null wl/p, non-positive dimensions or parameters, a negative host count or
@@ -190,7 +201,8 @@ int moe_select_evaluate(const moe_workload_t* wl, const moe_select_params_t* p,
                         int64_t* T_num_out, int32_t n, int64_t* T_den_out);
 
 /* Parameters for the fused kernel on a HIP device: its tile shapes (the
- * owner-write consumer task at its full size of 64 tokens x 1024 columns),
+ * owner-write consumer task at its full size of 64 tokens x 1024 columns,
+ * the last split's at 32 tokens: comm_tile_m_last = 32),
  * its occupancy from hipOccupancyMaxActiveBlocksPerMultiprocessor (capped
  * by its LDS and register budget), the device's CU count, the candidate set
  * C = 0..64 (C = 0 is the role switch, a legal launch of this kernel) and
@@ -221,7 +233,9 @@ int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk, moe_sele
  * launch would have fewer than 512 tasks (splits * ceil(T/TM) *
  * ceil(H/splits/1024)), so that a small batch's combine still spreads over
  * every CU; comm_tile_m = TM and rho_ref, calibrated for 64-token tasks, is
- * scaled by TM/64 (a task's bytes are proportional to its tokens).  Mode 1:
+ * scaled by TM/64 (a task's bytes are proportional to its tokens); the last
+ * split's tasks take TM_last = TM/2 tokens when TM > 16 (else TM), so that
+ * the launch ends evenly over the CUs: comm_tile_m_last = TM_last.  Mode 1:
  * as moe_gemm2_default_params_ex(device, 1, wl->topk).  Mode 2: tasks of
  * TM tokens x min(1024, H) columns of the full width, TM = 64 halved down
  * to 16 while there would be fewer than 512 (ceil(T/TM) ceil(H/1024)),
@@ -307,11 +321,13 @@ int moe_gemm2_combine(const void* x_perm, const void* w2, const int32_t* expert_
  * publish for a workgroup's last tile of a split); then, from word
  * 4 * max_tiles (max_tiles = splits * ceil(ceil(H/splits)/256) *
  * (ceil(rows/256) + E)), for each consumer task j, words 4j..4j+3 = wait
- * start, wait end, finish, workgroup id (task j: split j / tasks_per_split,
- * token block and column block from j % tasks_per_split, with
- * tasks_per_split = ceil(T/TM) * ceil(H/splits/1024) and TM the task's
- * tokens given by moe_gemm2_launch_params).  The arithmetic and the result are
- * identical to the untraced call. */
+ * start, wait end, finish, workgroup id (task j: split
+ * s = min(j / tasks_per_split, splits - 1), task i = j - s tasks_per_split of
+ * that split, token block and column block from i, with tasks_per_split =
+ * ceil(T/TM) * ceil(H/splits/1024); the last split has
+ * ceil(T/TM_last) * ceil(H/splits/1024) tasks; TM and TM_last are the
+ * comm_tile_m and comm_tile_m_last that moe_gemm2_launch_params gives).  The
+ * arithmetic and the result are identical to the untraced call. */
 int moe_gemm2_combine_traced(const void* x_perm, const void* w2, const int32_t* expert_offsets,
                              const int32_t* token_ids, const float* gate_w, float* out,
                              const moe_workload_t* wl, int32_t num_consumers,
@@ -393,7 +409,8 @@ int moe_gemm2_combine_noalloc(const void* x_perm, const void* w2, const int32_t*
 
 /* Bytes the trace buffer needs for this workload (0 for an invalid one):
  * 4 * max_tiles words for the compute tiles, then 4 words for each of
- * max(splits * tasks_per_split, band tasks, max_tiles) consumer tasks
+ * max((splits - 1) * tasks_per_split + last split's tasks, band tasks,
+ * max_tiles) consumer tasks
  * (tasks_per_split as for moe_gemm2_combine_traced, band tasks as for
  * moe_gemm2_combine_ex mode 2); max_tiles = splits * ceil(ceil(H/splits)/256)
  * * (ceil(rows/256) + E). */
@@ -477,7 +494,7 @@ int moe_gemm2_status(void* workspace, void* stream, int clear);
 /* Static description of an error code. */
 const char* moe_strerror(int status);
 
-/* ABI version of this header (major * 100 + minor): 106. */
+/* ABI version of this header (major * 100 + minor): 107. */
 int moe_gemm2_abi_version(void);
 
 #ifdef __cplusplus

@@ -54,11 +54,22 @@ special case split_axis = 0, drain = False, one given L):
     the calibration's, k bf16 rows read and one fp32 output written per
     token and column: rho times (2 k + 4) / (2 k_ref + 4) times w / w_ref,
     with the task width w = min(T_N^comm, ceil(N/L)) for column splits and
-    min(T_N^comm, N) for token bands.
+    min(T_N^comm, N) for token bands;
+  * a finer last split (column splits, readiness 0): the last split's
+    consumer tasks hold T_M^last tokens instead of T_M^comm, so it has
+    W_last = ceil(ceil(M/D) / T_M^last) ceil(ceil(N/L) / T_N^comm) tasks,
+    each served in rho_last = rho T_M^last / T_M^comm (a task's bytes follow
+    its tokens): F_{L-1} = max(A_{L-1}, F_{L-2}) + rho_last ceil(W_last / C)
+    (drain: C + P slots).  For C = 0 every task is counted in units of rho/a,
+    with a : b = T_M^comm : T_M^last in lowest terms (a units for a task of
+    the other splits, b for one of the last split), all of them over the P0
+    slots: T(0) = ceil(L W_comp / P0) + (rho/a) ceil((a (L-1) W_comm + b W_last) / P0).
+    T_M^last = T_M^comm is the model without this extension.
 """
 from __future__ import annotations
 
 import dataclasses
+import math
 from fractions import Fraction
 from typing import List, Optional, Sequence
 
@@ -127,14 +138,27 @@ def task_width(H: int, L: int, comm_n: int, split_axis: int = 0) -> int:
     return min(span, comm_n)
 
 
+@dataclasses.dataclass
+class LastSplit:
+    """The finer last split: its task count, its rho, and a : b."""
+    W: int
+    rho: Fraction
+    a: int
+    b: int
+
+
 def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
              o_comp: int, rho: Fraction, drain: bool = False,
-             readiness: int = 0) -> Optional[Candidate]:
+             readiness: int = 0, last: Optional[LastSplit] = None) -> Optional[Candidate]:
     """The recurrence for one candidate C; None if P(C) <= 0 (illegal)."""
     if C == 0:
         P0 = o_comp * G
         A_last = cdiv(L * W_comp, P0)
-        q = Fraction(rho) * cdiv(L * W_comm, P0)
+        if last is None:
+            q = Fraction(rho) * cdiv(L * W_comm, P0)
+        else:
+            units = last.a * (L - 1) * W_comm + last.b * last.W
+            q = Fraction(rho) / last.a * cdiv(units, P0)
         T = A_last + q
         V_comp = cdiv(W_comp, P0)
         return Candidate(C=0, R=0, P=P0, A=[A_last], V_comm=cdiv(L * W_comm, P0), q=q,
@@ -151,10 +175,12 @@ def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
     A = [cdiv((s + 1) * W_comp, P) for s in range(L)]
     F: List[Fraction] = []
     prev = Fraction(0)
+    W_l, rho_l = (W_comm, Fraction(rho)) if last is None else (last.W, last.rho)
     for s in range(L):
-        if drain and s == L - 1:
-            # every slot serves the last split once its tiles are done
-            prev = max(Fraction(A[s]), prev) + Fraction(rho) * cdiv(W_comm, C + P)
+        if s == L - 1:
+            # the last split: its own tasks, and with drain every slot serves
+            # it once its tiles are done
+            prev = max(Fraction(A[s]), prev) + rho_l * cdiv(W_l, C + P if drain else C)
         else:
             prev = max(Fraction(A[s]), prev) + q
         F.append(prev)
@@ -190,13 +216,14 @@ def _per_wave(C, R, P, W_comp, W_comm, L, rho, drain, V_comm, q, V_comp) -> Cand
 
 def select_from_work(W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
                      o_comp: int, rho: Fraction, c_min: int, c_max: int,
-                     drain: bool = False, readiness: int = 0):
+                     drain: bool = False, readiness: int = 0,
+                     last: Optional[LastSplit] = None):
     """Argmin of T(C) over the legal C, then smallest Delta, then smallest C.
 
     Returns (best Candidate or None, list of all legal candidates)."""
     cands = []
     for C in range(c_min, c_max + 1):
-        c = evaluate(C, W_comp, W_comm, L, G, o_comm, o_comp, rho, drain, readiness)
+        c = evaluate(C, W_comp, W_comm, L, G, o_comm, o_comp, rho, drain, readiness, last)
         if c is not None:
             cands.append(c)
     if not cands:
@@ -228,6 +255,7 @@ class SelectParams:
     topk_ref: int = 6
     comm_tile_n_ref: int = 1024
     readiness: int = 0
+    comm_tile_m_last: int = 0      # 0: the last split's tasks as the others'
 
 
 def select(T: int, H: int, I: int, E: int, topk: int, L: int,
@@ -242,10 +270,25 @@ def select(T: int, H: int, I: int, E: int, topk: int, L: int,
         rho *= task_bytes_factor(topk, p.topk_ref,
                                  task_width(H, L, p.comm_tile_n, p.split_axis),
                                  p.comm_tile_n_ref)
+    last = last_split(T, D, H, L, p, rho)
     best, cands = select_from_work(W_comp, W_comm, L, p.num_cus, p.occ_comm,
                                    p.occ_comp, rho, p.c_min, p.c_max, bool(p.drain),
-                                   p.readiness)
+                                   p.readiness, last)
     return best, cands, W_comp, W_comm, rho
+
+
+def last_split(T: int, D: int, H: int, L: int, p: SelectParams,
+               rho: Fraction) -> Optional[LastSplit]:
+    """The finer last split of the parameters, or None when its tasks are
+    the other splits' (then the model is the paper's)."""
+    tm, tm_last = p.comm_tile_m, p.comm_tile_m_last or p.comm_tile_m
+    if tm_last == tm:
+        return None
+    if p.split_axis != 0 or p.readiness != 0:
+        raise ValueError("a finer last split is defined for column splits ready a split at a time")
+    g = math.gcd(tm, tm_last)
+    return LastSplit(W=comm_work(T, D, H, L, tm_last, p.comm_tile_n),
+                     rho=Fraction(rho) * Fraction(tm_last, tm), a=tm // g, b=tm_last // g)
 
 
 def select_splits(T: int, H: int, I: int, E: int, topk: int,

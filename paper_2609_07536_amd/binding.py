@@ -62,7 +62,8 @@ class SelectParams(ctypes.Structure):
                 ("tile_n_ref", ctypes.c_int32), ("d_ref", ctypes.c_int32),
                 ("split_axis", ctypes.c_int32), ("drain", ctypes.c_int32),
                 ("rho_kh", ctypes.c_int32), ("topk_ref", ctypes.c_int32),
-                ("comm_tile_n_ref", ctypes.c_int32), ("readiness", ctypes.c_int32)]
+                ("comm_tile_n_ref", ctypes.c_int32), ("readiness", ctypes.c_int32),
+                ("comm_tile_m_last", ctypes.c_int32)]
 
 
 class Partition(ctypes.Structure):

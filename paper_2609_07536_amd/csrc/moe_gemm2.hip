@@ -108,6 +108,8 @@ struct KArgs {
   int comm_tn;                // consumer task width (<= kCommTN)
   int cb_per_split;           // consumer column blocks per split
   int tasks_per_split;
+  int comm_tm_last;           // owner-write (column splits): tokens of the last split's
+  int tasks_last;             //   tasks (finer, so that the launch ends evenly) and their count
   u64* epoch_word;            // the workspace's last completed launch epoch
   uint32_t* done_ctr;         // workgroups of this launch that have finished
   uint32_t* start_ctr;        // workgroups of this launch that have started
@@ -1426,20 +1428,34 @@ struct Consumer {
   int ready;     // splits [0, ready] were acquired by this workgroup (token bands:
                  // the tiles [0, ready) are known published)
   int split;     // the first split that may still have unclaimed tasks
-  int meta_t0;   // token block whose metadata is in LDS (-1: none)
+  int meta_t0;   // first token of the block whose metadata is in LDS (-1: none)
+  int meta_n;    // ... and its token count
   bool inv_ok;   // every workgroup's inverse-map share is published
   bool inv_acq;  // ... and acquired by this workgroup
   int tiles;     // atomic scatter: the tiles [0, tiles) of the global sequence are
                  // known published and acquired by this workgroup
 };
 
-// The owner-write task idx's metadata in LDS (unless it is there already).
-__device__ void ensure_task_meta(Smem& sm, const KArgs& a, int idx, Consumer& cs) {
-  const int t0 = (idx / a.cb_per_split) * a.comm_tm;
-  if (t0 != cs.meta_t0) {
+// Owner-write tasks of split s: their token count and how many there are
+// (column splits cut the last split's token blocks finer).
+__device__ __forceinline__ int task_tm(const KArgs& a, int s) {
+  return a.mode == 0 && s == a.L - 1 ? a.comm_tm_last : a.comm_tm;
+}
+__device__ __forceinline__ int split_tasks(const KArgs& a, int s) {
+  return a.mode == 0 && s == a.L - 1 ? a.tasks_last : a.tasks_per_split;
+}
+
+// The owner-write task idx's metadata in LDS (unless it is there already:
+// a block's metadata also serves any block that starts at the same token
+// and has no more tokens).
+__device__ void ensure_task_meta(Smem& sm, const KArgs& a, int tm, int idx, Consumer& cs) {
+  const int t0 = (idx / a.cb_per_split) * tm;
+  const int ntok = min(tm, a.T - t0);
+  if (t0 != cs.meta_t0 || ntok > cs.meta_n) {
     __syncthreads();   // every wave is done with the previous task's metadata
-    load_task_meta(sm, task_meta(sm), a, count_epoch(sm), t0, min(a.comm_tm, a.T - t0));
+    load_task_meta(sm, task_meta(sm), a, count_epoch(sm), t0, ntok);
     cs.meta_t0 = t0;
+    cs.meta_n = ntok;
   }
 }
 
@@ -1450,13 +1466,14 @@ __device__ void run_task(Smem& sm, const KArgs& a, int W_comp, int tps, int s, i
   if (a.mode == 1) {
     scatter_tile(a, decode_tile(sm, a, W_comp, s * W_comp + idx));
   } else {
+    const int tm = task_tm(a, s);
     const int tb = idx / a.cb_per_split;
     const int cb = idx - tb * a.cb_per_split;
-    const int t0 = tb * a.comm_tm;
-    const int ntok = min(a.comm_tm, a.T - t0);
+    const int t0 = tb * tm;
+    const int ntok = min(tm, a.T - t0);
     const int col0 = s * a.nsplit + cb * a.comm_tn;
     const int ncols = min(a.comm_tn, (s + 1) * a.nsplit - col0);
-    ensure_task_meta(sm, a, idx, cs);
+    ensure_task_meta(sm, a, tm, idx, cs);
     consume_task(a, task_meta(sm), t0, ntok, col0, ncols, s * (a.ysplit - a.nsplit));
   }
   if (a.trace) {
@@ -1494,6 +1511,8 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
   }
   // owner-write: tasks of comm_tm tokens x comm_tn columns; atomic scatter:
   // one task per compute tile
+  // (trace records: split s's tasks start at s tps, only the last split's
+  // count differs)
   const int tps = a.mode == 1 ? (int)W_comp : a.tasks_per_split;
   // owner-write: a split is ready once every compute workgroup has flagged
   // it (P flags, one per workgroup, instead of one per tile)
@@ -1501,6 +1520,7 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
   for (; cs.split < a.L; ++cs.split) {
     const int s = cs.split;
     uint32_t* sflags = a.split_flags + (long long)s * kMaxGrid;
+    const int ntask = a.mode == 1 ? (int)W_comp : split_tasks(a, s);
     while (true) {
       const u64 t_wait = now_100mhz();
       if (threadIdx.x < 64) {
@@ -1512,7 +1532,7 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
         const bool look = by_wg && s > cs.ready && a.P <= kPollSpan;
         const int first = look ? first_unpublished(sflags, 0, a.P, flag_epoch(sm), threadIdx.x) : 0;
         if (threadIdx.x == 0) {
-          sm.task = (int)min(claimed, (uint32_t)tps);
+          sm.task = (int)min(claimed, (uint32_t)ntask);
           sm.split_seen = look && first == kPollSpan;
         }
       }
@@ -1520,7 +1540,7 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
       const int idx = sm.task;
       const bool seen = sm.split_seen != 0;
       __syncthreads();   // sm.task is rewritten by the next claim
-      if (idx >= tps) break;
+      if (idx >= ntask) break;
       if (a.mode == 1) {
         // a scatter task needs only its own tile: it waits for the published
         // prefix of the tile sequence up to that tile (tiles are claimed in
@@ -1537,7 +1557,7 @@ __device__ void consumer_loop(Smem& sm, const KArgs& a, int W_comp, Consumer& cs
       } else if (s > cs.ready) {
         // a task's metadata needs the inverse map only: once that is
         // acquired, it loads while the task's split is still computing
-        if (cs.inv_acq && !seen) ensure_task_meta(sm, a, idx, cs);
+        if (cs.inv_acq && !seen) ensure_task_meta(sm, a, task_tm(a, s), idx, cs);
         if (seen) {
           acquire_workgroup();
         } else if (W_comp > 0) {
@@ -1583,7 +1603,7 @@ __device__ void consumer_loop_bands(Smem& sm, const KArgs& a, Consumer& cs) {
     const int ntok = min(a.comm_tm, a.T - t0);
     const int col0 = cb * a.comm_tn;
     const int ncols = min(a.comm_tn, a.H - col0);
-    ensure_task_meta(sm, a, idx, cs);
+    ensure_task_meta(sm, a, a.comm_tm, idx, cs);
     const int need = sm.band_start[min(sm.task_band, a.L - 1) + 1];
     if (need > cs.ready) {   // cs.ready: tiles [0, ready) are published and acquired
       if (!wait_flags(sm, a.tile_flags + cs.ready, need - cs.ready, a)) return;
@@ -1757,10 +1777,10 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
   // consumers, and role-switch workgroups after their tiles (one call site,
   // so that the loop is inlined)
   if (bands) {
-    Consumer cs = {0, 0, -1, false, false};
+    Consumer cs = {0, 0, -1, 0, false, false};
     consumer_loop_bands(sm, a, cs);
   } else {
-    Consumer cs = {-1, 0, -1, false, false};
+    Consumer cs = {-1, 0, -1, 0, false, false};
     consumer_loop(sm, a, W_comp, cs);
   }
 }
@@ -1839,10 +1859,13 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n, size_t epoch_at, u64 epo
 struct Layout {
   size_t status, wg_flags, split_flags, flags, tok_cnt, inv, Y, total;
   long long rows, max_tiles;
-  int nsplit, ntps, comm_tm, comm_tn, cb_per_split, tasks_per_split;
+  int nsplit, ntps, comm_tm, comm_tn, cb_per_split, tasks_per_split, comm_tm_last, tasks_last;
 };
 
 inline size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Tokens of the last split's owner-write tasks for tasks of comm_tm tokens.
+inline int last_split_tm(int comm_tm) { return comm_tm > kCommTMMin ? comm_tm / 2 : comm_tm; }
 
 int check_shape(const moe_workload_t* wl) {
   if (!wl) return MOE_ERR_INVALID_ARG;
@@ -1882,6 +1905,11 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
              kTaskTarget)
     L->comm_tm /= 2;
   L->tasks_per_split = ((wl->T + L->comm_tm - 1) / L->comm_tm) * L->cb_per_split;
+  // The last split's tasks take half the tokens (down to kCommTMMin): they
+  // start only after the last tiles, so finer tasks end the launch more
+  // evenly over the CUs.
+  L->comm_tm_last = last_split_tm(L->comm_tm);
+  L->tasks_last = ((wl->T + L->comm_tm_last - 1) / L->comm_tm_last) * L->cb_per_split;
   L->max_tiles = (long long)wl->splits * L->ntps * ((L->rows + kBM - 1) / kBM + wl->E);
   size_t off = 0;
   L->status = off;   // word 0: status bits; bytes 4..255: reserved;
@@ -2010,6 +2038,8 @@ void fill_params(const DevInfo& d, int mode, int topk, int comm_tm, moe_select_p
     p->rho_ref_num *= comm_tm;
     p->rho_ref_den *= kCommTM;
   }
+  // owner-write over column splits: the last split's tasks are cut finer
+  p->comm_tile_m_last = mode == 0 ? last_split_tm(comm_tm) : 0;
   p->k_ref = 704;
   p->tile_m_ref = kBM;
   p->tile_n_ref = kBN;
@@ -2275,6 +2305,8 @@ int launch(const void* x_perm, const void* w2, const int32_t* expert_offsets,
   a.comm_tn = L.comm_tn;
   a.cb_per_split = L.cb_per_split;
   a.tasks_per_split = L.tasks_per_split;
+  a.comm_tm_last = L.comm_tm_last;
+  a.tasks_last = L.tasks_last;
   a.mode = mode;
   if (mode == 2) {   // token bands: every band spans the full width
     const BandTasks bt = band_tasks(wl);
@@ -2332,7 +2364,7 @@ extern "C" size_t moe_gemm2_trace_size(const moe_workload_t* wl) {
   // atomic scatter, one per compute tile)
   // consumer-task records: the most of the column-split tasks, the token-band
   // tasks and (atomic scatter) the compute tiles
-  long long tasks = (long long)wl->splits * L.tasks_per_split;
+  long long tasks = (long long)(wl->splits - 1) * L.tasks_per_split + L.tasks_last;
   const long long band = band_tasks(wl).tasks;
   if (band > tasks) tasks = band;
   return (size_t)(4 * L.max_tiles + 4 * (tasks > L.max_tiles ? tasks : L.max_tiles)) * 8;

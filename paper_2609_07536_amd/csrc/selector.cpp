@@ -2,8 +2,9 @@
 // paper's Method section, evaluated exactly on the host.
 //
 // Time is kept as an integer count of 1/rho_den compute waves, where
-// rho = rho_num / rho_den is the reduced service-time ratio of eq:rho-scaling,
-// so T(C) compares exactly and ties (eq:tie-breaker) are real ties.
+// rho = rho_num / rho_den is the service-time ratio of eq:rho-scaling
+// (reduced, unless the last split's tasks are cut finer: see below), so T(C)
+// compares exactly and ties (eq:tie-breaker) are real ties.
 //
 //   W_comp = g * (sum_e ceil(M_e/T_M)) * ceil(ceil(N/L)/T_N)       eq:compute-work
 //   W_comm = ceil(ceil(M/D)/T_M^comm) * ceil(ceil(N/L)/T_N^comm)    eq:communication-work
@@ -35,7 +36,16 @@
 //       F_v = max(v, F_{v-1}) + rho ceil(w_v / C),   T(C) = F_V
 //     (drain: the last wave's tasks over C + P slots);
 //   rho_kh = 1: rho also scales with the consumer task's bytes,
-//       (2 k + 4) / (2 k_ref + 4) * w / w_ref (w: the task width).
+//       (2 k + 4) / (2 k_ref + 4) * w / w_ref (w: the task width);
+//   comm_tile_m_last = T_M^last (column splits, split readiness): the last
+//     split's consumer tasks hold T_M^last tokens, so
+//       W_last = ceil(ceil(M/D)/T_M^last) ceil(ceil(N/L)/T_N^comm),
+//       rho_last = rho T_M^last / T_M^comm,
+//       F_{L-1} = max(A_{L-1}, F_{L-2}) + rho_last ceil(W_last / C)  (drain: C + P),
+//     and for C = 0, with a : b = T_M^comm : T_M^last in lowest terms (a task
+//     of the other splits is a units of rho/a, one of the last split b units),
+//       T(0) = ceil(L W_comp / P0) + (rho/a) ceil((a (L-1) W_comm + b W_last) / P0).
+//     Time is then counted in 1/(rho_den a / gcd(rho_num, a)) compute waves.
 #include <cstdint>
 #include <cstdlib>
 
@@ -75,7 +85,12 @@ inline i128 gcd128(i128 a, i128 b) {
 
 struct Model {
   int64_t W_comp = 0, W_comm = 0;
-  int64_t rho_num = 0, rho_den = 1;
+  int64_t rho_num = 0, rho_den = 1;   // rho over the time unit (not reduced when the last
+                                      // split's tasks are cut finer)
+  int64_t W_last = 0;                 // consumer tasks of the last split
+  int64_t rho_last = 0;               // rho_last over the same unit
+  int64_t a = 1, b = 1;               // T_M^comm : T_M^last in lowest terms
+  int64_t rho_unit = 0;               // rho / a over the time unit
   int L = 1;
   int drain = 0;
   int readiness = 0;
@@ -111,13 +126,19 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
   if (p->readiness != 0 && p->readiness != 1) return MOE_ERR_INVALID_ARG;
   if (p->readiness == 1 && p->split_axis != 0) return MOE_ERR_INVALID_ARG;
   const int64_t token_blocks = cdiv64(cdiv64(wl->T, wl->ranks), p->comm_tile_m);
+  if (p->comm_tile_m_last < 0) return MOE_ERR_INVALID_ARG;
+  const int64_t tm_last = p->comm_tile_m_last > 0 ? p->comm_tile_m_last : p->comm_tile_m;
+  if (tm_last != p->comm_tile_m && (p->split_axis != 0 || p->readiness != 0))
+    return MOE_ERR_INVALID_ARG;   // defined for column splits ready a split at a time
   if (p->split_axis == 0) {
     const int64_t n_split = cdiv64(wl->H, wl->splits);
     m->W_comp = (int64_t)p->groups * m_tiles * cdiv64(n_split, p->tile_n);
     m->W_comm = token_blocks * cdiv64(n_split, p->comm_tile_n);
+    m->W_last = cdiv64(cdiv64(wl->T, wl->ranks), tm_last) * cdiv64(n_split, p->comm_tile_n);
   } else {
     m->W_comp = cdiv64((int64_t)p->groups * m_tiles, wl->splits) * cdiv64(wl->H, p->tile_n);
     m->W_comm = cdiv64(token_blocks, wl->splits) * cdiv64(wl->H, p->comm_tile_n);
+    m->W_last = m->W_comm;
   }
   m->L = wl->splits;
   m->drain = p->drain;
@@ -142,8 +163,19 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
   num /= gd;
   den /= gd;
   if (num > kI64Max || den > kI64Max) return MOE_ERR_INVALID_ARG;
-  m->rho_num = (int64_t)num;
-  m->rho_den = (int64_t)den;
+  // the last split's rho over a common unit: rho = num/den = (num a/g)/(den a/g)
+  // and rho_last = (num b/g)/(den a/g), g = gcd(num, a), integral as gcd(a, b) = 1
+  const i128 gab = gcd128(p->comm_tile_m, tm_last);
+  const i128 a = p->comm_tile_m / gab, b = tm_last / gab;
+  const i128 g = gcd128(num, a);
+  const i128 rn = num * (a / g), rd = den * (a / g), rl = num / g * b, ru = num / g;
+  if (rn > kI64Max || rd > kI64Max || rl > kI64Max) return MOE_ERR_INVALID_ARG;
+  m->rho_num = (int64_t)rn;
+  m->rho_den = (int64_t)rd;
+  m->rho_last = (int64_t)rl;
+  m->rho_unit = (int64_t)ru;
+  m->a = (int64_t)a;
+  m->b = (int64_t)b;
   return MOE_OK;
 }
 
@@ -157,7 +189,14 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
   if (C == 0) {
     const int64_t P0 = (int64_t)p->occ_comp * p->num_cus;
     const i128 A = (i128)cdiv64((int64_t)m.L * m.W_comp, P0) * m.rho_den;
-    const i128 F = A + (i128)m.rho_num * cdiv64((int64_t)m.L * m.W_comm, P0);
+    // every task in units of rho/a: a for the other splits' tasks, b for the
+    // last split's (a = b = 1 gives rho ceil(L W_comm / P0))
+    const i128 units = (i128)m.a * (m.L - 1) * m.W_comm + (i128)m.b * m.W_last;
+    if (units > kI64Max) {
+      *status = MOE_ERR_INVALID_ARG;
+      return false;
+    }
+    const i128 F = A + (i128)m.rho_unit * cdiv64((int64_t)units, P0);
     if (F > kI64Max) {
       *status = MOE_ERR_INVALID_ARG;
       return false;
@@ -202,14 +241,16 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
   } else {
     // 64-bit with overflow checks: F_s >= A_s and F_s >= q, so any term
     // that overflows makes T(C) overflow too, the same error either way
-    int64_t q, q_drain, F64 = 0;
+    // q for the splits before the last, q_last for the last (its own task
+    // size; with drain = 1 served by all C + P slots)
+    int64_t q, q_last, F64 = 0;
     bool ovf = __builtin_mul_overflow(m.rho_num, cdiv64(m.W_comm, C), &q);
-    q_drain = q;
-    if (m.drain) ovf |= __builtin_mul_overflow(m.rho_num, cdiv64(m.W_comm, (int64_t)C + P), &q_drain);
+    ovf |= __builtin_mul_overflow(m.rho_last, cdiv64(m.W_last, m.drain ? (int64_t)C + P : C),
+                                  &q_last);
     for (int s = 0; s < m.L && !ovf; ++s) {
       int64_t A;
       ovf |= __builtin_mul_overflow(cdiv64((int64_t)(s + 1) * m.W_comp, P), m.rho_den, &A);
-      ovf |= __builtin_add_overflow(A > F64 ? A : F64, m.drain && s == m.L - 1 ? q_drain : q, &F64);
+      ovf |= __builtin_add_overflow(A > F64 ? A : F64, s == m.L - 1 ? q_last : q, &F64);
       if (A_rec) A_rec[s] = A;
       if (F_rec) F_rec[s] = F64;
     }
@@ -370,4 +411,4 @@ extern "C" const char* moe_strerror(int status) {
   }
 }
 
-extern "C" int moe_gemm2_abi_version(void) { return 106; }
+extern "C" int moe_gemm2_abi_version(void) { return 107; }

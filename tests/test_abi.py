@@ -1,6 +1,7 @@
 """The C ABI on the CPU: exports, the selector (bit-exact against the Python
 oracle) and host-side validation.  Nothing here launches GPU work."""
 import ctypes
+import math
 import os
 import random
 import re
@@ -28,7 +29,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(B.EXPORTED)
-    assert L.moe_gemm2_abi_version() == 106
+    assert L.moe_gemm2_abi_version() == 107
 
 
 def _params(**kw):
@@ -36,7 +37,7 @@ def _params(**kw):
                        occ_comp=1, occ_comm=1, num_cus=256, c_min=1, c_max=64, groups=1,
                        rho_ref_num=4, rho_ref_den=3, k_ref=704, tile_m_ref=256,
                        tile_n_ref=256, d_ref=1, rho_kh=0, topk_ref=6, comm_tile_n_ref=1024,
-                       readiness=0)
+                       readiness=0, comm_tile_m_last=0)
     for k, v in kw.items():
         setattr(p, k, v)
     return p
@@ -50,7 +51,17 @@ def _oracle_params(p):
         rho_ref=Fraction(p.rho_ref_num, p.rho_ref_den), k_ref=p.k_ref,
         tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups,
         split_axis=p.split_axis, drain=bool(p.drain), rho_kh=bool(p.rho_kh),
-        topk_ref=p.topk_ref, comm_tile_n_ref=p.comm_tile_n_ref, readiness=p.readiness)
+        topk_ref=p.topk_ref, comm_tile_n_ref=p.comm_tile_n_ref, readiness=p.readiness,
+        comm_tile_m_last=p.comm_tile_m_last)
+
+
+def _time_den(p, rho):
+    """The library's time unit: rho's denominator, times a / gcd(rho's
+    numerator, a) when the last split's tasks are cut finer
+    (a : b = comm_tile_m : comm_tile_m_last in lowest terms)."""
+    tm_last = p.comm_tile_m_last or p.comm_tile_m
+    a = p.comm_tile_m // math.gcd(p.comm_tile_m, tm_last)
+    return rho.denominator * a // math.gcd(rho.numerator, a)
 
 
 def test_hand_example_through_the_abi():
@@ -100,6 +111,33 @@ def test_rho_kh_hand_example_through_the_abi():
         assert B.select_partition(wl, q)[0] == B.MOE_ERR_INVALID_ARG, bad
 
 
+def test_finer_last_split_hand_example_through_the_abi():
+    """The hand example with the last split's tasks cut to 2 tokens
+    (W_last = 15, rho_last = 3/5): T(5) = 39/5, T(2) = 113/10 and the role
+    switch T(0) = 39/10, over the time unit 1/(2 * 5 / gcd(3, 5)) = 1/10."""
+    p = _params(tile_m=1, tile_n=1, comm_tile_m=5, comm_tile_n=1, occ_comp=2,
+                occ_comm=1, num_cus=10, c_min=0, c_max=6, rho_ref_num=3, rho_ref_den=2,
+                k_ref=8, tile_m_ref=1, tile_n_ref=1, comm_tile_m_last=2)
+    wl, keep = B.make_workload(30, 2, 8, 1, 1, 2, [30])
+    n, table, den = B.select_evaluate(wl, p)
+    assert den == 10
+    assert Fraction(table[0], den) == Fraction(39, 10)
+    assert Fraction(table[2], den) == Fraction(113, 10)
+    assert Fraction(table[5], den) == Fraction(39, 5)
+    r, part = B.select_partition(wl, p)
+    assert r == 0 and part.W_comm == 6 and part.T_den == 10
+    r, num, rden, A, F = B.select_candidate(wl, p, 5)
+    assert (num, rden) == (15, 10) and A == [30, 60] and F == [60, 78]
+    # defined for column splits ready a split at a time only; negative is invalid
+    for bad in (dict(split_axis=1), dict(readiness=1), dict(comm_tile_m_last=-1)):
+        q = _params(tile_m=1, tile_n=1, comm_tile_m=5, comm_tile_n=1, occ_comp=2,
+                    occ_comm=1, num_cus=10, c_min=0, c_max=6, rho_ref_num=3, rho_ref_den=2,
+                    k_ref=8, tile_m_ref=1, tile_n_ref=1, comm_tile_m_last=2)
+        for k, v in bad.items():
+            setattr(q, k, v)
+        assert B.select_partition(wl, q)[0] == B.MOE_ERR_INVALID_ARG, bad
+
+
 def _random_case(rnd):
     E = rnd.randint(1, 64)
     topk = rnd.randint(1, min(E, 8))
@@ -130,6 +168,8 @@ def _random_case(rnd):
         tiles = L * osel.compute_work(m_tiles, H, L, p.tile_n, p.groups)
         if tiles <= 2000:
             p.readiness = rnd.choice([0, 1, 1])
+        if p.readiness == 0:
+            p.comm_tile_m_last = rnd.choice([0, 0, p.comm_tile_m // 2, 16, 48, p.comm_tile_m])
     D = rnd.choice([1, 1, 2, 4])
     return T, H, I, E, topk, L, counts, p, D
 
@@ -149,7 +189,7 @@ def test_selector_bit_exact_against_oracle():
         assert r == best.C
         assert (part.C, part.R, part.P, part.delta_comp) == (best.C, best.R, best.P, best.delta)
         assert (part.W_comp, part.W_comm) == (W_comp, W_comm)
-        assert part.T_den == rho.denominator
+        assert part.T_den == _time_den(p, rho)
         assert Fraction(part.T_num, part.T_den) == best.T
         # whole table
         n, table, den = B.select_evaluate(wl, p)
@@ -183,7 +223,7 @@ def test_candidate_internals_bit_exact_against_oracle():
             assert r == B.MOE_ERR_NO_LEGAL_PARTITION, (r, C)
             continue
         cand = byC[C]
-        assert Fraction(num, den) == rho and den == rho.denominator
+        assert Fraction(num, den) == rho and den == _time_den(p, rho)
         assert r == len(cand.A) == len(cand.F)
         if p.readiness == 0:
             assert r == (1 if C == 0 else L)
@@ -402,7 +442,9 @@ def test_trace_size_counts_the_adaptive_consumer_tasks(T, H, L, tm):
     wl, _ = B.make_workload(T=T, H=H, I=I, E=E, topk=k, splits=L)
     rows = T * k
     max_tiles = L * -(-(H // L) // 256) * (-(-rows // 256) + E)
-    tasks = L * -(-T // tm) * -(-(H // L) // 1024)
+    tm_last = tm // 2 if tm > 16 else tm     # the last split's tasks are cut finer
+    cb = -(-(H // L) // 1024)
+    tasks = (L - 1) * -(-T // tm) * cb + -(-T // tm_last) * cb
     assert B.trace_size(wl) == 8 * (4 * max_tiles + 4 * max(tasks, max_tiles))
 
 

@@ -28,12 +28,22 @@ def _small(seed=5):
     return custom(T=700, H=512, I=96, E=6, topk=3, L=2, routing=("zipf", 1.0), seed=seed)
 
 
-def test_traced_matches_untraced(gpu_lib):
+def _owner_tasks(w, p):
+    """Owner-write task records of a launch: tasks_per_split for every split
+    but the last, whose tasks hold comm_tile_m_last tokens."""
+    tm, tm_last = p.comm_tile_m, p.comm_tile_m_last or p.comm_tile_m
+    cb = (w.H // w.L + 1023) // 1024
+    return (w.L - 1) * -(-w.T // tm) * cb + -(-w.T // tm_last) * cb
+
+
+@pytest.mark.parametrize("T", [700, 8192])
+def test_traced_matches_untraced(gpu_lib, T):
+    """(T = 8192 has 32-token tasks and a last split of 16-token ones.)"""
     import torch
 
     import gpu_util
     from paper_2609_07536_amd import binding as B
-    w = _small()
+    w = custom(T=T, H=512, I=96, E=6, topk=3, L=2, routing=("zipf", 1.0), seed=5)
     dev = gpu_util.to_device(w)
     for C in (0, 4):
         plain, used, ws = gpu_util.run(w, C=C, dev=dev)
@@ -49,8 +59,9 @@ def test_traced_matches_untraced(gpu_lib):
         t = tr[:4 * n_tiles].reshape(-1, 4)
         assert (t[:, 3] > 0).all(), "every tile publishes"
         assert (np.diff(t, axis=1) >= 0).all(), "tile timestamps ordered"
-        tm = p.comm_tile_m
-        n_tasks = w.L * ((w.T + tm - 1) // tm) * ((w.H // w.L + 1023) // 1024)
+        n_tasks = _owner_tasks(w, p)
+        if T == 8192:
+            assert (p.comm_tile_m, p.comm_tile_m_last) == (32, 16)
         rows = w.x_perm.shape[0]
         max_tiles = w.L * (-(-(w.H // w.L) // 256)) * (-(-rows // 256) + w.E)
         k = tr[4 * max_tiles:4 * max_tiles + 4 * n_tasks].reshape(-1, 4)
@@ -205,8 +216,7 @@ def test_scatter_traced_records_every_tile_task(gpu_lib):
         tr = trace.cpu().numpy().astype(np.int64)
         rows = w.x_perm.shape[0]
         max_tiles = w.L * (-(-(w.H // w.L) // 256)) * (-(-rows // 256) + w.E)
-        tm = B.launch_params(wl).comm_tile_m
-        owner_tasks = w.L * (-(-w.T // tm)) * (-(-(w.H // w.L) // 1024))
+        owner_tasks = _owner_tasks(w, B.launch_params(wl))
         assert len(tr) == 4 * max_tiles + 4 * max(owner_tasks, max_tiles)
         t = tr[:4 * n_tiles].reshape(-1, 4)
         assert (t[:, 3] > 0).all()

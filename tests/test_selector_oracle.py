@@ -310,3 +310,77 @@ def test_per_wave_readiness_releases_every_task_once():
         assert all(b >= a for a, b in zip(c.F, c.F[1:]))
         # served at least as the split-level model's single last split
         assert c.T >= Fraction(c.A[-1])
+
+
+def test_finer_last_split_hand_example():
+    """The hand example's workload (G=10, o_comm=1, o_comp=2, W_comp=30,
+    W_comm=6, L=2, rho=3/2, 30 tokens in tasks of 5) with the last split's
+    tasks cut to 2 tokens: W_last = ceil(30/2) = 15 tasks of
+    rho_last = 3/2 * 2/5 = 3/5, a : b = 5 : 2.  By hand:
+      C=5: P=10, A=(3,6), F_0 = 3 + 3/2 ceil(6/5) = 6,
+           F_1 = max(6, 6) + 3/5 ceil(15/5) = 39/5   (the paper's model: 9);
+      C=2: P=16, A=(2,4), F_0 = 2 + 3/2 ceil(6/2) = 13/2,
+           F_1 = 13/2 + 3/5 ceil(15/2) = 13/2 + 24/5 = 113/10   (the paper's model: 11);
+      C=0: P0=20, A=ceil(60/20)=3, units = 5*1*6 + 2*15 = 60,
+           T = 3 + (3/2)/5 ceil(60/20) = 39/10       (the paper's extension: 9/2).
+    """
+    rho = Fraction(3, 2)
+    last = sel.LastSplit(W=15, rho=Fraction(3, 5), a=5, b=2)
+    c5 = sel.evaluate(5, 30, 6, 2, 10, 1, 2, rho, last=last)
+    assert (c5.P, c5.A, c5.F) == (10, [3, 6], [Fraction(6), Fraction(39, 5)])
+    c2 = sel.evaluate(2, 30, 6, 2, 10, 1, 2, rho, last=last)
+    assert (c2.A, c2.F) == ([2, 4], [Fraction(13, 2), Fraction(113, 10)])
+    c0 = sel.evaluate(0, 30, 6, 2, 10, 1, 2, rho, last=last)
+    assert (c0.P, c0.T) == (20, Fraction(39, 10))
+    # through select(): one expert of 30 rows, 1-row tiles, two 1-column splits
+    p = sel.SelectParams(tile_m=1, tile_n=1, comm_tile_m=5, comm_tile_n=1, occ_comp=2,
+                         occ_comm=1, num_cus=10, c_min=0, c_max=6, rho_ref=Fraction(3, 2),
+                         k_ref=8, tile_m_ref=1, tile_n_ref=1, d_ref=1, comm_tile_m_last=2)
+    best, cands, W_comp, W_comm, r = sel.select(30, 2, 8, 1, 1, 2, [30], p)
+    assert (W_comp, W_comm, r) == (30, 6, rho)
+    byC = {c.C: c.T for c in cands}
+    assert byC[5] == Fraction(39, 5) and byC[2] == Fraction(113, 10) and byC[0] == Fraction(39, 10)
+    assert best.C == 0
+
+
+def test_finer_last_split_reduces_to_the_paper_model():
+    """T_M^last = T_M^comm (or 0) is the model without the extension, for
+    every candidate, with and without drain."""
+    for drain in (False, True):
+        for tm_last in (0, 64):
+            p = sel.SelectParams(tile_m=256, tile_n=256, comm_tile_m=64, comm_tile_n=1024,
+                                 occ_comp=1, occ_comm=1, num_cus=256, c_min=0, c_max=64,
+                                 rho_ref=Fraction(148, 100), k_ref=704, tile_m_ref=256,
+                                 tile_n_ref=256, d_ref=1, drain=drain, comm_tile_m_last=tm_last)
+            counts = [3072 + 97 * (e % 7) for e in range(32)]
+            _, cands, W_comp, W_comm, rho = sel.select(16384, 2048, 704, 32, 6, 2, counts, p)
+            assert sel.last_split(16384, 1, 2048, 2, p, rho) is None
+            for c in cands:
+                ref = sel.evaluate(c.C, W_comp, W_comm, 2, 256, 1, 1, rho, drain)
+                assert c.T == ref.T and c.F == ref.F
+
+
+def test_finer_last_split_service_by_brute_force():
+    """For C >= 1 the last split's service is rho_last times the number of
+    rounds in which C consumers clear W_last tasks, found by simulating the
+    rounds one at a time; the splits before it are unchanged."""
+    rho = Fraction(7, 3)
+    for W_last, C in ((1, 1), (15, 4), (16, 4), (17, 4), (100, 7), (3, 50)):
+        last = sel.LastSplit(W=W_last, rho=rho / 2, a=2, b=1)
+        c = sel.evaluate(C, 40, 9, 3, 64, 1, 1, rho, last=last)
+        ref = sel.evaluate(C, 40, 9, 3, 64, 1, 1, rho)
+        left, rounds = W_last, 0
+        while left > 0:
+            left -= min(C, left)
+            rounds += 1
+        assert c.F[:2] == ref.F[:2]
+        assert c.F[2] - max(Fraction(c.A[2]), c.F[1]) == rho / 2 * rounds
+
+
+def test_finer_last_split_needs_column_splits():
+    p = sel.SelectParams(tile_m=256, tile_n=256, comm_tile_m=64, comm_tile_n=1024, occ_comp=1,
+                         occ_comm=1, num_cus=256, c_min=0, c_max=8, rho_ref=Fraction(1),
+                         k_ref=704, tile_m_ref=256, tile_n_ref=256, d_ref=1,
+                         comm_tile_m_last=32, split_axis=1)
+    with pytest.raises(ValueError):
+        sel.select(4096, 2048, 704, 8, 2, 2, None, p)
