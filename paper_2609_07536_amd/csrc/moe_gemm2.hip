@@ -742,6 +742,26 @@ __device__ __forceinline__ void gather_commit(Smem& sm, const G1Args& a, int t) 
 __device__ __forceinline__ int y_split_pitch(const KArgs& a) { return a.ysplit; }
 __device__ __forceinline__ int y_split_pitch(const G1Args& a) { return a.nsplit; }
 
+// The last index i in [0, n) with pre[i] <= v, for a non-decreasing pre with
+// pre[0] <= v, found by the whole wave: each round tests 64 evenly spaced
+// candidates at once (one LDS read per lane) and keeps the gap after the
+// last one that passes, so E <= 64 experts take one round trip instead of
+// log2(E) dependent ones.  Every lane of the wave must take part.
+__device__ __forceinline__ int wave_last_le(const int* pre, int n, int v) {
+  const int lane = threadIdx.x & 63;
+  int lo = 0, len = n;   // the answer lies in [lo, lo + len); pre[lo] <= v
+  while (len > 64) {
+    const int step = (len + 63) >> 6;
+    const int i = lo + lane * step;
+    const u64 m = __ballot(lane * step < len && pre[i] <= v);
+    const int j = 63 - __builtin_clzll(m);   // lane 0 always passes
+    lo += j * step;
+    len = min(step, len - j * step);
+  }
+  const u64 m = __ballot(lane < len && pre[lo + lane] <= v);
+  return lo + 63 - __builtin_clzll(m);
+}
+
 // Tile g of the global sequence (split-major, then expert, m-tile, n-tile).
 // Every tile count fits in 32 bits (checked on the host for the worst case
 // of overlapping expert ranges).
@@ -752,11 +772,7 @@ __device__ TileInfo decode_tile(const Smem& sm, const Args& a, int W_comp, int g
   const int mt = idx / a.ntps;
   const int nt = idx - mt * a.ntps;
   // expert owning m-tile mt: last e with tile_prefix[e] <= mt
-  int lo = 0, hi = a.E - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (sm.tile_prefix[mid] <= mt) lo = mid; else hi = mid - 1;
-  }
+  const int lo = wave_last_le(sm.tile_prefix, a.E, mt);
   TileInfo ti;
   ti.e = lo;
   ti.r0 = sm.start[lo] + (mt - sm.tile_prefix[lo]) * kBM;
@@ -828,11 +844,8 @@ __device__ TileInfo decode_band_tile(const Smem& sm, const KArgs& a, int g) {
   const int mt = idx / a.ntps;
   const int nt = idx - mt * a.ntps;
   const int* pre = sm.band_pre + b * (a.E + 1);
-  int lo = 0, hi = a.E - 1;
-  while (lo < hi) {   // last expert whose band-b run starts at or before mt
-    const int mid = (lo + hi + 1) >> 1;
-    if (pre[mid] <= mt) lo = mid; else hi = mid - 1;
-  }
+  // last expert whose band-b run starts at or before mt
+  const int lo = wave_last_le(pre, a.E, mt);
   const int n_e = (sm.count[lo] + kBM - 1) / kBM;
   const int i = band_lo(n_e, b, a.L) + (mt - pre[lo]);
   TileInfo ti;
