@@ -57,6 +57,7 @@ constexpr int kMaxSplits = 16;
 constexpr int kMaxBandTab = 2048;       // (E + 1) * L entries of the token-band tables
 constexpr int kMaxTopk = 64;
 constexpr int kMaxGrid = 4096;
+constexpr int kRotMinRounds = 16;   // launches this long rotate their rounds
 
 // Y rows are padded by 128 bytes: with a power-of-two pitch (H = 2048: 4 KB)
 // the rows of a tile fall on few memory channels, which cost ~18% of the
@@ -1664,8 +1665,18 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
   const int total = bands ? sm.band_start[a.L] : W_comp * a.L;
   const int first_split_end = bands ? sm.band_start[1] : W_comp;
   auto split_of = [&](int g) { return bands ? band_of_tile(sm, a, g) : g / W_comp; };
-  // compute workgroup c takes tiles c, c+P, c+2P, ... (XCD-aware: the
-  // workgroups of consecutive c share an XCD, and so do their tiles)
+  // Round k of the sequence is tiles [k P, (k+1) P).  Compute workgroup c
+  // takes tile k P + c of every round (XCD-aware: the workgroups of
+  // consecutive c share an XCD, and so do their tiles).  The ntps workgroups
+  // on the n-tiles of one m-tile share its x rows; with P a multiple of
+  // ntps the same workgroups meet again in every round and request the same
+  // lines at the same moment.  Launches of at least kRotMinRounds rounds
+  // then give workgroup c tile k P + (c + k) mod P, which moves the m-tile
+  // boundaries by one workgroup each round, so the partners change.  (On
+  // shorter launches the fixed partners measured as fast or faster.)
+  const int rounds = (total + a.P - 1) / a.P;
+  const bool rot = rounds >= kRotMinRounds && a.P % a.ntps == 0;
+  auto tile_of = [&](int k) { return k * a.P + (rot ? (c + k) % a.P : c); };
   const int g_first = b >= a.C && c < total ? c : -1;
   // A compute workgroup with a tile in split 0 publishes its share of the
   // inverse map with that split (consumers read it only after a split).
@@ -1696,7 +1707,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
         __hip_atomic_fetch_or(a.status, kStBadRouting, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       return;
     }
-    int split_first = g_first;   // this workgroup's first tile of the current split
+    int split_first = 0;   // round of this workgroup's first tile of the current split
     int base = 0;                // ring slot of the current tile's stage 0
     // Column splits: this workgroup's flag of split s (its compute index c)
     // says that it has published all its tiles of s, or has none there; the
@@ -1713,8 +1724,8 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
     // the inverse-map stores are done before the tile loop (once), so that
     // the compiler has nothing in flight to wait for inside it
     waitcnt_vm<0>();
-    for (int g = g_first; g >= 0;) {
-      const int g_next = g + a.P < total ? g + a.P : -1;
+    for (int g = g_first, k = 0; g >= 0; ++k) {
+      const int g_next = tile_of(k + 1) < total ? tile_of(k + 1) : -1;
       const bool next = g_next >= 0;
       const TileInfo nt = next ? decode(g_next) : cur;
       const u64 t_start = now_100mhz();
@@ -1747,11 +1758,12 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
         if (threadIdx.x == 0) {
           release_agent();
           const uint32_t epoch = flag_epoch(sm);
-          for (int gg = split_first; gg <= g; gg += a.P)
-            __hip_atomic_store(&a.tile_flags[gg], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          for (int kk = split_first; kk <= k; ++kk)
+            __hip_atomic_store(&a.tile_flags[tile_of(kk)], epoch, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
           // this workgroup is done with every split before its next tile's
           if (!bands) flag_splits(next ? g_next / W_comp : a.L);
-          if (defer_inverse && split_first == g_first)   // first publish: also the inverse map
+          if (defer_inverse && split_first == 0)   // first publish: also the inverse map
             __hip_atomic_store(&a.wg_flags[blockIdx.x], epoch, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
         }
@@ -1759,7 +1771,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
         // it would wait for it (and, in order, for the ring loads issued
         // since) at the next tile's start, on every tile
         waitcnt_vm<0>();
-        split_first = g_next;
+        split_first = k + 1;
         if (next && nk >= 2) issue_stage1_a(sm, a, nt, base);
       }
       if (a.trace && threadIdx.x == 0) {

@@ -63,6 +63,25 @@ def test_dedicated_consumers_full_size_bitwise(gpu_lib, name, C):
         _check(got, ref, f"{name} C=64 vs oracle")
 
 
+@pytest.mark.parametrize("mode,C", [(0, 56), (0, 60), (2, 0), (2, 1), (2, 8), (1, 0)])
+def test_rotated_rounds_largest_sweep_shape(gpu_lib, mode, C):
+    """T = 32768 has about 25 compute rounds, so workgroups whose P is a
+    multiple of the n-tiles per m-tile take their tiles rotated by one more
+    each round (C = 0, 56 and 60 with column splits, C = 0 and 8 with token
+    bands; C = 1 with bands and C = 57 keep the plain order).  Owner-write
+    results stay bitwise equal to the oracle-checked C = 0 output; the atomic
+    scatter is checked against the oracle."""
+    import gpu_util
+    w, ref, dev, ws, base = _full("sweep_T32768_uniform")
+    print(f"T=32768 mode={mode} C={C}", flush=True)
+    got, used, _ = gpu_util.run(w, C=C, dev=dev, workspace=ws, mode=mode)
+    assert used == C
+    if mode == 1:
+        _check(got, ref, f"T=32768 scatter C={C}")
+    else:
+        assert np.array_equal(got.view(np.uint32), base.view(np.uint32)), (mode, C)
+
+
 def _mid(seed=21):
     return custom(T=2048, H=1024, I=256, E=16, topk=4, L=2, routing=("zipf", 1.0), seed=seed)
 

@@ -101,6 +101,8 @@ EDGE = [
     ("many_experts", 1000, 256, 64, 200, 8, 2, ("zipf", 0.5)),
     ("topk_16", 200, 128, 32, 20, 16, 1, ("uniform",)),
     ("single_token", 1, 1024, 512, 8, 2, 1, ("uniform",)),
+    # 32-token tasks, the last split's 16-token ones with an 8-token tail block
+    ("ragged_last_split", 8200, 512, 96, 6, 3, 2, ("zipf", 1.0)),
 ]
 
 
