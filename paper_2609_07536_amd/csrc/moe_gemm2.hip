@@ -551,9 +551,14 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // time per stage.)
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void dma16(i32x4 rsrc, uint32_t voff, uint32_t lds_base) {
+  // (the resource is wave-uniform; readfirstlane keeps it in scalar
+  // registers also where the compiler cannot prove that)
+  i32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r[i] = __builtin_amdgcn_readfirstlane(rsrc[i]);
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
-               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc)
+               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(r)
                : "memory", "m0");
 }
 
@@ -1054,9 +1059,12 @@ __device__ __forceinline__ void epilogue_store(Smem& sm, const G1Args& a, f32x16
 // from this tile's last stage boundary (the slot freed there, while this
 // tile's last stage computes) and its stage 1 after this tile's Y stores
 // (the slot of this tile's last stage, which carries the epilogue).
+// tctx: on entry the tile's load addresses when it is `filled` (its caller
+// made them for its ring fill), on return the next tile's.
 template <class Args>
 __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool filled, bool next,
-                             const TileInfo& nt, int base, u64* t_mid, bool defer_stage1 = false) {
+                             const TileInfo& nt, int base, u64* t_mid, TileCtx& tctx,
+                             bool defer_stage1 = false) {
   // The lane's LDS offsets are recomputed for every tile (a few VALU
   // operations) rather than kept across the tile loop.
   const int lane = opaque_tid() & 63;
@@ -1070,7 +1078,8 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
       block_barrier();
     }
   }
-  const TileCtx t = make_ctx(sm, a, ti, wave);
+  if (!filled) tctx = make_ctx(sm, a, ti, wave);
+  const TileCtx t = tctx;
 
   // per-lane LDS element offsets of the MFMA fragments (stage 0, step 0)
   const int wn0 = (wave % kWavesN) * kWN;
@@ -1146,15 +1155,18 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
     boundary_steps(acc, af, bm, a, slot_a(kt + 1), slot_b(kt + 1), offA, offB, t, kt + kStages,
                    slot_of(kt), wave, true);
   }
-  // the last boundary: its freed slot takes the next tile's stage 0
+  // The next tile's load addresses (nt is a valid tile, == ti, without a
+  // next one), made once for its stage 0 and 1 here and kept for it; a
+  // gathering stage makes them after the next tile's rows are staged.
+  // The last boundary: its freed slot takes the next tile's stage 0.
   if (nk >= 2) {
     wait_stage(0);
     if constexpr (RowGather<Args>::on) {
       if (next) gather_commit(sm, a, next_tok);   // this tile's rows are in t already
     }
     block_barrier();
-    const TileCtx tn = make_ctx(sm, a, nt, wave);   // nt is a valid tile (== ti) without a next one
-    boundary_steps(acc, af, bm, a, slot_a(nk - 1), slot_b(nk - 1), offA, offB, tn, 0,
+    tctx = make_ctx(sm, a, nt, wave);
+    boundary_steps(acc, af, bm, a, slot_a(nk - 1), slot_b(nk - 1), offA, offB, tctx, 0,
                    slot_of(nk), wave, next);
   }
   mfma_step(acc, af[(kKS - 1) & 1], bm[(kKS - 1) & 1]);
@@ -1168,7 +1180,8 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
   const int eslot = slot_of(nk - 1);
   // with a single stage there was no boundary: the next tile's stage 0 goes
   // into the other slot now, ahead of the Y stores
-  if (next && nk == 1) issue_stage(a, make_ctx(sm, a, nt, wave), 0, slot_of(nk), wave);
+  if (nk == 1) tctx = make_ctx(sm, a, nt, wave);
+  if (next && nk == 1) issue_stage(a, tctx, 0, slot_of(nk), wave);
 
   // The down-projection's epilogue uses only the x part of the slot, so the
   // W2 half of the next tile's stage 1 loads during it.
@@ -1176,16 +1189,16 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
   // (Also before a split's publish: those loads are older than the Y
   // stores, so the publish's wait for the stores covers them at no cost.)
   const bool stage1_now = next && nk >= 2 && !defer_stage1;
-  if (kEarlyB && next && nk >= 2) issue_stage_b(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
+  if (kEarlyB && next && nk >= 2) issue_stage_b(a, tctx, 1, eslot, wave);
   epilogue_store(sm, a, acc, eslot, lane, wave, wn0, wm0, ti);
   if (stage1_now) {
     // every wave has read its block back (its stores carry the data), so
     // the slot may take the rest of the next tile's stage 1
     block_barrier();
     if (kEarlyB)
-      issue_stage_a(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
+      issue_stage_a(a, tctx, 1, eslot, wave);
     else
-      issue_stage(a, make_ctx(sm, a, nt, wave), 1, eslot, wave);
+      issue_stage(a, tctx, 1, eslot, wave);
   }
   t_mid[1] = now_100mhz();
 }
@@ -1193,9 +1206,9 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
 // The x half of the next tile's stage 1 into its slot, when the tile
 // before deferred it past its split's publish (after every wave has read
 // its epilogue block back); the W2 half went in before the epilogue.
-__device__ __forceinline__ void issue_stage1_a(Smem& sm, const KArgs& a, const TileInfo& nt, int base) {
+__device__ __forceinline__ void issue_stage1_a(const KArgs& a, const TileCtx& tn, int base) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  issue_stage_a(a, make_ctx(sm, a, nt, wave), 1, (base + 1) % kStages, wave);
+  issue_stage_a(a, tn, 1, (base + 1) % kStages, wave);
 }
 
 // ---- consumer role: one task --------------------------------------------------
@@ -1692,11 +1705,13 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
   // A compute workgroup issues its first tile's ring fill before building
   // its share of the inverse map, so those loads fly during its atomics.
   TileInfo cur = {0, 0, 0, 0, 0};
+  TileCtx tctx;   // the load addresses of the tile whose ring stages are in flight
   bool filled = false;
   if (total <= a.max_tiles && g_first >= 0) {
     cur = decode(g_first);
-    issue_prologue(a, make_ctx(sm, a, cur, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)), nk,
-                   0, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    tctx = make_ctx(sm, a, cur, wave);
+    issue_prologue(a, tctx, nk, 0, wave);
     filled = true;
   }
   consumer_prologue(sm, a, rows_dev, !defer_inverse);
@@ -1734,7 +1749,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
       // A split's last tile holds the x half of its next tile's stage 1
       // back until the publish, so that the publish's waits cover nothing
       // issued after the Y stores.
-      compute_tile(sm, a, cur, filled, next, nt, base, t_mid, last_of_split);
+      compute_tile(sm, a, cur, filled, next, nt, base, t_mid, tctx, last_of_split);
       base = (base + nk) % kStages;   // the next tile's stages follow this tile's
       // Publish once per split: consumers wait for whole splits, so the tiles
       // of a split are published together after this workgroup's last tile of
@@ -1772,7 +1787,7 @@ __device__ __forceinline__ void fused_body(Smem& sm, const KArgs& a) {
         // since) at the next tile's start, on every tile
         waitcnt_vm<0>();
         split_first = k + 1;
-        if (next && nk >= 2) issue_stage1_a(sm, a, nt, base);
+        if (next && nk >= 2) issue_stage1_a(a, tctx, base);
       }
       if (a.trace && threadIdx.x == 0) {
         store8(&a.trace[4 * g + 0], t_start);
@@ -1844,13 +1859,14 @@ moe_gemm1_swiglu_kernel(G1Args a) {
   if (c >= total) return;
   const int nk = (a.H + kBK - 1) / kBK;
   bool filled = false;
+  TileCtx tctx;
   int base = 0;
   for (int g = c; g < total; g += P) {
     const bool next = g + P < total;
     const TileInfo cur = decode_tile(sm, a, total, g);
     const TileInfo nt = decode_tile(sm, a, total, next ? g + P : g);
     u64 t_mid[2];
-    compute_tile(sm, a, cur, filled, next, nt, base, t_mid);
+    compute_tile(sm, a, cur, filled, next, nt, base, t_mid, tctx);
     base = (base + nk) % kStages;
     filled = next;
   }
