@@ -700,6 +700,18 @@ __device__ __forceinline__ void mfma_step(f32x16 (&acc)[kNB][kMB], const bf16x8 
       acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[nb], bm[mb], acc[nb][mb], 0, 0, 0);
 }
 
+// The first K=16 step of a tile: every accumulator from zero (an inline
+// zero operand, so no register clearing before it).
+__device__ __forceinline__ void mfma_step_zero(f32x16 (&acc)[kNB][kMB], const bf16x8 (&af)[kNB],
+                                               const bf16x8 (&bm)[kMB]) {
+  const f32x16 z = {};
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < kMB; ++mb)
+      acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[nb], bm[mb], z, 0, 0, 0);
+}
+
 // mfma_step with loads q0 .. q0+kNB-1 of stage kt issued one after each
 // n-block of MFMAs: spread out, the loads never hold the wave's in-order
 // issue long enough to starve the matrix core.
@@ -1106,13 +1118,8 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
     }
   }
 
+  // (the first K=16 step writes every accumulator from zero)
   f32x16 acc[kNB][kMB];
-#pragma unroll
-  for (int i = 0; i < kNB; ++i)
-#pragma unroll
-    for (int j = 0; j < kMB; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   // prologue: fill the ring (unless done during the previous tile's
   // publish), then wait for stage 0 (every wave's share)
@@ -1144,7 +1151,10 @@ __device__ void compute_tile(Smem& sm, const Args& a, const TileInfo& ti, bool f
   for (int ks = 0; ks + 1 < kKS; ++ks) {
     load_frags(slot_a(0), slot_b(0), offA, offB, ks + 1, af[(ks + 1) & 1], bm[(ks + 1) & 1]);
     __builtin_amdgcn_sched_barrier(0);   // keep the next step's reads ahead of these MFMAs
-    mfma_step(acc, af[ks & 1], bm[ks & 1]);
+    if (ks == 0)
+      mfma_step_zero(acc, af[0], bm[0]);
+    else
+      mfma_step(acc, af[ks & 1], bm[ks & 1]);
   }
   static_assert(kLoadsPerOperand % kNB == 0 && kLoadsPerOperand / kNB <= kKS, "load spread");
   static_assert(kStages == 2, "the boundary loop refills one stage ahead");
