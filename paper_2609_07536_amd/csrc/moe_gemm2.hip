@@ -1233,6 +1233,7 @@ struct TaskMeta {
   int n[kCommTM];
   int row[kCommTM * kMaxTopk];
   float gate[kCommTM * kMaxTopk];
+  int unsorted[kCommTM * kMaxTopk];   // the rows in inverse-map order, while they are ranked
 };
 
 static_assert(sizeof(TaskMeta) <= sizeof(Smem::a) + sizeof(Smem::b) &&
@@ -1248,41 +1249,37 @@ __device__ void load_task_meta(Smem& sm, TaskMeta& m, const KArgs& a, u64 cnt_ep
     if (threadIdx.x == 0) sm.task_band = 0;
     __syncthreads();
   }
+  // One thread per (token, slot): the token's count and the slot's inverse-
+  // map entry in one round trip (the entry is in bounds; past the count it
+  // is stale and ignored), then the row's gate in a second.  The rows of a
+  // token are distinct, so each takes the position of its rank among them
+  // (ascending row order), counted over the unsorted copy in LDS.
   for (int i = opaque_tid(); i < ntok * K; i += kThreads) {
     const int t = i / K;
     const int j = i - t * K;
-    // the count and the entry are loaded together (one round trip); an
-    // entry past the count is stale and ignored
-    const uint32_t have = epoch_count(ld_relaxed(&a.tok_cnt[t0 + t]), cnt_epoch);
+    const u64 cv = ld_relaxed(&a.tok_cnt[t0 + t]);
+    const int r = a.inv[(long long)(t0 + t) * K + j];
+    const uint32_t have = epoch_count(cv, cnt_epoch);
     const int n = (int)(have < (uint32_t)K ? have : (uint32_t)K);
-    int r = 0;
-    float g = 0.f;
-    if (j < n) {
-      r = a.inv[(long long)(t0 + t) * K + j];
-      g = a.gate_w[r];
-      if (bands) atomicMax(&sm.task_band, band_of_row(sm, a, r));
-    }
-    m.row[i] = r;
-    m.gate[i] = g;
+    m.unsorted[i] = j < n ? r : 0;
     if (j == 0) m.n[t] = n;
   }
   __syncthreads();
-  // rows of a token are distinct: sort them ascending (one thread per token)
-  for (int t = threadIdx.x; t < ntok; t += kThreads) {
+  for (int i = opaque_tid(); i < ntok * K; i += kThreads) {
+    const int t = i / K;
+    const int j = i - t * K;
     const int n = m.n[t];
-    int* R = &m.row[t * K];
-    float* G = &m.gate[t * K];
-    for (int i = 1; i < n; ++i) {
-      const int r = R[i];
-      const float g = G[i];
-      int q = i - 1;
-      while (q >= 0 && R[q] > r) {
-        R[q + 1] = R[q];
-        G[q + 1] = G[q];
-        --q;
-      }
-      R[q + 1] = r;
-      G[q + 1] = g;
+    if (j < n) {
+      const int r = m.unsorted[i];
+      const float g = a.gate_w[r];
+      int rank = 0;
+      for (int q = 0; q < n; ++q) rank += m.unsorted[t * K + q] < r;
+      m.row[t * K + rank] = r;
+      m.gate[t * K + rank] = g;
+      if (bands) atomicMax(&sm.task_band, band_of_row(sm, a, r));
+    } else {
+      m.row[i] = 0;
+      m.gate[i] = 0.f;
     }
   }
   __syncthreads();
