@@ -91,7 +91,8 @@ typedef struct {
                                         moe_gemm2_combine_ex mode 2) */
   int32_t drain;                     /* 0: the paper's recurrence; 1: compute slots join the
                                         consumers after their tiles (the last split is served
-                                        by all C + P slots) */
+                                        by all C + P slots); 2: they serve whatever remains of
+                                        every split (the work-conserving drain) */
   int32_t rho_kh;                    /* 0: eq:rho-scaling as printed; 1: also scale rho by the
                                         consumer task's bytes relative to the calibration:
                                         (2 topk + 4) / (2 topk_ref + 4) for the Y rows read
@@ -135,6 +136,14 @@ typedef struct {
  *     W_comm = ceil(ceil(ceil(M/D)/T_M^comm) / L) ceil(N/T_N^comm);
  *   drain = 1: the last split's service uses every slot,
  *     F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
+ *   drain = 2 (readiness = 0, comm_tile_m_last = comm_tile_m or 0): every
+ *     slot serves what remains of every split once the compute ends at
+ *     E = A_{L-1}.  Until then the C consumers take the splits in order,
+ *     split s from max(A_s, the end of split s-1), in rounds of C tasks of
+ *     rho each: they complete min(W_comm, C floor((E - start)/rho)) tasks of
+ *     it, stopping at the first split they cannot finish; with R the tasks
+ *     left of all L W_comm, T(C) = E + rho ceil(R / (C + P)).  F_s is the
+ *     end of split s where the consumers finished it before E, else T(C);
  *   readiness = 1 (column splits only): the consumer work is released
  *     a compute wave at a time instead of a split at a time.  The L W_comp
  *     tiles complete in V = ceil(L W_comp / P) waves, wave v (1-based) the
@@ -219,7 +228,7 @@ int moe_gemm2_default_params(int device, moe_select_params_t* out);
  * (MOE_GEMM2_RHO_REF_SCATTER="num/den" overrides it) and readiness = 1 (a
  * scatter task waits only for the published prefix of the tile sequence up
  * to its own tile); mode 2 (token bands)
- * sets split_axis = 1, drain = 1 and rho_ref to that mode's calibration
+ * sets split_axis = 1, drain = 2 and rho_ref to that mode's calibration
  * (MOE_GEMM2_RHO_REF_BANDS overrides it).  Modes 0 and 1 leave split_axis
  * and drain 0.  Every mode sets topk_ref = 6 and comm_tile_n_ref = 1024 (the
  * calibration's) and rho_kh = 0; modes 0 and 2 set rho_kh = 1 when the
@@ -239,7 +248,7 @@ int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk, moe_sele
  * as moe_gemm2_default_params_ex(device, 1, wl->topk).  Mode 2: tasks of
  * TM tokens x min(1024, H) columns of the full width, TM = 64 halved down
  * to 16 while there would be fewer than 512 (ceil(T/TM) ceil(H/1024)),
- * rho_ref scaled by TM/64, split_axis = 1, drain = 1.  Returns 0,
+ * rho_ref scaled by TM/64, split_axis = 1, drain = 2.  Returns 0,
  * MOE_ERR_INVALID_ARG (null pointer, mode other than 0, 1 or 2, invalid
  * workload), MOE_ERR_UNSUPPORTED (shape outside moe_gemm2_combine_ex's
  * range for that mode) or MOE_ERR_HIP. */

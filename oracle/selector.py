@@ -39,9 +39,18 @@ special case split_axis = 0, drain = False, one given L):
     the full width and 1/L of the token blocks:
     W_comp = ceil(g m_tiles / L) ceil(N / T_N),
     W_comm = ceil(ceil(ceil(M/D) / T_M^comm) / L) ceil(N / T_N^comm);
-  * drain: compute slots join the consumers after their last tile, so the
-    last split is served by all C + P slots:
+  * drain (1): compute slots join the consumers after their last tile, so
+    the last split is served by all C + P slots:
     F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
+  * work-conserving drain (2; readiness 0, no finer last split): the compute
+    slots serve whatever remains of every split once the compute ends at
+    E = A_{L-1}.  Until then the C consumers take the splits in order,
+    split s from start = max(A_s, the end of split s-1), in rounds of C
+    tasks of rho each; the rounds that start before E claim
+    min(W_comm, C ceil((E - start)/rho)) tasks of split s, stopping at the
+    first split not wholly claimed.  With R the tasks left of all L W_comm
+    and e the end of the consumers' last claimed round,
+    T(C) = max(E + rho ceil(R / (C + P)), e);
   * L as a decision variable: the (L, C) pair with the least T(C) over a
     range of L, ties to the smaller L;
   * readiness = 1 (column splits): the consumer work is released a compute
@@ -148,7 +157,7 @@ class LastSplit:
 
 
 def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
-             o_comp: int, rho: Fraction, drain: bool = False,
+             o_comp: int, rho: Fraction, drain: int = 0,
              readiness: int = 0, last: Optional[LastSplit] = None) -> Optional[Candidate]:
     """The recurrence for one candidate C; None if P(C) <= 0 (illegal)."""
     if C == 0:
@@ -173,6 +182,8 @@ def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
     if readiness == 1:
         return _per_wave(C, R, P, W_comp, W_comm, L, rho, drain, V_comm, q, V_comp)
     A = [cdiv((s + 1) * W_comp, P) for s in range(L)]
+    if drain == 2:
+        return _work_conserving(C, R, P, A, W_comm, L, rho, V_comm, q, V_comp, W_comp)
     F: List[Fraction] = []
     prev = Fraction(0)
     W_l, rho_l = (W_comm, Fraction(rho)) if last is None else (last.W, last.rho)
@@ -185,6 +196,36 @@ def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
             prev = max(Fraction(A[s]), prev) + q
         F.append(prev)
     return Candidate(C=C, R=R, P=P, A=A, V_comm=V_comm, q=q, F=F, T=F[-1],
+                     V_comp=V_comp, delta=V_comp * P - W_comp)
+
+
+def _work_conserving(C, R, P, A, W_comm, L, rho, V_comm, q, V_comp, W_comp) -> Candidate:
+    """The drain = 2 model: the consumers' claims until the compute ends,
+    then every slot on what remains."""
+    rho = Fraction(rho)
+    end = Fraction(A[L - 1])
+    cur = Fraction(A[0])
+    claimed = 0
+    last_end = Fraction(0)
+    F: List[Fraction] = []
+    for s in range(L - 1):
+        start = max(Fraction(A[s]), cur)
+        need = cdiv(W_comm, C)
+        started = math.ceil((end - start) / rho) if start < end else 0   # rounds begun before E
+        if started >= need:
+            claimed += W_comm
+            cur = start + need * rho
+            if need > 0:
+                last_end = cur
+            F.append(cur)
+        else:
+            claimed += C * started
+            if started > 0:
+                last_end = start + started * rho
+            break
+    T = max(end + rho * cdiv(L * W_comm - claimed, C + P), last_end)
+    F += [T] * (L - len(F))
+    return Candidate(C=C, R=R, P=P, A=A, V_comm=V_comm, q=q, F=F, T=T,
                      V_comp=V_comp, delta=V_comp * P - W_comp)
 
 
@@ -216,7 +257,7 @@ def _per_wave(C, R, P, W_comp, W_comm, L, rho, drain, V_comm, q, V_comp) -> Cand
 
 def select_from_work(W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
                      o_comp: int, rho: Fraction, c_min: int, c_max: int,
-                     drain: bool = False, readiness: int = 0,
+                     drain: int = 0, readiness: int = 0,
                      last: Optional[LastSplit] = None):
     """Argmin of T(C) over the legal C, then smallest Delta, then smallest C.
 
@@ -250,7 +291,7 @@ class SelectParams:
     d_ref: int
     groups: int = 1
     split_axis: int = 0
-    drain: bool = False
+    drain: int = 0                 # 0, 1 or 2 (see the module notes)
     rho_kh: bool = False
     topk_ref: int = 6
     comm_tile_n_ref: int = 1024
@@ -272,7 +313,7 @@ def select(T: int, H: int, I: int, E: int, topk: int, L: int,
                                  p.comm_tile_n_ref)
     last = last_split(T, D, H, L, p, rho)
     best, cands = select_from_work(W_comp, W_comm, L, p.num_cus, p.occ_comm,
-                                   p.occ_comp, rho, p.c_min, p.c_max, bool(p.drain),
+                                   p.occ_comp, rho, p.c_min, p.c_max, int(p.drain),
                                    p.readiness, last)
     return best, cands, W_comp, W_comm, rho
 
@@ -284,7 +325,7 @@ def last_split(T: int, D: int, H: int, L: int, p: SelectParams,
     tm, tm_last = p.comm_tile_m, p.comm_tile_m_last or p.comm_tile_m
     if tm_last == tm:
         return None
-    if p.split_axis != 0 or p.readiness != 0:
+    if p.split_axis != 0 or p.readiness != 0 or int(p.drain) == 2:
         raise ValueError("a finer last split is defined for column splits ready a split at a time")
     g = math.gcd(tm, tm_last)
     return LastSplit(W=comm_work(T, D, H, L, tm_last, p.comm_tile_n),

@@ -2070,7 +2070,9 @@ void fill_params(const DevInfo& d, int mode, int topk, int comm_tm, moe_select_p
   p->rho_ref_num = mode == 1 ? kRhoScatterNum : mode == 2 ? kRhoBandsNum : kRhoRefNum;
   p->rho_ref_den = mode == 1 ? kRhoScatterDen : mode == 2 ? kRhoBandsDen : kRhoRefDen;
   p->split_axis = mode == 2 ? 1 : 0;
-  p->drain = mode == 2 ? 1 : 0;
+  // token bands: the compute workgroups drain into every band's remaining
+  // tasks (the work-conserving drain)
+  p->drain = mode == 2 ? 2 : 0;
   // a scatter task needs only its own tile and waits for the published
   // prefix up to it: its work is released a compute wave at a time
   p->readiness = mode == 1 ? 1 : 0;

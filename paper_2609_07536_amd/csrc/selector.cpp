@@ -29,6 +29,15 @@
 //   drain = 1: the compute slots join the consumers after their last tile,
 //     so the last split is served by all C + P slots:
 //       F_{L-1} = max(A_{L-1}, F_{L-2}) + rho ceil(W_comm / (C + P));
+//   drain = 2 (readiness 0, no finer last split): the same, but the compute
+//     slots serve whatever remains of every split: the C consumers take the
+//     splits in order, split s from start_s = max(A_s, the end of split
+//     s-1), in rounds of C tasks of rho each; the rounds that start before
+//     the compute ends at E = A_{L-1} claim
+//       min(W_comm, C ceil((E - start_s) / rho)) tasks of split s,
+//     stopping at the first split not wholly claimed; with R the tasks left
+//     (of all L W_comm) and e the end of the consumers' last claimed round,
+//       T(C) = max(E + rho ceil(R / (C + P)), e);
 //   readiness = 1 (column splits): consumer work is released a compute wave
 //     at a time: of V = ceil(L W_comp / P) waves, wave v releases the tasks
 //     of the tiles it completes, w_v = ceil(t_v L W_comm / (L W_comp)) -
@@ -122,13 +131,14 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
     m_tiles = (int64_t)wl->E * cdiv64(cdiv64(total, wl->E), p->tile_m);
   }
   if (p->split_axis != 0 && p->split_axis != 1) return MOE_ERR_INVALID_ARG;
-  if (p->drain != 0 && p->drain != 1) return MOE_ERR_INVALID_ARG;
+  if (p->drain < 0 || p->drain > 2) return MOE_ERR_INVALID_ARG;
+  if (p->drain == 2 && p->readiness != 0) return MOE_ERR_INVALID_ARG;
   if (p->readiness != 0 && p->readiness != 1) return MOE_ERR_INVALID_ARG;
   if (p->readiness == 1 && p->split_axis != 0) return MOE_ERR_INVALID_ARG;
   const int64_t token_blocks = cdiv64(cdiv64(wl->T, wl->ranks), p->comm_tile_m);
   if (p->comm_tile_m_last < 0) return MOE_ERR_INVALID_ARG;
   const int64_t tm_last = p->comm_tile_m_last > 0 ? p->comm_tile_m_last : p->comm_tile_m;
-  if (tm_last != p->comm_tile_m && (p->split_axis != 0 || p->readiness != 0))
+  if (tm_last != p->comm_tile_m && (p->split_axis != 0 || p->readiness != 0 || p->drain == 2))
     return MOE_ERR_INVALID_ARG;   // defined for column splits ready a split at a time
   if (p->split_axis == 0) {
     const int64_t n_split = cdiv64(wl->H, wl->splits);
@@ -237,6 +247,44 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
         if (A_rec) A_rec[v - 1] = (int64_t)A;
         if (F_rec) F_rec[v - 1] = (int64_t)F;
       }
+    }
+  } else if (m.drain == 2) {
+    // work-conserving drain: the dedicated consumers' claims until the
+    // compute ends, then every slot on what remains (exact, in 128 bits)
+    const i128 E = (i128)cdiv64((int64_t)m.L * m.W_comp, P) * m.rho_den;
+    i128 cur = (i128)cdiv64(m.W_comp, P) * m.rho_den;   // A_0
+    i128 last_end = 0;      // end of the consumers' last claimed round
+    int64_t claimed = 0;
+    int s_stop = m.L - 1;   // first split the consumers do not wholly claim
+    for (int s = 0; s + 1 < m.L; ++s) {
+      const i128 A = (i128)cdiv64((int64_t)(s + 1) * m.W_comp, P) * m.rho_den;
+      if (A_rec) A_rec[s] = (int64_t)A;
+      const i128 start = A > cur ? A : cur;
+      const int64_t need = cdiv64(m.W_comm, C);
+      // rounds that start before E
+      const i128 started = start < E ? (E - start + m.rho_num - 1) / m.rho_num : 0;
+      if (started >= need) {
+        claimed += m.W_comm;
+        cur = start + (i128)need * m.rho_num;
+        if (need > 0) last_end = cur;
+        if (F_rec) F_rec[s] = (int64_t)cur;
+      } else {
+        claimed += (int64_t)((i128)C * started);
+        if (started > 0) last_end = start + started * m.rho_num;
+        s_stop = s;
+        break;
+      }
+    }
+    const int64_t R = (int64_t)((i128)m.L * m.W_comm - claimed);
+    F = E + (i128)m.rho_num * cdiv64(R, (int64_t)C + P);
+    if (last_end > F) F = last_end;
+    if (F > kI64Max) {
+      *status = MOE_ERR_INVALID_ARG;
+      return false;
+    }
+    for (int s = s_stop; s < m.L; ++s) {   // splits finished in the drain end with it
+      if (A_rec) A_rec[s] = (int64_t)((i128)cdiv64((int64_t)(s + 1) * m.W_comp, P) * m.rho_den);
+      if (F_rec) F_rec[s] = (int64_t)F;
     }
   } else {
     // 64-bit with overflow checks: F_s >= A_s and F_s >= q, so any term

@@ -50,7 +50,7 @@ def _oracle_params(p):
         num_cus=p.num_cus, c_min=p.c_min, c_max=p.c_max,
         rho_ref=Fraction(p.rho_ref_num, p.rho_ref_den), k_ref=p.k_ref,
         tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups,
-        split_axis=p.split_axis, drain=bool(p.drain), rho_kh=bool(p.rho_kh),
+        split_axis=p.split_axis, drain=int(p.drain), rho_kh=bool(p.rho_kh),
         topk_ref=p.topk_ref, comm_tile_n_ref=p.comm_tile_n_ref, readiness=p.readiness,
         comm_tile_m_last=p.comm_tile_m_last)
 
@@ -138,6 +138,30 @@ def test_finer_last_split_hand_example_through_the_abi():
         assert B.select_partition(wl, q)[0] == B.MOE_ERR_INVALID_ARG, bad
 
 
+def test_work_conserving_drain_hand_example_through_the_abi():
+    """The hand example with drain = 2: T(1) = T(2) = 11/2, T(5) = 15/2
+    (drain = 1: 25/2, 8, 15/2); the split times of C = 5 are (3, 6) and
+    (6, 15/2).  drain = 2 with per-wave readiness or a finer last split is
+    refused."""
+    p = _params(tile_m=1, tile_n=1, comm_tile_m=5, comm_tile_n=1, occ_comp=2,
+                occ_comm=1, num_cus=10, c_min=1, c_max=6, rho_ref_num=3, rho_ref_den=2,
+                k_ref=8, tile_m_ref=1, tile_n_ref=1, drain=2)
+    wl, keep = B.make_workload(30, 2, 8, 1, 1, 2, [30])
+    n, table, den = B.select_evaluate(wl, p)
+    assert den == 2
+    assert [Fraction(t, den) for t in (table[0], table[1], table[4])] == \
+        [Fraction(11, 2), Fraction(11, 2), Fraction(15, 2)]
+    r, num, rden, A, F = B.select_candidate(wl, p, 5)
+    assert (num, rden) == (3, 2) and A == [6, 12] and F == [12, 15]
+    for bad in (dict(readiness=1), dict(comm_tile_m_last=2), dict(drain=3)):
+        q = _params(tile_m=1, tile_n=1, comm_tile_m=5, comm_tile_n=1, occ_comp=2,
+                    occ_comm=1, num_cus=10, c_min=1, c_max=6, rho_ref_num=3, rho_ref_den=2,
+                    k_ref=8, tile_m_ref=1, tile_n_ref=1, drain=2)
+        for k, v in bad.items():
+            setattr(q, k, v)
+        assert B.select_partition(wl, q)[0] == B.MOE_ERR_INVALID_ARG, bad
+
+
 def _random_case(rnd):
     E = rnd.randint(1, 64)
     topk = rnd.randint(1, min(E, 8))
@@ -159,16 +183,16 @@ def _random_case(rnd):
                 rho_ref_den=rnd.randint(1, 10000), k_ref=rnd.choice([352, 704, 1408]),
                 tile_m_ref=rnd.choice([128, 256]), tile_n_ref=rnd.choice([128, 256]),
                 d_ref=rnd.choice([1, 4]), split_axis=rnd.choice([0, 0, 1]),
-                drain=rnd.choice([0, 0, 1]), rho_kh=rnd.choice([0, 0, 1]),
+                drain=rnd.choice([0, 0, 1, 2]), rho_kh=rnd.choice([0, 0, 1]),
                 topk_ref=rnd.randint(1, 16), comm_tile_n_ref=rnd.choice([256, 512, 1024, 2048]))
     if p.split_axis == 0:
         # per-wave readiness walks every compute wave in the oracle: keep it to
         # workloads of at most 2000 tiles so the suite stays fast
         m_tiles = osel.routed_m_tiles(counts, p.tile_m, E, T * topk)
         tiles = L * osel.compute_work(m_tiles, H, L, p.tile_n, p.groups)
-        if tiles <= 2000:
+        if tiles <= 2000 and p.drain != 2:
             p.readiness = rnd.choice([0, 1, 1])
-        if p.readiness == 0:
+        if p.readiness == 0 and p.drain != 2:
             p.comm_tile_m_last = rnd.choice([0, 0, p.comm_tile_m // 2, 16, 48, p.comm_tile_m])
     D = rnd.choice([1, 1, 2, 4])
     return T, H, I, E, topk, L, counts, p, D
@@ -309,8 +333,8 @@ def test_split_selection_bit_exact_against_oracle():
     wl, keep = B.make_workload(100, 256, 64, 4, 2, 1, [50, 50, 50, 50])
     assert B.select_partition_splits(wl, _params(), 0, 3)[0] == B.MOE_ERR_INVALID_ARG
     assert B.select_partition_splits(wl, _params(), 3, 2)[0] == B.MOE_ERR_INVALID_ARG
-    for field in ("split_axis", "drain", "readiness"):
-        assert B.select_partition(wl, _params(**{field: 2}))[0] == B.MOE_ERR_INVALID_ARG
+    for field, bad in (("split_axis", 2), ("drain", 3), ("drain", -1), ("readiness", 2)):
+        assert B.select_partition(wl, _params(**{field: bad}))[0] == B.MOE_ERR_INVALID_ARG
     # per-wave readiness is defined for column splits only
     assert B.select_partition(wl, _params(split_axis=1, readiness=1))[0] == \
         B.MOE_ERR_INVALID_ARG

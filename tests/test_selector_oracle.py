@@ -384,3 +384,69 @@ def test_finer_last_split_needs_column_splits():
                          comm_tile_m_last=32, split_axis=1)
     with pytest.raises(ValueError):
         sel.select(4096, 2048, 704, 8, 2, 2, None, p)
+
+
+def test_work_conserving_drain_hand_example():
+    """The hand example's workload (G=10, o_comm=1, o_comp=2, W_comp=30,
+    W_comm=6, L=2, rho=3/2) with drain = 2, worked by hand:
+      C=1: P=18, A=(2,4), E=4; split 0 from 2 needs 6 rounds, 2 begin before
+           E (at 2 and 3.5): 2 tasks claimed, the last round ends at 5;
+           R = 10, T = max(4 + 1.5 ceil(10/19), 5) = 11/2
+           (drain = 1: F_0 = 2 + 9 = 11, T = 11 + 1.5 = 25/2);
+      C=2: P=16, A=(2,4); 3 rounds needed, 2 begin before E: 4 claimed, the
+           last ends at 5; R = 8, T = max(4 + 1.5 ceil(8/18), 5) = 11/2
+           (drain = 1: 8);
+      C=5: P=10, A=(3,6), E=6; 2 rounds needed, both begin before E: split 0
+           ends at 6, R = 6, T = max(6 + 1.5 ceil(6/15), 6) = 15/2
+           (= drain 1's 15/2).
+    """
+    rho = Fraction(3, 2)
+    want = {1: ([2, 4], [Fraction(11, 2), Fraction(11, 2)], Fraction(11, 2)),
+            2: ([2, 4], [Fraction(11, 2), Fraction(11, 2)], Fraction(11, 2)),
+            5: ([3, 6], [Fraction(6), Fraction(15, 2)], Fraction(15, 2))}
+    for C, (A, F, T) in want.items():
+        c = sel.evaluate(C, 30, 6, 2, 10, 1, 2, rho, drain=2)
+        assert (c.A, c.F, c.T) == (A, F, T), C
+    assert sel.evaluate(1, 30, 6, 2, 10, 1, 2, rho, drain=1).T == Fraction(25, 2)
+    assert sel.evaluate(2, 30, 6, 2, 10, 1, 2, rho, drain=1).T == 8
+    assert sel.evaluate(5, 30, 6, 2, 10, 1, 2, rho, drain=1).T == Fraction(15, 2)
+
+
+def test_work_conserving_drain_properties():
+    """drain = 2 never predicts a later end than drain = 1 (the compute slots
+    only add service), equals it where the consumers finish every split but
+    the last by the time the compute ends (and for L = 1), and matches a
+    direct simulation of the consumers' rounds."""
+    import random
+    rnd = random.Random(7)
+    n_equal = 0
+    for _ in range(400):
+        W_comp, W_comm = rnd.randint(0, 600), rnd.randint(0, 300)
+        L, G, o = rnd.randint(1, 5), rnd.randint(2, 40), rnd.randint(1, 2)
+        rho = Fraction(rnd.randint(1, 50), rnd.randint(1, 20))
+        for C in range(1, min(12, G)):
+            c2 = sel.evaluate(C, W_comp, W_comm, L, G, 1, o, rho, drain=2)
+            if c2 is None:
+                continue
+            c1 = sel.evaluate(C, W_comp, W_comm, L, G, 1, o, rho, drain=1)
+            assert c2.T <= c1.T
+            if L == 1 or c1.F[L - 2] <= c1.A[L - 1]:
+                assert c2.T == c1.T
+                n_equal += 1
+            # the consumers' rounds one at a time: a round that begins before
+            # E claims up to C tasks of the current split
+            E, t, claimed, last = Fraction(c2.A[L - 1]), None, 0, Fraction(0)
+            for s in range(L - 1):
+                t = Fraction(c2.A[s]) if t is None else max(Fraction(c2.A[s]), t)
+                left = W_comm
+                while left > 0 and t < E:
+                    k = min(C, left)
+                    left -= k
+                    claimed += k
+                    t += rho
+                    last = t
+                if left > 0:
+                    break
+            want = max(E + rho * sel.cdiv(L * W_comm - claimed, C + c2.P), last)
+            assert c2.T == want
+    assert n_equal > 100
