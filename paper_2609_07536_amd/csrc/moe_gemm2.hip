@@ -2031,17 +2031,17 @@ int device_info(int dev, DevInfo* out) {
 // compute-tile time (one consumer wave over one compute wave), measured with
 // the traced entry point at the reference configuration (T=16384, H=2048,
 // I=704, E=32, top-6, L=2, C=32, 64-token tasks; the last split's 32-token
-// tasks counted at twice their time): 30.5 us / 19.7 us = 1.54 (three runs:
-// 1.540 to 1.547).  MOE_GEMM2_RHO_REF="num/den" overrides it.
-constexpr int64_t kRhoRefNum = 154;
+// tasks counted at twice their time): 27.9 us / 19.4 us = 1.44 (three runs:
+// 1.436 to 1.445).  MOE_GEMM2_RHO_REF="num/den" overrides it.
+constexpr int64_t kRhoRefNum = 144;
 constexpr int64_t kRhoRefDen = 100;
 // The same ratio for the atomic scatter (one task = one compute tile's
-// rows), measured the same way: 26.2 us / 21.8 us = 1.20.
-constexpr int64_t kRhoScatterNum = 120;
+// rows), measured the same way: 26.2 us / 21.5 us = 1.22.
+constexpr int64_t kRhoScatterNum = 122;
 constexpr int64_t kRhoScatterDen = 100;
 // The same for token bands (mode 2), 64-token tasks over 1024 columns:
-// 35.1 us / 20.9 us = 1.68.
-constexpr int64_t kRhoBandsNum = 168;
+// 36.7 us / 20.3 us = 1.81.
+constexpr int64_t kRhoBandsNum = 181;
 constexpr int64_t kRhoBandsDen = 100;
 constexpr int kDefaultFixedC = 8;
 
