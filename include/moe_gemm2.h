@@ -106,6 +106,11 @@ typedef struct {
   int32_t comm_tile_m_last;          /* tokens of the last split's consumer tasks (T_M^last);
                                         0 or comm_tile_m: as the other splits' (the paper).
                                         Column splits with readiness = 0 only */
+  int64_t split_cost_num, split_cost_den; /* pi_ref >= 0: compute waves (at the reference K and
+                                        tile, scaled as rho's first two factors) by which each
+                                        split's publish delays the compute of the splits
+                                        after it; split_cost_num = 0: none (the paper).
+                                        readiness = 0 only */
 } moe_select_params_t;
 
 /* The chosen partition.  T(C) = T_num / T_den in compute-wave units; W_comp
@@ -139,11 +144,23 @@ typedef struct {
  *   drain = 2 (readiness = 0, comm_tile_m_last = comm_tile_m or 0): every
  *     slot serves what remains of every split once the compute ends at
  *     E = A_{L-1}.  Until then the C consumers take the splits in order,
- *     split s from max(A_s, the end of split s-1), in rounds of C tasks of
- *     rho each: they complete min(W_comm, C floor((E - start)/rho)) tasks of
- *     it, stopping at the first split they cannot finish; with R the tasks
- *     left of all L W_comm, T(C) = E + rho ceil(R / (C + P)).  F_s is the
- *     end of split s where the consumers finished it before E, else T(C);
+ *     split s from start = max(A_s, the end of split s-1), in rounds of C
+ *     tasks of rho each; the rounds begun before E claim
+ *     min(W_comm, C ceil((E - start)/rho)) tasks of it, stopping at the first
+ *     split they do not wholly claim.  The Idle = V P - L W_comp compute
+ *     slots without a tile in the last compute wave (V = ceil(L W_comp / P))
+ *     are free from E - 1: in their ceil(1/rho) rounds begun before E they
+ *     claim up to Idle ceil(1/rho) of the unclaimed tasks of the splits
+ *     with A_s <= E - 1 (s < L - 1), ending at E - 1 + rho ceil(taken/Idle).
+ *     With R the tasks left of all L W_comm and e the end of the last
+ *     claimed round, T(C) = max(E + rho ceil(R / (C + P)), e); C = 0 is the
+ *     same with no consumers and P = P0.  F_s is the end of split s where
+ *     the consumers finished it before E, else T(C);
+ *   split_cost = pi_ref > 0 (readiness = 0): pi = pi_ref (K_ref/K)
+ *     (T_M,ref T_N,ref)/(T_M T_N) compute waves per split boundary, so
+ *     A_s = ceil((s+1) W_comp / P) + s pi (and for C = 0 the end of the
+ *     compute is ceil(L W_comp / P0) + (L-1) pi); T_den is then the least
+ *     common multiple of rho's denominator and pi's;
  *   readiness = 1 (column splits only): the consumer work is released
  *     a compute wave at a time instead of a split at a time.  The L W_comp
  *     tiles complete in V = ceil(L W_comp / P) waves, wave v (1-based) the
@@ -503,7 +520,7 @@ int moe_gemm2_status(void* workspace, void* stream, int clear);
 /* Static description of an error code. */
 const char* moe_strerror(int status);
 
-/* ABI version of this header (major * 100 + minor): 107. */
+/* ABI version of this header (major * 100 + minor): 108. */
 int moe_gemm2_abi_version(void);
 
 #ifdef __cplusplus

@@ -48,9 +48,19 @@ special case split_axis = 0, drain = False, one given L):
     split s from start = max(A_s, the end of split s-1), in rounds of C
     tasks of rho each; the rounds that start before E claim
     min(W_comm, C ceil((E - start)/rho)) tasks of split s, stopping at the
-    first split not wholly claimed.  With R the tasks left of all L W_comm
-    and e the end of the consumers' last claimed round,
-    T(C) = max(E + rho ceil(R / (C + P)), e);
+    first split not wholly claimed.  The Idle = V P - L W_comp compute
+    slots that hold no tile in the last of the V = ceil(L W_comp / P)
+    compute waves are free from E - 1; in the ceil(1/rho) rounds they begin
+    before E they take up to Idle ceil(1/rho) of the tasks not yet claimed
+    of the splits ready by then (A_s <= E - 1, s < L - 1), ending at
+    E - 1 + rho ceil(taken / Idle).  With R the tasks left of all L W_comm
+    and e the end of the last claimed round,
+    T(C) = max(E + rho ceil(R / (C + P)), e); C = 0 is the same with no
+    consumers and P0 slots;
+  * split cost pi_ref (readiness 0): each split's publish delays the
+    compute of the splits after it by pi = pi_ref (K_ref/K)
+    (T_M,ref T_N,ref)/(T_M T_N) compute waves: A_s = ceil((s+1) W_comp / P)
+    + s pi, and for C = 0 the compute ends at ceil(L W_comp / P0) + (L-1) pi;
   * L as a decision variable: the (L, C) pair with the least T(C) over a
     range of L, ties to the smaller L;
   * readiness = 1 (column splits): the consumer work is released a compute
@@ -158,11 +168,21 @@ class LastSplit:
 
 def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
              o_comp: int, rho: Fraction, drain: int = 0,
-             readiness: int = 0, last: Optional[LastSplit] = None) -> Optional[Candidate]:
-    """The recurrence for one candidate C; None if P(C) <= 0 (illegal)."""
+             readiness: int = 0, last: Optional[LastSplit] = None,
+             pi: Fraction = Fraction(0)) -> Optional[Candidate]:
+    """The recurrence for one candidate C; None if P(C) <= 0 (illegal).
+    pi: the split cost, compute waves each earlier split's publish adds to
+    A_s (0 in the paper's model)."""
+    pi = Fraction(pi)
+    if pi and readiness != 0:
+        raise ValueError("a split cost is defined for split readiness")
     if C == 0:
         P0 = o_comp * G
-        A_last = cdiv(L * W_comp, P0)
+        A_last = cdiv(L * W_comp, P0) + (L - 1) * pi
+        if drain == 2:
+            A = [cdiv((s + 1) * W_comp, P0) + s * pi for s in range(L)]
+            return _work_conserving(0, 0, P0, A, W_comm, L, rho, cdiv(L * W_comm, P0),
+                                    Fraction(0), cdiv(W_comp, P0), W_comp)
         if last is None:
             q = Fraction(rho) * cdiv(L * W_comm, P0)
         else:
@@ -181,7 +201,7 @@ def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
     V_comp = cdiv(W_comp, P)
     if readiness == 1:
         return _per_wave(C, R, P, W_comp, W_comm, L, rho, drain, V_comm, q, V_comp)
-    A = [cdiv((s + 1) * W_comp, P) for s in range(L)]
+    A = [cdiv((s + 1) * W_comp, P) + s * pi for s in range(L)]
     if drain == 2:
         return _work_conserving(C, R, P, A, W_comm, L, rho, V_comm, q, V_comp, W_comp)
     F: List[Fraction] = []
@@ -201,17 +221,20 @@ def evaluate(C: int, W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
 
 def _work_conserving(C, R, P, A, W_comm, L, rho, V_comm, q, V_comp, W_comp) -> Candidate:
     """The drain = 2 model: the consumers' claims until the compute ends,
-    then every slot on what remains."""
+    the claims of the compute slots idle in the last compute wave, then
+    every slot on what remains.  C = 0: no consumers, P = P0 (one A and one
+    F entry: the end of the compute and T)."""
     rho = Fraction(rho)
-    end = Fraction(A[L - 1])
+    end = Fraction(A[L - 1])                # E, the end of the compute
     cur = Fraction(A[0])
     claimed = 0
     last_end = Fraction(0)
     F: List[Fraction] = []
-    for s in range(L - 1):
+    # the C consumers, split by split in order, rounds begun before E
+    for s in range(L - 1 if C > 0 else 0):
         start = max(Fraction(A[s]), cur)
         need = cdiv(W_comm, C)
-        started = math.ceil((end - start) / rho) if start < end else 0   # rounds begun before E
+        started = math.ceil((end - start) / rho) if start < end else 0
         if started >= need:
             claimed += W_comm
             cur = start + need * rho
@@ -223,7 +246,23 @@ def _work_conserving(C, R, P, A, W_comm, L, rho, V_comm, q, V_comp, W_comp) -> C
             if started > 0:
                 last_end = start + started * rho
             break
+    # compute slots with no tile in the last of the V compute waves: free
+    # from E - 1, they take unclaimed tasks of the splits ready by then
+    V = cdiv(L * W_comp, P)
+    idle = V * P - L * W_comp
+    if V > 0 and idle > 0:
+        t0 = end - 1
+        ready = [s for s in range(L - 1) if A[s] <= t0]
+        avail = len(ready) * W_comm - claimed
+        if avail > 0:
+            rounds = math.ceil(1 / rho)         # rounds they begin before E
+            take = min(avail, idle * rounds)
+            claimed += take
+            last_end = max(last_end, t0 + cdiv(take, idle) * rho)
     T = max(end + rho * cdiv(L * W_comm - claimed, C + P), last_end)
+    if C == 0:
+        return Candidate(C=0, R=0, P=P, A=[end], V_comm=V_comm, q=rho * V_comm, F=[T], T=T,
+                         V_comp=V_comp, delta=V_comp * P - W_comp)
     F += [T] * (L - len(F))
     return Candidate(C=C, R=R, P=P, A=A, V_comm=V_comm, q=q, F=F, T=T,
                      V_comp=V_comp, delta=V_comp * P - W_comp)
@@ -258,13 +297,13 @@ def _per_wave(C, R, P, W_comp, W_comm, L, rho, drain, V_comm, q, V_comp) -> Cand
 def select_from_work(W_comp: int, W_comm: int, L: int, G: int, o_comm: int,
                      o_comp: int, rho: Fraction, c_min: int, c_max: int,
                      drain: int = 0, readiness: int = 0,
-                     last: Optional[LastSplit] = None):
+                     last: Optional[LastSplit] = None, pi: Fraction = Fraction(0)):
     """Argmin of T(C) over the legal C, then smallest Delta, then smallest C.
 
     Returns (best Candidate or None, list of all legal candidates)."""
     cands = []
     for C in range(c_min, c_max + 1):
-        c = evaluate(C, W_comp, W_comm, L, G, o_comm, o_comp, rho, drain, readiness, last)
+        c = evaluate(C, W_comp, W_comm, L, G, o_comm, o_comp, rho, drain, readiness, last, pi)
         if c is not None:
             cands.append(c)
     if not cands:
@@ -297,6 +336,7 @@ class SelectParams:
     comm_tile_n_ref: int = 1024
     readiness: int = 0
     comm_tile_m_last: int = 0      # 0: the last split's tasks as the others'
+    split_cost: Fraction = Fraction(0)   # pi_ref; 0: no split cost (the paper)
 
 
 def select(T: int, H: int, I: int, E: int, topk: int, L: int,
@@ -312,10 +352,18 @@ def select(T: int, H: int, I: int, E: int, topk: int, L: int,
                                  task_width(H, L, p.comm_tile_n, p.split_axis),
                                  p.comm_tile_n_ref)
     last = last_split(T, D, H, L, p, rho)
+    pi = split_cost(p, I)
     best, cands = select_from_work(W_comp, W_comm, L, p.num_cus, p.occ_comm,
                                    p.occ_comp, rho, p.c_min, p.c_max, int(p.drain),
-                                   p.readiness, last)
+                                   p.readiness, last, pi)
     return best, cands, W_comp, W_comm, rho
+
+
+def split_cost(p: SelectParams, K: int) -> Fraction:
+    """pi = pi_ref (K_ref/K) (T_M,ref T_N,ref)/(T_M T_N): a publish costs a
+    fixed time, a compute wave scales with the tile's work."""
+    return (Fraction(p.split_cost) * Fraction(p.k_ref, K)
+            * Fraction(p.tile_m_ref * p.tile_n_ref, p.tile_m * p.tile_n))
 
 
 def last_split(T: int, D: int, H: int, L: int, p: SelectParams,

@@ -63,7 +63,8 @@ class SelectParams(ctypes.Structure):
                 ("split_axis", ctypes.c_int32), ("drain", ctypes.c_int32),
                 ("rho_kh", ctypes.c_int32), ("topk_ref", ctypes.c_int32),
                 ("comm_tile_n_ref", ctypes.c_int32), ("readiness", ctypes.c_int32),
-                ("comm_tile_m_last", ctypes.c_int32)]
+                ("comm_tile_m_last", ctypes.c_int32),
+                ("split_cost_num", ctypes.c_int64), ("split_cost_den", ctypes.c_int64)]
 
 
 class Partition(ctypes.Structure):

@@ -2043,6 +2043,12 @@ constexpr int64_t kRhoScatterDen = 100;
 // 36.7 us / 20.3 us = 1.81.
 constexpr int64_t kRhoBandsNum = 181;
 constexpr int64_t kRhoBandsDen = 100;
+// The split cost of token bands: the compute workgroups' busy time per band
+// boundary (the publish, ~5 us, and the slower stages around it) over the
+// mean tile time, traced at T = 16384, H = 2048, I = 704, E = 32, top-6,
+// uniform routing, C = 0, L = 1, 2, 4: 8.5 us / 19.7 us = 0.43.
+constexpr int64_t kSplitCostBandsNum = 43;
+constexpr int64_t kSplitCostBandsDen = 100;
 constexpr int kDefaultFixedC = 8;
 
 // Selector parameters of a launch.  comm_tm is the owner-write task's token
@@ -2101,6 +2107,10 @@ void fill_params(const DevInfo& d, int mode, int topk, int comm_tm, moe_select_p
   p->topk_ref = 6;
   p->comm_tile_n_ref = kCommTN;
   p->rho_kh = 0;
+  // token bands, where L is chosen as well: what each band's publish costs
+  // the compute (the owner-write selection keeps the paper's model)
+  p->split_cost_num = mode == 2 ? kSplitCostBandsNum : 0;
+  p->split_cost_den = mode == 2 ? kSplitCostBandsDen : 1;
   if (mode != 1)
     if (const char* s = std::getenv("MOE_GEMM2_RHO_KH")) p->rho_kh = std::atoi(s) == 1 ? 1 : 0;
 }

@@ -35,9 +35,19 @@
 //     s-1), in rounds of C tasks of rho each; the rounds that start before
 //     the compute ends at E = A_{L-1} claim
 //       min(W_comm, C ceil((E - start_s) / rho)) tasks of split s,
-//     stopping at the first split not wholly claimed; with R the tasks left
-//     (of all L W_comm) and e the end of the consumers' last claimed round,
+//     stopping at the first split not wholly claimed.  The
+//     Idle = V P - L W_comp compute slots with no tile in the last compute
+//     wave (V = ceil(L W_comp / P)) are free from E - 1 and claim, in their
+//     ceil(1/rho) rounds begun before E, up to Idle ceil(1/rho) unclaimed
+//     tasks of the splits ready by then (A_s <= E - 1, s < L - 1).  With R
+//     the tasks left (of all L W_comm) and e the end of the last claimed
+//     round,
 //       T(C) = max(E + rho ceil(R / (C + P)), e);
+//     C = 0 is the same with no consumers over P0 slots;
+//   split_cost = pi_ref > 0 (readiness 0): each split's publish delays the
+//     compute after it by pi = pi_ref (K_ref/K) (T_M,ref T_N,ref)/(T_M T_N)
+//     compute waves: A_s = ceil((s+1) W_comp / P) + s pi (C = 0: the compute
+//     ends at ceil(L W_comp / P0) + (L-1) pi);
 //   readiness = 1 (column splits): consumer work is released a compute wave
 //     at a time: of V = ceil(L W_comp / P) waves, wave v releases the tasks
 //     of the tiles it completes, w_v = ceil(t_v L W_comm / (L W_comp)) -
@@ -100,6 +110,7 @@ struct Model {
   int64_t rho_last = 0;               // rho_last over the same unit
   int64_t a = 1, b = 1;               // T_M^comm : T_M^last in lowest terms
   int64_t rho_unit = 0;               // rho / a over the time unit
+  int64_t pi = 0;                     // split_cost over the time unit
   int L = 1;
   int drain = 0;
   int readiness = 0;
@@ -180,13 +191,101 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
   const i128 g = gcd128(num, a);
   const i128 rn = num * (a / g), rd = den * (a / g), rl = num / g * b, ru = num / g;
   if (rn > kI64Max || rd > kI64Max || rl > kI64Max) return MOE_ERR_INVALID_ARG;
-  m->rho_num = (int64_t)rn;
-  m->rho_den = (int64_t)rd;
-  m->rho_last = (int64_t)rl;
-  m->rho_unit = (int64_t)ru;
+  // the split cost pi = pi_ref (K_ref/K) (T_M,ref T_N,ref)/(T_M T_N) waves,
+  // pn/pd in lowest terms; the time unit becomes 1/lcm(rd, pd) waves
+  i128 pn = 0, pd = 1;
+  if (p->split_cost_num < 0) return MOE_ERR_INVALID_ARG;
+  if (p->split_cost_num > 0) {
+    if (p->split_cost_den <= 0 || p->readiness != 0) return MOE_ERR_INVALID_ARG;
+    pn = (i128)p->split_cost_num * p->k_ref * p->tile_m_ref * p->tile_n_ref;
+    pd = (i128)p->split_cost_den * wl->I * p->tile_m * p->tile_n;
+    const i128 gp = gcd128(pn, pd);
+    pn /= gp;
+    pd /= gp;
+  }
+  const i128 u = pd / gcd128(rd, pd);
+  const i128 rn2 = rn * u, rd2 = rd * u, rl2 = rl * u, ru2 = ru * u;
+  if (rn2 > kI64Max || rd2 > kI64Max || rl2 > kI64Max || pn > kI64Max)
+    return MOE_ERR_INVALID_ARG;
+  const i128 pi = pn * (rd2 / pd);
+  if (pi > kI64Max / (wl->splits > 1 ? wl->splits : 1)) return MOE_ERR_INVALID_ARG;
+  m->pi = (int64_t)pi;
+  m->rho_num = (int64_t)rn2;
+  m->rho_den = (int64_t)rd2;
+  m->rho_last = (int64_t)rl2;
+  m->rho_unit = (int64_t)ru2;
   m->a = (int64_t)a;
   m->b = (int64_t)b;
   return MOE_OK;
+}
+
+// The split arrival time A_s = ceil((s+1) W_comp / P) + s pi over the time
+// unit (exact in 128 bits).
+inline i128 arrival(const Model& m, int s, int64_t P) {
+  return (i128)cdiv64((int64_t)(s + 1) * m.W_comp, P) * m.rho_den + (i128)s * m.pi;
+}
+
+// The work-conserving drain (drain = 2) for C >= 0 consumers beside P
+// compute slots: the consumers' claims until the compute ends at
+// E = A_{L-1}, the claims of the compute slots that hold no tile in the last
+// compute wave, then every slot on what remains.  Returns T(C); false on
+// overflow.  Records A_s and F_s for s < L when C > 0.
+bool work_conserving(const Model& m, int64_t C, int64_t P, i128* T, int64_t* A_rec,
+                     int64_t* F_rec) {
+  const i128 E = arrival(m, m.L - 1, P);
+  i128 cur = arrival(m, 0, P);
+  i128 last_end = 0;      // end of the last claimed round
+  int64_t claimed = 0;
+  int s_stop = C > 0 ? m.L - 1 : 0;   // first split the consumers do not wholly claim
+  for (int s = 0; C > 0 && s + 1 < m.L; ++s) {
+    const i128 A = arrival(m, s, P);
+    if (A_rec) A_rec[s] = (int64_t)A;
+    const i128 start = A > cur ? A : cur;
+    const int64_t need = cdiv64(m.W_comm, C);
+    // rounds that start before E
+    const i128 started = start < E ? (E - start + m.rho_num - 1) / m.rho_num : 0;
+    if (started >= need) {
+      claimed += m.W_comm;
+      cur = start + (i128)need * m.rho_num;
+      if (need > 0) last_end = cur;
+      if (F_rec) F_rec[s] = (int64_t)cur;
+    } else {
+      claimed += (int64_t)((i128)C * started);
+      if (started > 0) last_end = start + started * m.rho_num;
+      s_stop = s;
+      break;
+    }
+  }
+  // the compute slots with no tile in the last compute wave, free one wave
+  // before E, on the unclaimed tasks of the splits ready by then
+  const int64_t tiles = (int64_t)m.L * m.W_comp;
+  const int64_t V = cdiv64(tiles, P);
+  const i128 idle = (i128)V * P - tiles;
+  if (V > 0 && idle > 0) {
+    const i128 t0 = E - m.rho_den;
+    int ready = 0;
+    while (ready + 1 < m.L && arrival(m, ready, P) <= t0) ++ready;
+    const i128 avail = (i128)ready * m.W_comm - claimed;
+    if (avail > 0) {
+      const i128 rounds = ((i128)m.rho_den + m.rho_num - 1) / m.rho_num;
+      const i128 cap = idle * rounds;
+      const i128 take = avail < cap ? avail : cap;
+      claimed += (int64_t)take;
+      const i128 end = t0 + (take + idle - 1) / idle * m.rho_num;
+      if (end > last_end) last_end = end;
+    }
+  }
+  const int64_t R = (int64_t)((i128)m.L * m.W_comm - claimed);
+  i128 F = E + (i128)m.rho_num * cdiv64(R, C + P);
+  if (last_end > F) F = last_end;
+  if (F > kI64Max) return false;
+  if (C > 0)
+    for (int s = s_stop; s < m.L; ++s) {   // splits finished in the drain end with it
+      if (A_rec) A_rec[s] = (int64_t)arrival(m, s, P);
+      if (F_rec) F_rec[s] = (int64_t)F;
+    }
+  *T = F;
+  return true;
 }
 
 // One candidate; returns false if P(C) <= 0.  Status MOE_ERR_INVALID_ARG on
@@ -198,16 +297,24 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
                     int64_t* A_rec = nullptr, int64_t* F_rec = nullptr) {
   if (C == 0) {
     const int64_t P0 = (int64_t)p->occ_comp * p->num_cus;
-    const i128 A = (i128)cdiv64((int64_t)m.L * m.W_comp, P0) * m.rho_den;
-    // every task in units of rho/a: a for the other splits' tasks, b for the
-    // last split's (a = b = 1 gives rho ceil(L W_comm / P0))
-    const i128 units = (i128)m.a * (m.L - 1) * m.W_comm + (i128)m.b * m.W_last;
-    if (units > kI64Max) {
-      *status = MOE_ERR_INVALID_ARG;
-      return false;
+    const i128 A = arrival(m, m.L - 1, P0);
+    i128 F;
+    if (m.drain == 2) {
+      if (!work_conserving(m, 0, P0, &F, nullptr, nullptr)) {
+        *status = MOE_ERR_INVALID_ARG;
+        return false;
+      }
+    } else {
+      // every task in units of rho/a: a for the other splits' tasks, b for
+      // the last split's (a = b = 1 gives rho ceil(L W_comm / P0))
+      const i128 units = (i128)m.a * (m.L - 1) * m.W_comm + (i128)m.b * m.W_last;
+      if (units > kI64Max) {
+        *status = MOE_ERR_INVALID_ARG;
+        return false;
+      }
+      F = A + (i128)m.rho_unit * cdiv64((int64_t)units, P0);
     }
-    const i128 F = A + (i128)m.rho_unit * cdiv64((int64_t)units, P0);
-    if (F > kI64Max) {
+    if (A > kI64Max || F > kI64Max) {
       *status = MOE_ERR_INVALID_ARG;
       return false;
     }
@@ -249,42 +356,9 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
       }
     }
   } else if (m.drain == 2) {
-    // work-conserving drain: the dedicated consumers' claims until the
-    // compute ends, then every slot on what remains (exact, in 128 bits)
-    const i128 E = (i128)cdiv64((int64_t)m.L * m.W_comp, P) * m.rho_den;
-    i128 cur = (i128)cdiv64(m.W_comp, P) * m.rho_den;   // A_0
-    i128 last_end = 0;      // end of the consumers' last claimed round
-    int64_t claimed = 0;
-    int s_stop = m.L - 1;   // first split the consumers do not wholly claim
-    for (int s = 0; s + 1 < m.L; ++s) {
-      const i128 A = (i128)cdiv64((int64_t)(s + 1) * m.W_comp, P) * m.rho_den;
-      if (A_rec) A_rec[s] = (int64_t)A;
-      const i128 start = A > cur ? A : cur;
-      const int64_t need = cdiv64(m.W_comm, C);
-      // rounds that start before E
-      const i128 started = start < E ? (E - start + m.rho_num - 1) / m.rho_num : 0;
-      if (started >= need) {
-        claimed += m.W_comm;
-        cur = start + (i128)need * m.rho_num;
-        if (need > 0) last_end = cur;
-        if (F_rec) F_rec[s] = (int64_t)cur;
-      } else {
-        claimed += (int64_t)((i128)C * started);
-        if (started > 0) last_end = start + started * m.rho_num;
-        s_stop = s;
-        break;
-      }
-    }
-    const int64_t R = (int64_t)((i128)m.L * m.W_comm - claimed);
-    F = E + (i128)m.rho_num * cdiv64(R, (int64_t)C + P);
-    if (last_end > F) F = last_end;
-    if (F > kI64Max) {
+    if (!work_conserving(m, C, P, &F, A_rec, F_rec)) {
       *status = MOE_ERR_INVALID_ARG;
       return false;
-    }
-    for (int s = s_stop; s < m.L; ++s) {   // splits finished in the drain end with it
-      if (A_rec) A_rec[s] = (int64_t)((i128)cdiv64((int64_t)(s + 1) * m.W_comp, P) * m.rho_den);
-      if (F_rec) F_rec[s] = (int64_t)F;
     }
   } else {
     // 64-bit with overflow checks: F_s >= A_s and F_s >= q, so any term
@@ -298,6 +372,7 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
     for (int s = 0; s < m.L && !ovf; ++s) {
       int64_t A;
       ovf |= __builtin_mul_overflow(cdiv64((int64_t)(s + 1) * m.W_comp, P), m.rho_den, &A);
+      ovf |= __builtin_add_overflow(A, (int64_t)s * m.pi, &A);
       ovf |= __builtin_add_overflow(A > F64 ? A : F64, s == m.L - 1 ? q_last : q, &F64);
       if (A_rec) A_rec[s] = A;
       if (F_rec) F_rec[s] = F64;
@@ -459,4 +534,4 @@ extern "C" const char* moe_strerror(int status) {
   }
 }
 
-extern "C" int moe_gemm2_abi_version(void) { return 107; }
+extern "C" int moe_gemm2_abi_version(void) { return 108; }

@@ -29,7 +29,7 @@ def test_library_exports_every_declared_function():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(B.EXPORTED)
-    assert L.moe_gemm2_abi_version() == 107
+    assert L.moe_gemm2_abi_version() == 108
 
 
 def _params(**kw):
@@ -52,16 +52,23 @@ def _oracle_params(p):
         tile_m_ref=p.tile_m_ref, tile_n_ref=p.tile_n_ref, d_ref=p.d_ref, groups=p.groups,
         split_axis=p.split_axis, drain=int(p.drain), rho_kh=bool(p.rho_kh),
         topk_ref=p.topk_ref, comm_tile_n_ref=p.comm_tile_n_ref, readiness=p.readiness,
-        comm_tile_m_last=p.comm_tile_m_last)
+        comm_tile_m_last=p.comm_tile_m_last,
+        split_cost=(Fraction(p.split_cost_num, p.split_cost_den) if p.split_cost_num > 0
+                    else Fraction(0)))
 
 
-def _time_den(p, rho):
+def _time_den(p, rho, I=None):
     """The library's time unit: rho's denominator, times a / gcd(rho's
     numerator, a) when the last split's tasks are cut finer
-    (a : b = comm_tile_m : comm_tile_m_last in lowest terms)."""
+    (a : b = comm_tile_m : comm_tile_m_last in lowest terms), then the least
+    common multiple with the split cost's denominator (K = I)."""
     tm_last = p.comm_tile_m_last or p.comm_tile_m
     a = p.comm_tile_m // math.gcd(p.comm_tile_m, tm_last)
-    return rho.denominator * a // math.gcd(rho.numerator, a)
+    den = rho.denominator * a // math.gcd(rho.numerator, a)
+    if p.split_cost_num > 0:
+        pd = osel.split_cost(_oracle_params(p), I).denominator
+        den = den * pd // math.gcd(den, pd)
+    return den
 
 
 def test_hand_example_through_the_abi():
@@ -162,6 +169,34 @@ def test_work_conserving_drain_hand_example_through_the_abi():
         assert B.select_partition(wl, q)[0] == B.MOE_ERR_INVALID_ARG, bad
 
 
+def test_idle_slots_and_split_cost_through_the_abi():
+    """The oracle's hand example for the idle compute slots and the split
+    cost (G=10, W_comp=13, W_comm=12, L=2, rho=1/2, drain = 2): one expert of
+    13 rows in 1x1 tiles over two 1-column splits, 24 tokens in tasks of 2.
+    T(0), T(1), T(2) = 4, 4, 5; with pi = 1/4: 17/4, 17/4, 21/4."""
+    p = _params(tile_m=1, tile_n=1, comm_tile_m=2, comm_tile_n=1, occ_comp=1, occ_comm=1,
+                num_cus=10, c_min=0, c_max=2, rho_ref_num=1, rho_ref_den=2, k_ref=8,
+                tile_m_ref=1, tile_n_ref=1, drain=2)
+    wl, keep = B.make_workload(T=24, H=2, I=8, E=1, topk=1, splits=2, counts=[13])
+    n, table, den = B.select_evaluate(wl, p)
+    assert [Fraction(t, den) for t in table] == [4, 4, 5]
+    p.split_cost_num, p.split_cost_den = 1, 4
+    n, table, den = B.select_evaluate(wl, p)
+    assert den == 4 and [Fraction(t, den) for t in table] == \
+        [Fraction(17, 4), Fraction(17, 4), Fraction(21, 4)]
+    assert B.select_candidate(wl, p, 2) == (2, 2, 4, [8, 17], [21, 21])
+    assert B.select_candidate(wl, p, 0) == (1, 2, 4, [13], [17])
+    # a split cost needs split readiness; a negative one is invalid
+    p.readiness = 1
+    p.drain = 0
+    assert B.select_partition(wl, p)[0] == B.MOE_ERR_INVALID_ARG
+    p.readiness = 0
+    p.split_cost_num = -1
+    assert B.select_partition(wl, p)[0] == B.MOE_ERR_INVALID_ARG
+    p.split_cost_num, p.split_cost_den = 1, 0
+    assert B.select_partition(wl, p)[0] == B.MOE_ERR_INVALID_ARG
+
+
 def _random_case(rnd):
     E = rnd.randint(1, 64)
     topk = rnd.randint(1, min(E, 8))
@@ -194,6 +229,9 @@ def _random_case(rnd):
             p.readiness = rnd.choice([0, 1, 1])
         if p.readiness == 0 and p.drain != 2:
             p.comm_tile_m_last = rnd.choice([0, 0, p.comm_tile_m // 2, 16, 48, p.comm_tile_m])
+    if p.readiness == 0 and rnd.random() < 0.4:
+        p.split_cost_num = rnd.choice([1, 2, 43, 100, 7919])
+        p.split_cost_den = rnd.choice([1, 3, 100, 257])
     D = rnd.choice([1, 1, 2, 4])
     return T, H, I, E, topk, L, counts, p, D
 
@@ -213,7 +251,7 @@ def test_selector_bit_exact_against_oracle():
         assert r == best.C
         assert (part.C, part.R, part.P, part.delta_comp) == (best.C, best.R, best.P, best.delta)
         assert (part.W_comp, part.W_comm) == (W_comp, W_comm)
-        assert part.T_den == _time_den(p, rho)
+        assert part.T_den == _time_den(p, rho, I)
         assert Fraction(part.T_num, part.T_den) == best.T
         # whole table
         n, table, den = B.select_evaluate(wl, p)
@@ -247,7 +285,7 @@ def test_candidate_internals_bit_exact_against_oracle():
             assert r == B.MOE_ERR_NO_LEGAL_PARTITION, (r, C)
             continue
         cand = byC[C]
-        assert Fraction(num, den) == rho and den == _time_den(p, rho)
+        assert Fraction(num, den) == rho and den == _time_den(p, rho, I)
         assert r == len(cand.A) == len(cand.F)
         if p.readiness == 0:
             assert r == (1 if C == 0 else L)

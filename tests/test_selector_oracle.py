@@ -412,6 +412,48 @@ def test_work_conserving_drain_hand_example():
     assert sel.evaluate(5, 30, 6, 2, 10, 1, 2, rho, drain=1).T == Fraction(15, 2)
 
 
+def test_idle_slots_and_split_cost_hand_example():
+    """drain = 2 on G=10, o=1, W_comp=13, W_comm=12, L=2, rho=1/2, worked by
+    hand (the idle compute slots of the last compute wave, and the split
+    cost pi):
+      C=0: P0=10, 26 tiles in V=3 waves, Idle = 30 - 26 = 4 slots free from
+           E - 1 = 2; split 0 is ready (A_0 = ceil(13/10) = 2 <= 2); they
+           begin ceil(1/rho) = 2 rounds before E = 3 and take 8 of its 12
+           tasks, ending at 2 + 2 rho = 3; R = 24 - 8 = 16,
+           T = max(3 + rho ceil(16/10), 3) = 4, against 3 + rho ceil(24/10)
+           = 9/2 without the idle slots, and 9/2 for the same work in one
+           split (L=1: nothing is ready before E);
+      C=0, pi=1/4: E = 3 + 1/4 = 13/4, the idle slots from 9/4 (split 0
+           ready) take 8 in 2 rounds ending at 13/4; T = 13/4 + 1 = 17/4;
+      C=2: P=8, A=(2,4)=(A_0,E), V=4, Idle=6; the consumers begin 4 rounds
+           before E (2, 5/2, 3, 7/2) and claim 8, the last ending at 4; the
+           idle slots from 3 take the other 4 (one round, ending at 7/2);
+           R = 12, T = max(4 + rho ceil(12/10), 4) = 5;
+      C=2, pi=1/4: A = (2, 17/4); the consumers begin 5 rounds before E and
+           claim 10 (ending at 9/2), the idle slots from 13/4 the other 2;
+           R = 12, T = 17/4 + 1 = 21/4; and the paper's recurrence with the
+           same pi: F_0 = 2 + 6 rho = 5, F_1 = max(17/4, 5) + 6 rho = 8."""
+    rho = Fraction(1, 2)
+    c = sel.evaluate(0, 13, 12, 2, 10, 1, 1, rho, drain=2)
+    assert (c.A, c.F, c.T) == ([3], [4], 4)
+    assert sel.evaluate(0, 13, 12, 2, 10, 1, 1, rho).T == Fraction(9, 2)
+    assert sel.evaluate(0, 26, 24, 1, 10, 1, 1, rho, drain=2).T == Fraction(9, 2)
+    c = sel.evaluate(0, 13, 12, 2, 10, 1, 1, rho, drain=2, pi=Fraction(1, 4))
+    assert (c.A, c.T) == ([Fraction(13, 4)], Fraction(17, 4))
+    c = sel.evaluate(2, 13, 12, 2, 10, 1, 1, rho, drain=2)
+    assert (c.A, c.F, c.T) == ([2, 4], [5, 5], 5)
+    c = sel.evaluate(2, 13, 12, 2, 10, 1, 1, rho, drain=2, pi=Fraction(1, 4))
+    assert (c.A, c.F, c.T) == ([2, Fraction(17, 4)], [Fraction(21, 4)] * 2, Fraction(21, 4))
+    c = sel.evaluate(2, 13, 12, 2, 10, 1, 1, rho, pi=Fraction(1, 4))
+    assert (c.A, c.F, c.T) == ([2, Fraction(17, 4)], [5, 8], 8)
+    # the split cost scales like rho's first two factors
+    p = sel.SelectParams(tile_m=128, tile_n=256, comm_tile_m=64, comm_tile_n=1024, occ_comp=1,
+                         occ_comm=1, num_cus=256, c_min=0, c_max=8, rho_ref=Fraction(1),
+                         k_ref=704, tile_m_ref=256, tile_n_ref=256, d_ref=1,
+                         split_cost=Fraction(43, 100))
+    assert sel.split_cost(p, 1408) == Fraction(43, 100) * Fraction(1, 2) * 2
+
+
 def test_work_conserving_drain_properties():
     """drain = 2 never predicts a later end than drain = 1 (the compute slots
     only add service), equals it where the consumers finish every split but
@@ -433,20 +475,43 @@ def test_work_conserving_drain_properties():
             if L == 1 or c1.F[L - 2] <= c1.A[L - 1]:
                 assert c2.T == c1.T
                 n_equal += 1
-            # the consumers' rounds one at a time: a round that begins before
-            # E claims up to C tasks of the current split
-            E, t, claimed, last = Fraction(c2.A[L - 1]), None, 0, Fraction(0)
-            for s in range(L - 1):
-                t = Fraction(c2.A[s]) if t is None else max(Fraction(c2.A[s]), t)
-                left = W_comm
-                while left > 0 and t < E:
-                    k = min(C, left)
-                    left -= k
-                    claimed += k
-                    t += rho
-                    last = t
-                if left > 0:
-                    break
-            want = max(E + rho * sel.cdiv(L * W_comm - claimed, C + c2.P), last)
-            assert c2.T == want
+            assert c2.T == _simulate_work_conserving(C, c2.P, c2.A, W_comp, W_comm, L, rho)
+        # the role switch: no consumers, the compute slots only
+        c0 = sel.evaluate(0, W_comp, W_comm, L, G, 1, o, rho, drain=2)
+        A0 = [Fraction(sel.cdiv((s + 1) * W_comp, o * G)) for s in range(L)]
+        assert c0.T == _simulate_work_conserving(0, o * G, A0, W_comp, W_comm, L, rho)
+        assert c0.T <= sel.evaluate(0, W_comp, W_comm, L, G, 1, o, rho).T
     assert n_equal > 100
+
+
+def _simulate_work_conserving(C, P, A, W_comp, W_comm, L, rho):
+    """The drain = 2 model by direct simulation, one round at a time: the
+    consumers' rounds that begin before E each claim up to C tasks of the
+    current split; then the compute slots idle in the last compute wave,
+    from E - 1, claim up to that many tasks per round of the splits ready by
+    then, in rounds that begin before E; every slot serves the rest."""
+    E, t, claimed, last = Fraction(A[L - 1]), None, 0, Fraction(0)
+    for s in range(L - 1 if C > 0 else 0):
+        t = Fraction(A[s]) if t is None else max(Fraction(A[s]), t)
+        left = W_comm
+        while left > 0 and t < E:
+            k = min(C, left)
+            left -= k
+            claimed += k
+            t += rho
+            last = t
+        if left > 0:
+            break
+    V = -(-(L * W_comp) // P)
+    idle = V * P - L * W_comp
+    if V > 0 and idle > 0:
+        ready = sum(W_comm for s in range(L - 1) if A[s] <= E - 1)
+        left = ready - claimed
+        t = E - 1
+        while left > 0 and t < E:
+            k = min(idle, left)
+            left -= k
+            claimed += k
+            t += rho
+            last = max(last, t)
+    return max(E + rho * sel.cdiv(L * W_comm - claimed, C + P), last)
