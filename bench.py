@@ -207,7 +207,9 @@ def launch_cfg(dw, c):
 def time_configs(launch, keys, samples, warmups, torch):
     """Event time (us) of every key, `samples` times each: `warmups`
     untimed passes over all keys, then passes alternately forward and
-    backward over the keys (ABBA), one stream synchronisation per pass."""
+    backward over the keys (ABBA), one stream synchronisation per pass.
+    Each pass starts with an untimed launch of its first key, so that no
+    timed launch starts on a GPU left idle by the synchronisation."""
     stream = torch.cuda.current_stream()
     for _ in range(warmups):
         for k in keys:
@@ -216,6 +218,7 @@ def time_configs(launch, keys, samples, warmups, torch):
     times = {k: [] for k in keys}
     for s in range(samples):
         order = keys if s % 2 == 0 else keys[::-1]
+        launch(order[0])
         evs = []
         for k in order:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -297,8 +300,10 @@ def run_sweep(B, torch, samples, warmups, repeats=2, c_max=64):
         res = {}
         for pt in order:
             log(f"sweep {rep_i + 1}/{repeats} {pt.name}")
-            keys = Cs + [k for k in band_grid] + ([pt.pick_bands] if pt.pick_bands not in
-                                                  band_grid else [])
+            # the band pick among its grid neighbours (ordered by L, then C),
+            # not at an end of the pass
+            band_keys = sorted(set(band_grid) | {pt.pick_bands}, key=lambda k: (k[2], k[0]))
+            keys = Cs + band_keys
             t = time_configs(lambda c: launch_cfg(pt.dw, c), keys, samples, warmups, torch)
             assert pt.dw.ws.status() == 0
             res[pt.name] = {k: median_ci(v) for k, v in t.items()}
