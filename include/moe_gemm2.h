@@ -245,9 +245,10 @@ int moe_gemm2_default_params(int device, moe_select_params_t* out);
  * (MOE_GEMM2_RHO_REF_SCATTER="num/den" overrides it) and readiness = 1 (a
  * scatter task waits only for the published prefix of the tile sequence up
  * to its own tile); mode 2 (token bands)
- * sets split_axis = 1, drain = 2 and rho_ref to that mode's calibration
- * (MOE_GEMM2_RHO_REF_BANDS overrides it).  Modes 0 and 1 leave split_axis
- * and drain 0.  Every mode sets topk_ref = 6 and comm_tile_n_ref = 1024 (the
+ * sets split_axis = 1, drain = 2, rho_ref to that mode's calibration
+ * (MOE_GEMM2_RHO_REF_BANDS overrides it) and the split cost pi_ref = 43/100
+ * (split_cost_num / split_cost_den).  Modes 0 and 1 leave split_axis, drain
+ * and the split cost 0.  Every mode sets topk_ref = 6 and comm_tile_n_ref = 1024 (the
  * calibration's) and rho_kh = 0; modes 0 and 2 set rho_kh = 1 when the
  * environment sets MOE_GEMM2_RHO_KH=1.  Returns 0 or MOE_ERR_HIP / MOE_ERR_INVALID_ARG (also for a
  * mode other than 0, 1 or 2 or topk <= 0). */
@@ -265,7 +266,9 @@ int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk, moe_sele
  * as moe_gemm2_default_params_ex(device, 1, wl->topk).  Mode 2: tasks of
  * TM tokens x min(1024, H) columns of the full width, TM = 64 halved down
  * to 16 while there would be fewer than 512 (ceil(T/TM) ceil(H/1024)),
- * rho_ref scaled by TM/64, split_axis = 1, drain = 2.  Returns 0,
+ * rho_ref scaled by TM/64, split_axis = 1, drain = 2, and the split cost
+ * pi_ref = 43/100 (split_cost_num / split_cost_den; 0 in modes 0 and 1).
+ * Returns 0,
  * MOE_ERR_INVALID_ARG (null pointer, mode other than 0, 1 or 2, invalid
  * workload), MOE_ERR_UNSUPPORTED (shape outside moe_gemm2_combine_ex's
  * range for that mode) or MOE_ERR_HIP. */
