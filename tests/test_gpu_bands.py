@@ -129,3 +129,34 @@ def test_bands_dropped_slots_and_no_rows(gpu_lib):
     w0.gate_w = np.zeros(1, dtype=np.float32)
     got, used, _ = gpu_util.run(w0, C=2, counts=False, mode=2, splits=3)
     assert np.all(got == 0)
+
+
+@pytest.mark.parametrize("name", ["sweep_T4096_zipf1.2", "sweep_T16384_uniform"])
+def test_bands_selector_pick_bitwise(gpu_lib, name):
+    """The token-band selector's joint (C, L) pick, the configuration the
+    benchmark times (odd C such as 13 or 29 included), and the launch's own
+    selection at that L (num_consumers = -1): bitwise the column-split
+    owner-write output, which is checked against the oracle."""
+    import gpu_util
+    from paper_2609_07536_amd import binding as B
+    from workloads import sweep_workload
+    w = sweep_workload(name)
+    print(f"{name}: T={w.T} rows={w.Mtot}", flush=True)
+    ref = oc.combine_reference(w.x_perm, w.w2, w.expert_offsets, w.token_ids, w.gate_w, w.T)
+    dev = gpu_util.to_device(w)
+    sizes = [B.workspace_size(B.make_workload(w.T, w.H, w.I, w.E, w.topk, L, w.counts,
+                                              rows=w.Mtot)[0]) for L in (1, 2, 3, 4)]
+    ws = B.Workspace(max(sizes))
+    base, _, _ = gpu_util.run(w, C=0, dev=dev, workspace=ws)
+    _check(base, ref, f"{name} mode 0")
+    wl1, _ = B.make_workload(w.T, w.H, w.I, w.E, w.topk, 1, w.counts, rows=w.Mtot)
+    C, L, part = B.select_partition_splits(wl1, B.launch_params(wl1, 2), 1, 4)
+    assert C >= 0 and 1 <= L <= 4
+    for c in (C, -1):
+        print(f"{name} bands pick C={C} L={L} (num_consumers {c})", flush=True)
+        got, used, _ = gpu_util.run(w, C=c, dev=dev, workspace=ws, mode=2, splits=L)
+        if c >= 0:
+            assert used == C
+        if not np.array_equal(got.view(np.uint32), base.view(np.uint32)):
+            _check(got, ref, f"{name} bands C={used} L={L}")
+            raise AssertionError(f"{name} bands C={used} L={L}: not bitwise equal to mode 0")
