@@ -169,6 +169,7 @@ typedef struct {
  *     tasks, t_v = min(v P, L W_comp), and
  *     F_v = max(v, F_{v-1}) + rho ceil(w_v / C), T(C) = F_V (with drain = 1
  *     the last wave's tasks are served by C + P slots); C = 0 is unchanged;
+ *     a candidate with V > 2^20 is an error (MOE_ERR_INVALID_ARG);
  *   rho_kh = 1: rho of eq:rho-scaling times
  *     (2 topk + 4) / (2 topk_ref + 4) * w / comm_tile_n_ref, with the task
  *     width w = min(comm_tile_n, ceil(N/L)) (column splits) or
@@ -182,9 +183,13 @@ typedef struct {
  *     T(0) = ceil(L W_comp / P0) + (rho/a) ceil((a (L-1) W_comm + b W_last) / P0);
  *     T_den is then rho's denominator times a / gcd(rho's numerator, a).
  * Pure host code: no HIP call, no allocation, thread-safe.
+ * Since P(C) does not grow with C, the candidates past the first illegal
+ * C >= 1 are not evaluated (any c_max up to INT32_MAX costs no more than the
+ * legal range).
  * Returns C* >= c_min and fills *out when out != NULL; MOE_ERR_INVALID_ARG for a
- * null wl/p, non-positive dimensions or parameters, a negative host count or
- * arithmetic overflow; MOE_ERR_NO_LEGAL_PARTITION when no candidate is legal. */
+ * null wl/p, non-positive dimensions or parameters, o_comp G > INT32_MAX,
+ * more than 2^20 splits, a negative host count or arithmetic overflow;
+ * MOE_ERR_NO_LEGAL_PARTITION when no candidate is legal. */
 int moe_select_partition(const moe_workload_t* wl, const moe_select_params_t* p,
                          moe_partition_t* out);
 
@@ -196,7 +201,7 @@ int moe_select_partition(const moe_workload_t* wl, const moe_select_params_t* p,
  * *out (each when non-NULL).  wl->splits is ignored.  The caller keeps L
  * within what the launch accepts (column splits: H % (8 L) == 0; token
  * bands: (E + 1) L <= 2048).  Returns C >= 0, MOE_ERR_INVALID_ARG
- * (l_min < 1, l_max < l_min, or as moe_select_partition) or
+ * (l_min < 1, l_max < l_min, l_max > 1024, or as moe_select_partition) or
  * MOE_ERR_NO_LEGAL_PARTITION. */
 int moe_select_partition_splits(const moe_workload_t* wl, const moe_select_params_t* p,
                                 int32_t l_min, int32_t l_max, moe_partition_t* out,

@@ -76,6 +76,12 @@ typedef __int128 i128;
 
 const i128 kI64Max = (i128)INT64_MAX;
 
+// the largest split count moe_select_partition_splits searches
+constexpr int32_t kMaxSplitsSearched = 1024;
+// the most splits, or compute waves with readiness = 1, a candidate's
+// recurrence walks
+constexpr int64_t kMaxSteps = 1 << 20;
+
 // ceil(a / b) for a >= 0, b > 0; in 32 bits when both fit (a 64-bit
 // division costs several times a 32-bit one, and a selection does hundreds)
 inline int64_t cdiv64(int64_t a, int64_t b) {
@@ -127,6 +133,11 @@ int build_model(const moe_workload_t* wl, const moe_select_params_t* p, Model* m
       p->c_max < p->c_min || p->groups <= 0 || p->rho_ref_num <= 0 || p->rho_ref_den <= 0 ||
       p->k_ref <= 0 || p->tile_m_ref <= 0 || p->tile_n_ref <= 0 || p->d_ref <= 0)
     return MOE_ERR_INVALID_ARG;
+  // P(C) <= P(0) = o_comp G is reported as an int32
+  if ((int64_t)p->occ_comp * p->num_cus > INT32_MAX) return MOE_ERR_INVALID_ARG;
+  // the recurrence walks the splits (and with readiness = 1 the compute
+  // waves) of every candidate: bounded so that a selection stays cheap
+  if (wl->splits > kMaxSteps) return MOE_ERR_INVALID_ARG;
 
   // eq:routed-tile-reduction, or the even-load estimate when the counts only
   // live on the device (Method, "System Integration and Correctness").
@@ -338,6 +349,10 @@ bool eval_candidate(const Model& m, const moe_select_params_t* p, int32_t C, int
       if (F_rec) F_rec[0] = (int64_t)F;
     } else {
       const int64_t V = cdiv64(tiles, P);
+      if (V > kMaxSteps) {
+        *status = MOE_ERR_INVALID_ARG;
+        return false;
+      }
       int64_t released = 0;
       for (int64_t v = 1; v <= V; ++v) {
         const int64_t t = v * P < tiles ? v * P : tiles;
@@ -402,12 +417,15 @@ extern "C" int moe_select_partition(const moe_workload_t* wl, const moe_select_p
   bool found = false;
   int64_t bestT = 0, bestD = -1;   // bestD < 0: not computed yet (Delta is needed only on ties)
   int32_t bestC = 0, bestR = 0, bestP = 0;
-  for (int32_t C = p->c_min; C <= p->c_max; ++C) {
+  // P(C) does not grow with C, so past the first C >= 1 with P(C) <= 0
+  // no candidate is legal (and a huge c_max costs nothing)
+  for (int64_t C = p->c_min; C <= p->c_max; ++C) {
     int64_t T;
     int32_t R, P;
     st = MOE_OK;
-    if (!eval_candidate(m, p, C, &T, &R, &P, &st)) {
+    if (!eval_candidate(m, p, (int32_t)C, &T, &R, &P, &st)) {
       if (st != MOE_OK) return st;
+      if (C >= 1) break;
       continue;
     }
     // lexicographic (T, Delta, C); C ascends, so strict improvement only
@@ -422,7 +440,7 @@ extern "C" int moe_select_partition(const moe_workload_t* wl, const moe_select_p
       found = true;
       bestT = T;
       bestD = D;
-      bestC = C;
+      bestC = (int32_t)C;
       bestR = R;
       bestP = P;
     }
@@ -445,7 +463,8 @@ extern "C" int moe_select_partition(const moe_workload_t* wl, const moe_select_p
 extern "C" int moe_select_partition_splits(const moe_workload_t* wl, const moe_select_params_t* p,
                                           int32_t l_min, int32_t l_max, moe_partition_t* out,
                                           int32_t* splits_out) {
-  if (!wl || !p || l_min < 1 || l_max < l_min) return MOE_ERR_INVALID_ARG;
+  if (!wl || !p || l_min < 1 || l_max < l_min || l_max > kMaxSplitsSearched)
+    return MOE_ERR_INVALID_ARG;
   bool found = false;
   moe_partition_t best{};
   int32_t bestL = 0;
@@ -477,21 +496,24 @@ extern "C" int moe_select_evaluate(const moe_workload_t* wl, const moe_select_pa
   Model m;
   int st = build_model(wl, p, &m);
   if (st != MOE_OK) return st;
-  const int32_t count = p->c_max - p->c_min + 1;
+  const int64_t count = (int64_t)p->c_max - p->c_min + 1;
   if (!T_num_out || n < count) return MOE_ERR_INVALID_ARG;
-  for (int32_t i = 0; i < count; ++i) {
+  bool past = false;   // past the legal candidates (P(C) does not grow with C)
+  for (int64_t i = 0; i < count; ++i) {
     int64_t T;
     int32_t R, P;
     st = MOE_OK;
-    if (eval_candidate(m, p, p->c_min + i, &T, &R, &P, &st)) {
+    const int64_t C = p->c_min + i;
+    if (!past && eval_candidate(m, p, (int32_t)C, &T, &R, &P, &st)) {
       T_num_out[i] = T;
     } else {
       if (st != MOE_OK) return st;
+      if (C >= 1) past = true;
       T_num_out[i] = -1;
     }
   }
   if (T_den_out) *T_den_out = m.rho_den;
-  return count;
+  return (int)count;
 }
 
 extern "C" int moe_select_candidate(const moe_workload_t* wl, const moe_select_params_t* p,
