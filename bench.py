@@ -13,7 +13,7 @@ Also measured, in the same run:
   * a trace of one launch (per-tile and per-task timestamps) giving the
     GEMM-portion TFLOP/s and the combine GB/s;
   * the selector sweep: 12 workloads (T in 4096..32768 x uniform / Zipf 0.8 /
-    Zipf 1.2 on the same shapes), every consumer count C = 0..64 timed, and
+    Zipf 1.2 on the same shapes), every consumer count C = 0..80 timed, and
     the selector's pick compared with the best (regret);
   * the CPU oracle on the same workload (the CPU baseline).
 """
@@ -277,14 +277,14 @@ class SweepPoint:
         self.pick_bands = (r, 2, L)
 
 
-def run_sweep(B, torch, samples, warmups, repeats=2, c_max=64):
+def run_sweep(B, torch, samples, warmups, repeats=2, c_max=80):
     """The selector sweep: the 12 workloads x C = 0..c_max (owner-write,
     column splits, as the selector's launch uses), every C timed `samples`
     times (ABBA) after `warmups` passes; the whole sweep is repeated
     `repeats` times (independent passes, the second over the workloads in
     reverse order).  Regret = (t(pick) - t(best)) / t(best) on medians, for
-    the library's candidate set 0..64 and for the paper's 1..64 (against
-    the best in 1..64).  Also the token-band consumer over a grid of (C, L)
+    the library's candidate set 0..80 and for the paper's 1..80 (against
+    the best in 1..80).  Also the token-band consumer over a grid of (C, L)
     with the selector's joint (C, L) pick."""
     from workloads import sweep_workloads
     names = [n for n, _ in sweep_workloads()]
@@ -329,13 +329,13 @@ def run_sweep(B, torch, samples, warmups, repeats=2, c_max=64):
             f = lambda k: [round(x, 1) for x in st[k]]   # noqa: E731
             row[f"s{ri + 1}"] = {
                 "best": [best] + f(best), "pick": [pt.pick] + f(pt.pick), "regret": round(r, 4),
-                "best_1_64": [best_dom] + f(best_dom),
+                "best_paper_set": [best_dom] + f(best_dom),
                 "pick_paper": [pt.pick_paper] + f(pt.pick_paper), "regret_paper": round(rp, 4),
                 "regret_estimate": round(re, 4),
                 "bands_best": [best_b[0], best_b[2]] + f(best_b),
                 "bands_pick": [pt.pick_bands[0], pt.pick_bands[2]] + f(pt.pick_bands),
                 "regret_bands": round(rb, 4),
-                "c0_vs_best_1_64": round(st[0][0] / st[best_dom][0], 4)}
+                "c0_vs_best_paper_set": round(st[0][0] / st[best_dom][0], 4)}
         rows.append(row)
 
     def by_rep(key):
@@ -380,9 +380,9 @@ def model_validation(B, torch, points, runs, Cs):
         rank_m = np.argsort(np.argsort([meas[c] for c in dom]))
         rho_s = float(np.corrcoef(rank_p, rank_m)[0, 1])
         out.append({"w": pt.name, "tile_us": round(t_tile, 2),
-                    "mape_1_64": round(float(np.mean([abs(errs[c]) for c in dom])), 4),
+                    "mape_paper_set": round(float(np.mean([abs(errs[c]) for c in dom])), 4),
                     "err_C0": round(errs[0], 4), "err_C16": round(errs[16], 4),
-                    "err_C64": round(errs[64], 4), "spearman_1_64": round(rho_s, 4),
+                    "err_C64": round(errs[64], 4), "spearman_paper_set": round(rho_s, 4),
                     "pred_over_meas_T0_T64": round((pred[0] / pred[64]) / (meas[0] / meas[64]), 4)})
     splits = []
     for pt in points:
@@ -410,9 +410,9 @@ def model_validation(B, torch, points, runs, Cs):
                            "F_us_meas": [round(x, 1) for x in F],
                            "F_us_model": [round(f / den * t_tile, 1) for f in F_m]})
     return {"per_workload": out,
-            "mape_1_64_mean": round(float(np.mean([o["mape_1_64"] for o in out])), 4),
+            "mape_paper_set_mean": round(float(np.mean([o["mape_paper_set"] for o in out])), 4),
             "err_C0_mean": round(float(np.mean([o["err_C0"] for o in out])), 4),
-            "spearman_1_64_mean": round(float(np.mean([o["spearman_1_64"] for o in out])), 4),
+            "spearman_paper_set_mean": round(float(np.mean([o["spearman_paper_set"] for o in out])), 4),
             "split_times": splits}
 
 
@@ -457,9 +457,9 @@ def rho_validation(B, torch, reps=5, C_ref=32):
 
 
 def saturation(B, torch, samples, warmups, name="sweep_T16384_uniform"):
-    """C past the paper-set bound of 64 on a workload whose time still falls
-    at C = 64: where does T(C) stop falling (the one-time saturation
-    characterisation that sets C_max)?"""
+    """The one-time saturation characterisation that sets C_max
+    (eq:c-domain): C = 32..192 on a workload whose time still falls at
+    C = 64; where does T(C) stop falling?"""
     pt = SweepPoint(name, B, torch)
     Cs = [32, 48, 56, 64, 72, 80, 96, 112, 128, 160, 192]
     t = time_configs(lambda c: pt.dw.run(c), Cs, samples, warmups, torch)
@@ -791,7 +791,7 @@ def main():
         del points
         torch.cuda.empty_cache()
         if not args.no_validate:
-            log("C past 64")
+            log("C saturation")
             res["c_max_saturation"] = saturation(B, torch, args.sweep_samples,
                                                  args.sweep_warmups)
             log("rho across the configurations")

@@ -2050,6 +2050,12 @@ constexpr int64_t kRhoBandsDen = 100;
 constexpr int64_t kSplitCostBandsNum = 43;
 constexpr int64_t kSplitCostBandsDen = 100;
 constexpr int kDefaultFixedC = 8;
+// C_max (eq:c-domain) from the kernel's saturation characterization: with
+// T = 16384, H = 2048, I = 704, E = 32, top-6, uniform routing, L = 2, the
+// launch takes 454 / 447 / 445 / 454 / 475 us at C = 64 / 72 / 80 / 96 /
+// 112 (three runs alike): past 80, more consumers take compute CUs without
+// shortening the combine.
+constexpr int kCMax = 80;
 
 // Selector parameters of a launch.  comm_tm is the owner-write task's token
 // count; rho_ref, calibrated for kCommTM-token tasks, scales with it (a
@@ -2071,7 +2077,7 @@ void fill_params(const DevInfo& d, int mode, int topk, int comm_tm, moe_select_p
   // C = 0 (every workgroup computes, then every workgroup consumes) is a
   // legal launch of this kernel, so it is part of the candidate set.
   p->c_min = 0;
-  p->c_max = 64;
+  p->c_max = kCMax;
   p->groups = 1;
   p->rho_ref_num = mode == 1 ? kRhoScatterNum : mode == 2 ? kRhoBandsNum : kRhoRefNum;
   p->rho_ref_den = mode == 1 ? kRhoScatterDen : mode == 2 ? kRhoBandsDen : kRhoRefDen;
