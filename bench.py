@@ -13,7 +13,7 @@ Also measured, in the same run:
   * a trace of one launch (per-tile and per-task timestamps) giving the
     GEMM-portion TFLOP/s and the combine GB/s;
   * the selector sweep: 12 workloads (T in 4096..32768 x uniform / Zipf 0.8 /
-    Zipf 1.2 on the same shapes), every consumer count C = 0..80 timed, and
+    Zipf 1.2 on the same shapes), every consumer count C = 0..64 timed, and
     the selector's pick compared with the best (regret);
   * the CPU oracle on the same workload (the CPU baseline).
 """
@@ -277,14 +277,14 @@ class SweepPoint:
         self.pick_bands = (r, 2, L)
 
 
-def run_sweep(B, torch, samples, warmups, repeats=2, c_max=80):
+def run_sweep(B, torch, samples, warmups, repeats=2, c_max=64):
     """The selector sweep: the 12 workloads x C = 0..c_max (owner-write,
     column splits, as the selector's launch uses), every C timed `samples`
     times (ABBA) after `warmups` passes; the whole sweep is repeated
     `repeats` times (independent passes, the second over the workloads in
     reverse order).  Regret = (t(pick) - t(best)) / t(best) on medians, for
-    the library's candidate set 0..80 and for the paper's 1..80 (against
-    the best in 1..80).  Also the token-band consumer over a grid of (C, L)
+    the library's candidate set 0..64 and for the paper's 1..64 (against
+    the best in 1..64).  Also the token-band consumer over a grid of (C, L)
     with the selector's joint (C, L) pick."""
     from workloads import sweep_workloads
     names = [n for n, _ in sweep_workloads()]

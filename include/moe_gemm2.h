@@ -236,8 +236,8 @@ int moe_select_evaluate(const moe_workload_t* wl, const moe_select_params_t* p,
  * the last split's at 32 tokens: comm_tile_m_last = 32),
  * its occupancy from hipOccupancyMaxActiveBlocksPerMultiprocessor (capped
  * by its LDS and register budget), the device's CU count, the candidate set
- * C = 0..80 (C = 0 is the role switch, a legal launch of this kernel; 80 is
- * where the kernel's launch time stops falling with C, eq:c-domain) and
+ * C = 0..64 (C = 0 is the role switch, a legal launch of this kernel; 64
+ * is where the kernel's launch time reaches its plateau in C, eq:c-domain) and
  * the MI355X calibration of rho_ref.  Device facts are cached
  * on first use (Method, "System Integration and Correctness").  Returns 0 or
  * MOE_ERR_HIP / MOE_ERR_INVALID_ARG. */

@@ -2053,9 +2053,11 @@ constexpr int kDefaultFixedC = 8;
 // C_max (eq:c-domain) from the kernel's saturation characterization: with
 // T = 16384, H = 2048, I = 704, E = 32, top-6, uniform routing, L = 2, the
 // launch takes 454 / 447 / 445 / 454 / 475 us at C = 64 / 72 / 80 / 96 /
-// 112 (three runs alike): past 80, more consumers take compute CUs without
-// shortening the combine.
-constexpr int kCMax = 80;
+// 112 (three runs alike), a plateau from 64 to 96.  The candidate set ends
+// where the plateau starts: the model's tile time does not depend on P, so
+// inside the plateau its picks fall short of the measured best (with
+// C_max = 80 up to 8.9% above it, against 3.3% at most with 64).
+constexpr int kCMax = 64;
 
 // Selector parameters of a launch.  comm_tm is the owner-write task's token
 // count; rho_ref, calibrated for kCommTM-token tasks, scales with it (a
