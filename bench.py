@@ -130,6 +130,23 @@ class DevWorkload:
         return used, tiles, tasks
 
 
+def settle(dw, C, torch, ms=60.0, chunk=16):
+    """Back-to-back launches (untimed) for `ms` of wall time before the
+    warm-up: after an idle period the GPU's first ~15 ms of sustained load
+    run slow (on the DeepSeek-V2-Lite-like share the first ~40 launches
+    5-10% above the steady state), so the timed steps would otherwise
+    measure the clock's ramp rather than the stage.  Returns the launches."""
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        for _ in range(chunk):
+            dw.run(C)
+        n += chunk
+        torch.cuda.synchronize()
+        if (time.perf_counter() - t0) * 1e3 >= ms:
+            return n
+
+
 def breakdown(dw, C, mode=None, reps=5):
     """GEMM portion and combine from traced launches: the launch with the
     median GEMM span out of `reps` (each after a short pause, so that one
@@ -639,17 +656,11 @@ def main():
         return
     stream = torch.cuda.current_stream()
 
-    log("warmup")
-    C_used = dw.run(args.consumers)
-    for _ in range(args.warmup):
-        dw.run(args.consumers)
-    torch.cuda.synchronize()
-    st = dw.ws.status()
-    assert st == 0, B.strerror(st)
-
     # selector cost on the host (pure C++, no HIP calls), 10^5 calls through
     # ctypes; the same loop around a call that does nothing (the ABI version)
-    # gives the ctypes overhead, which the net figure leaves out
+    # gives the ctypes overhead, which the net figure leaves out.  Measured
+    # before the launches, so that no idle gap separates the warm-up from the
+    # timed steps.
     params = B.launch_params(dw.wl)
     L_ = B.lib()
     nsel = 100000
@@ -664,9 +675,15 @@ def main():
         nop_fn()
     nop_us = (time.perf_counter() - t0) / nsel * 1e6
 
-    log(f"timing {args.steps} steps, C={C_used}")
+    log("settle")
+    C_used = dw.run(args.consumers)
+    settle_n = settle(dw, args.consumers, torch)
+    log("warmup")
+    for _ in range(args.warmup):
+        dw.run(args.consumers)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    log(f"timing {args.steps} steps, C={C_used}")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -675,6 +692,8 @@ def main():
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    st = dw.ws.status()
+    assert st == 0, B.strerror(st)
     ker_ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
     ms_per_step = wall * 1e3 / args.steps
     ker_avg_s = float(ker_ms.mean()) / 1e3
@@ -738,6 +757,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_launches": settle_n,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
