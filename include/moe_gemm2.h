@@ -233,7 +233,7 @@ int moe_select_evaluate(const moe_workload_t* wl, const moe_select_params_t* p,
 
 /* Parameters for the fused kernel on a HIP device: its tile shapes (the
  * owner-write consumer task at its full size of 64 tokens x 1024 columns,
- * the last split's at 32 tokens: comm_tile_m_last = 32),
+ * the last split's at 16 tokens: comm_tile_m_last = 16),
  * its occupancy from hipOccupancyMaxActiveBlocksPerMultiprocessor (capped
  * by its LDS and register budget), the device's CU count, the candidate set
  * C = 0..64 (C = 0 is the role switch, a legal launch of this kernel; 64
@@ -267,7 +267,7 @@ int moe_gemm2_default_params_ex(int device, int32_t mode, int32_t topk, moe_sele
  * ceil(H/splits/1024)), so that a small batch's combine still spreads over
  * every CU; comm_tile_m = TM and rho_ref, calibrated for 64-token tasks, is
  * scaled by TM/64 (a task's bytes are proportional to its tokens); the last
- * split's tasks take TM_last = TM/2 tokens when TM > 16 (else TM), so that
+ * split's tasks take TM_last = max(16, TM/4) tokens (at most TM), so that
  * the launch ends evenly over the CUs: comm_tile_m_last = TM_last.  Mode 1:
  * as moe_gemm2_default_params_ex(device, 1, wl->topk).  Mode 2: tasks of
  * TM tokens x min(1024, H) columns of the full width, TM = 64 halved down

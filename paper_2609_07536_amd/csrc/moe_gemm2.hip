@@ -1913,7 +1913,12 @@ struct Layout {
 inline size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // Tokens of the last split's owner-write tasks for tasks of comm_tm tokens.
-inline int last_split_tm(int comm_tm) { return comm_tm > kCommTMMin ? comm_tm / 2 : comm_tm; }
+// The last split's task: a quarter of the others' tokens, at least
+// kCommTMMin (and never more than the others').
+inline int last_split_tm(int comm_tm) {
+  const int q = comm_tm / 4 > kCommTMMin ? comm_tm / 4 : kCommTMMin;
+  return q < comm_tm ? q : comm_tm;
+}
 
 int check_shape(const moe_workload_t* wl) {
   if (!wl) return MOE_ERR_INVALID_ARG;
@@ -1953,9 +1958,9 @@ bool make_layout(const moe_workload_t* wl, Layout* L) {
              kTaskTarget)
     L->comm_tm /= 2;
   L->tasks_per_split = ((wl->T + L->comm_tm - 1) / L->comm_tm) * L->cb_per_split;
-  // The last split's tasks take half the tokens (down to kCommTMMin): they
-  // start only after the last tiles, so finer tasks end the launch more
-  // evenly over the CUs.
+  // The last split's tasks take a quarter of the tokens (down to
+  // kCommTMMin): they start only after the last tiles, so finer tasks end
+  // the launch more evenly over the CUs.
   L->comm_tm_last = last_split_tm(L->comm_tm);
   L->tasks_last = ((wl->T + L->comm_tm_last - 1) / L->comm_tm_last) * L->cb_per_split;
   L->max_tiles = (long long)wl->splits * L->ntps * ((L->rows + kBM - 1) / kBM + wl->E);
@@ -2030,10 +2035,10 @@ int device_info(int dev, DevInfo* out) {
 // rho_ref of the fused kernel on MI355X: mean consumer-task time over mean
 // compute-tile time (one consumer wave over one compute wave), measured with
 // the traced entry point at the reference configuration (T=16384, H=2048,
-// I=704, E=32, top-6, L=2, C=32, 64-token tasks; the last split's 32-token
-// tasks counted at twice their time): 27.9 us / 19.4 us = 1.44 (three runs:
-// 1.436 to 1.445).  MOE_GEMM2_RHO_REF="num/den" overrides it.
-constexpr int64_t kRhoRefNum = 144;
+// I=704, E=32, top-6, L=2, C=32, 64-token tasks; the last split's 16-token
+// tasks counted at four times their time): 30.4 us / 19.1 us = 1.59 (three
+// runs: 1.576 to 1.598).  MOE_GEMM2_RHO_REF="num/den" overrides it.
+constexpr int64_t kRhoRefNum = 159;
 constexpr int64_t kRhoRefDen = 100;
 // The same ratio for the atomic scatter (one task = one compute tile's
 // rows), measured the same way: 26.2 us / 21.5 us = 1.22.

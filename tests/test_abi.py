@@ -504,7 +504,7 @@ def test_trace_size_counts_the_adaptive_consumer_tasks(T, H, L, tm):
     wl, _ = B.make_workload(T=T, H=H, I=I, E=E, topk=k, splits=L)
     rows = T * k
     max_tiles = L * -(-(H // L) // 256) * (-(-rows // 256) + E)
-    tm_last = tm // 2 if tm > 16 else tm     # the last split's tasks are cut finer
+    tm_last = min(tm, max(16, tm // 4))      # the last split's tasks are cut finer
     cb = -(-(H // L) // 1024)
     tasks = (L - 1) * -(-T // tm) * cb + -(-T // tm_last) * cb
     assert B.trace_size(wl) == 8 * (4 * max_tiles + 4 * max(tasks, max_tiles))

@@ -49,7 +49,7 @@ def driver(tmp_path_factory):
 
 def _params(**kw):
     p = dict(tile_m=256, tile_n=256, comm_tile_m=64, comm_tile_n=1024, occ_comp=1, occ_comm=1,
-             num_cus=256, c_min=0, c_max=64, groups=1, rho_ref_num=144, rho_ref_den=100,
+             num_cus=256, c_min=0, c_max=64, groups=1, rho_ref_num=159, rho_ref_den=100,
              k_ref=704, tile_m_ref=256, tile_n_ref=256, d_ref=1, split_axis=0, drain=0,
              rho_kh=0, topk_ref=6, comm_tile_n_ref=1024, readiness=0, comm_tile_m_last=0,
              split_cost_num=0, split_cost_den=1)
