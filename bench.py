@@ -130,21 +130,28 @@ class DevWorkload:
         return used, tiles, tasks
 
 
-def settle(dw, C, torch, ms=60.0, chunk=16):
-    """Back-to-back launches (untimed) for `ms` of wall time before the
-    warm-up: after an idle period the GPU's first ~15 ms of sustained load
-    run slow (on the DeepSeek-V2-Lite-like share the first ~40 launches
-    5-10% above the steady state), so the timed steps would otherwise
-    measure the clock's ramp rather than the stage.  Returns the launches."""
+def settle_calls(fns, torch, ms=60.0, rounds=4):
+    """Untimed back-to-back calls of `fns` (in turn, `rounds` each between
+    synchronisations) for `ms` of wall time: after an idle period the GPU's
+    first ~15 ms of sustained load run slow (on the DeepSeek-V2-Lite-like
+    share the first ~40 launches 5-10% above the steady state), so timed
+    launches right after one would measure the clock's ramp rather than
+    the kernels.  Returns the number of calls."""
     n = 0
     t0 = time.perf_counter()
     while True:
-        for _ in range(chunk):
-            dw.run(C)
-        n += chunk
+        for _ in range(rounds):
+            for f in fns:
+                f()
+                n += 1
         torch.cuda.synchronize()
         if (time.perf_counter() - t0) * 1e3 >= ms:
             return n
+
+
+def settle(dw, C, torch, ms=60.0):
+    """The settle phase before the timed steps (see settle_calls)."""
+    return settle_calls([lambda: dw.run(C)], torch, ms, rounds=16)
 
 
 def breakdown(dw, C, mode=None, reps=5):
@@ -222,12 +229,14 @@ def launch_cfg(dw, c):
 
 
 def time_configs(launch, keys, samples, warmups, torch):
-    """Event time (us) of every key, `samples` times each: `warmups`
-    untimed passes over all keys, then passes alternately forward and
-    backward over the keys (ABBA), one stream synchronisation per pass.
-    Each pass starts with an untimed launch of its first key, so that no
-    timed launch starts on a GPU left idle by the synchronisation."""
+    """Event time (us) of every key, `samples` times each: a settle phase
+    (settle_calls) and `warmups` untimed passes over all keys, then passes
+    alternately forward and backward over the keys (ABBA), one stream
+    synchronisation per pass.  Each pass starts with an untimed launch of
+    its first key, so that no timed launch starts on a GPU left idle by the
+    synchronisation."""
     stream = torch.cuda.current_stream()
+    settle_calls([lambda k=k: launch(k) for k in keys], torch, rounds=1)
     for _ in range(warmups):
         for k in keys:
             launch(k)
@@ -513,9 +522,7 @@ def layer_measure(dw, B, torch, samples=20):
                         counts=w.counts, out=out, workspace=lws)
 
     fns = {"gemm1": gemm1, "layer": layer, "stage": lambda: dw.run(-1)}
-    for f in fns.values():
-        f()
-    torch.cuda.synchronize()
+    settle_calls(list(fns.values()), torch, rounds=1)
     stream = torch.cuda.current_stream()
     times = {k: [] for k in fns}
     keys = list(fns)
